@@ -1,0 +1,244 @@
+"""Benchmark of the whole Chameleon quantized-linear hot path on one MI355X.
+
+Workload: the SDXL-like 1280-wide transformer-block linear set at 1024 px with CFG batch 2 --
+M = 2048 tokens through QKV 1280->3840, out-proj 1280->1280, GEGLU 1280->10240 and FF-out
+5120->1280.  Weights are W4 with per-channel formats (heterogeneous synthetic rows);
+activations are A8 in the format a lookup table built for B = 4 timestep buckets from
+kurtosis and SNR (scaled-linear schedule 0.00085 -> 0.012, T = 1000) assigns.
+
+One step = one pass of every step of the path over one batch, all inputs resident in HBM:
+  select_weight_formats (4 layers) -> act_stats_accumulate (4 layer inputs) ->
+  build_act_lut -> quantize_act_lut (4) -> mixed_linear (4).
+
+Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step time (GEMM
+flops / step time; the search, statistics, LUT and quantization count against it).  The
+`roofline` object is for the dominant kernel (the mixed-format GEMM), timed with HIP events
+on the launch stream over the timed steps; the weight search's own HBM rate is reported
+beside it.  `cpu_baseline` times the CPU oracle on a bounded sample of the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+F16_PEAK_TFLOPS = 2500.0   # dense f16/bf16 MFMA
+T_SCHED = 1000
+B_BUCKETS = 4
+M_TOKENS = 2048
+D = 1280
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--t", type=int, default=375, help="timestep of the benchmarked batch")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    return p.parse_args()
+
+
+def search_bytes_per_weight(K: int) -> float:
+    """Algorithmic bytes of the W4 search per weight: 4 B read + 0.5 B codes + the block
+    metadata written for every channel (NF4 absmax 4 B / 64, E8M0 1 B / 32) + 14 B per
+    channel (format, scale, zero, perm, amortized over K)."""
+    return 4.0 + 0.5 + 4.0 / 64 + 1.0 / 32 + 14.0 / K
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only (this build has no multi-GPU path); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import __graft_entry__
+    from paper_2609_33496_amd import cham, synth
+
+    if not os.path.exists(cham.LIB_PATH):
+        __graft_entry__.build()
+    L = cham.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    S = ctypes.c_void_p(stream.cuda_stream)
+
+    layers = synth.sdxl_block_layers(D)
+    # ---- inputs (synthetic, resident in HBM before timing)
+    Ws, Xs = [], []
+    for li, (name, K, N) in enumerate(layers):
+        W, _ = synth.hetero_weights(100 + li, N, K)
+        Ws.append(torch.from_numpy(W).to(dev))
+        Xs.append(torch.from_numpy(synth.diffusion_acts(0, li, args.t, M_TOKENS, K)).to(dev))
+    wqs = [cham.alloc_wq(N, K, cham.MASK_W4, dev, want_perm=True) for (_, K, N) in layers]
+    aqs = [cham.alloc_aq(M_TOKENS, K, dev) for (_, K, N) in layers]
+    Ys = [torch.empty((M_TOKENS, N), dtype=torch.float32, device=dev) for (_, K, N) in layers]
+    stats = cham.alloc_stats(len(layers), B_BUCKETS, dev)
+    cham.act_stats_reset(stats)
+    # calibration pre-pass: two batches per bucket at the bucket's timesteps (setup, untimed)
+    for b in range(B_BUCKETS):
+        for i in range(2):
+            t = b * T_SCHED // B_BUCKETS + (2 * i + 1) * T_SCHED // (4 * B_BUCKETS)
+            for li, (_, K, _) in enumerate(layers):
+                x = torch.from_numpy(synth.diffusion_acts(1, li, t, 512, K)).to(dev)
+                cham.act_stats_accumulate(x, li, b, stats)
+    sched = cham.Schedule(T=T_SCHED)
+    lut = cham.build_act_lut(stats, sched, want_kappa=True)
+    lut.mirror()
+    bucket = cham.bucket(args.t, T_SCHED, B_BUCKETS)
+
+    # prepared C structs and workspaces (the step issues raw C-ABI calls)
+    ws_stats = [torch.empty(max(cham.workspace_bytes(cham.OP_STATS, X.numel(), 0, 0), 256), dtype=torch.uint8,
+                            device=dev) for X in Xs]
+    ws_q = [torch.empty(max(cham.workspace_bytes(cham.OP_QUANT_ACT, M_TOKENS, 0, X.shape[1]), 256),
+                        dtype=torch.uint8, device=dev) for X in Xs]
+    wq_s = [w.struct() for w in wqs]
+    st_s = stats.struct()
+    sc_s = sched.struct()
+    lut_s = lut.struct()
+    aq_s = [a.struct() for a in aqs]
+    Fh = ctypes.c_void_p(lut.F_host.data_ptr())
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+
+    ev = {k: [] for k in ("search", "gemm")}
+
+    def step(record=False):
+        e0 = e1 = None
+        if record:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+        for li in range(len(layers)):
+            rc = L.cham_select_weight_formats(P(Ws[li]), ctypes.byref(wq_s[li]), S)
+            assert rc == 0, rc
+        if record:
+            e1 = torch.cuda.Event(enable_timing=True)
+            e1.record(stream)
+            ev["search"].append((e0, e1))
+        for li in range(len(layers)):
+            rc = L.cham_act_stats_accumulate(P(Xs[li]), Xs[li].numel(), li, bucket, ctypes.byref(st_s),
+                                             P(ws_stats[li]), ws_stats[li].numel(), S)
+            assert rc == 0, rc
+        rc = L.cham_build_act_lut(ctypes.byref(st_s), ctypes.byref(sc_s), None, ctypes.byref(lut_s), None, S)
+        assert rc == 0, rc
+        for li in range(len(layers)):
+            rc = L.cham_quantize_act_lut(P(Xs[li]), ctypes.byref(lut_s), Fh, li, args.t, 0, ctypes.byref(aq_s[li]),
+                                         P(ws_q[li]), ws_q[li].numel(), S)
+            assert rc == 0, rc
+        if record:
+            e2 = torch.cuda.Event(enable_timing=True)
+            e2.record(stream)
+        for li in range(len(layers)):
+            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), None, 0, S)
+            assert rc == 0, rc
+        if record:
+            e3 = torch.cuda.Event(enable_timing=True)
+            e3.record(stream)
+            ev["gemm"].append((e2, e3))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        step(record=True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+    ms_search = float(np.mean([a.elapsed_time(b) for a, b in ev["search"]]))
+    ms_gemm = float(np.mean([a.elapsed_time(b) for a, b in ev["gemm"]]))
+
+    flops = sum(2.0 * M_TOKENS * N * K for (_, K, N) in layers)
+    sbytes = sum(N * K * search_bytes_per_weight(K) for (_, K, N) in layers)
+    gemm_tflops = flops / (ms_gemm * 1e-3) / 1e12
+    value = flops / (ms_step * 1e-3) / 1e12
+    search_gbps = sbytes / (ms_search * 1e-3) / 1e9
+
+    fmts = [int(lut.F_host[li * B_BUCKETS + bucket]) for li in range(len(layers))]
+    hist = np.bincount(torch.cat([w.fmt for w in wqs]).cpu().numpy(), minlength=9)
+    out = {
+        "metric": "mixed_linear TFLOP/s + weight-search GB/s (frac of MI355X peak), 1 GPU",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16-mfma(fp32 acc); w4 codes, a8 codes",
+        "data": "synthetic (seeded hetero W4 rows; diffusion-mixture activations)",
+        "config": {"workload": "SDXL-like 1280-wide block linears, M=2048 (1024 tokens x CFG 2), W4 per-channel, "
+                               "A8 LUT B=4 scaled-linear T=1000",
+                   "layers": [f"{n} {k}->{nn}" for (n, k, nn) in layers], "timestep": args.t, "bucket": bucket,
+                   "act_formats": [cham.A_NAMES[f] for f in fmts],
+                   "weight_format_hist": {cham.W_NAMES[i]: int(hist[i]) for i in range(9) if hist[i]}},
+        "gemm_tflops": round(gemm_tflops, 3),
+        "gemm_ms": round(ms_gemm, 4),
+        "search_GBps": round(search_gbps, 2),
+        "search_frac_hbm": round(search_gbps / HBM_PEAK_GBPS, 4),
+        "search_ms": round(ms_search, 4),
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "gemm_f16_kernel (4 launches/step, flop-weighted)"},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(layers, Ws, Xs, fmts, args.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
+    """The CPU oracle (single-threaded C) on a bounded sample of the same step, scaled to
+    the step's GEMM-flop throughput: a sample of output channels is searched, a sample of
+    activation rows quantized and a sample of outputs computed; the per-layer times are
+    extrapolated to the full sizes."""
+    import oracle
+    per_layer = budget_s / len(layers)
+    total_s = 0.0
+    flops = 0.0
+    samples = []
+    for li, (name, K, N) in enumerate(layers):
+        W = Ws[li].cpu().numpy()
+        X = Xs[li].cpu().numpy()
+        nrows = max(8, min(N, int(per_layer * 0.4 * 4e6 / K)))
+        t = time.perf_counter()
+        wq = oracle.select_weight_formats(W[:nrows], oracle.MASK_W4, want_err=False, want_perm=False)
+        t_search = (time.perf_counter() - t) * N / nrows
+        mrows = max(4, min(X.shape[0], int(per_layer * 0.2 * 2e6 / K)))
+        t = time.perf_counter()
+        lo, hi = oracle.minmax(X)
+        s, z = oracle.scale_zp(act_fmts[li], lo, hi)
+        _, _, xh = oracle.quantize_act(X[:mrows], act_fmts[li], s, z, want_xhat=True)
+        t_q = (time.perf_counter() - t) * X.shape[0] / mrows
+        Wh = oracle.dequant_weights(wq, K)
+        npairs = max(64, int(per_layer * 0.3 * 2e8 / K))
+        g = np.random.default_rng(li)
+        mm = g.integers(0, mrows, npairs)
+        nn = g.integers(0, nrows, npairs)
+        t = time.perf_counter()
+        oracle.linear_pairs(xh, Wh, mm, nn)
+        t_g = (time.perf_counter() - t) * (X.shape[0] * N) / npairs
+        total_s += t_search + t_q + t_g
+        flops += 2.0 * X.shape[0] * N * K
+        samples.append(f"{name}: {nrows}/{N} channels searched, {mrows}/{X.shape[0]} rows quantized, "
+                       f"{npairs} outputs")
+    return {"value": round(flops / total_s / 1e12, 9), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": "; ".join(samples) + "; per-layer times extrapolated to full size (stats/LUT omitted)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,246 @@
+/*
+ * chameleon.h -- C ABI of the MI355X (gfx950) hot path of Chameleon's per-tensor,
+ * format-adaptive post-training quantization (arXiv 2609.33496, "Chameleon: Dynamic Format
+ * Adapter for Efficient Diffusion"): the quantized linear layer of a denoiser.
+ *
+ *   cham_select_weight_formats  offline per-output-channel weight-format search + packing
+ *                               (Sec. 4.5, Eq. weight-argmax; palettes of Sec. 4.2)
+ *   cham_act_stats_accumulate   calibration power sums and range per (layer, bucket)
+ *                               (Sec. 4.4; App. A.7, Alg. 1 first loop)
+ *   cham_build_act_lut          kurtosis + SNR routing + ScaleZP -> format/scale/zero LUT
+ *                               (Sec. 4.3; App. A.7, Alg. 1 second loop)
+ *   cham_quantize_act           activation quantization to the LUT's format, static
+ *                               (UNet path, Alg. 2) or dynamic per-tensor (DiT path, Alg. 3)
+ *   cham_mixed_linear           Y = dequant(X codes) . dequant(W codes)^T with per-channel
+ *                               weight formats (Sec. 6: same-format sub-GEMMs / weights
+ *                               dequantized in registers)
+ *
+ * Conventions shared by every call:
+ *   - Every pointer inside a descriptor or passed as a buffer is DEVICE memory unless its
+ *     comment says "host".  The caller owns every buffer; the library allocates nothing and
+ *     keeps no mutable global state.  Calls are thread-safe.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only enqueues work
+ *     on that stream and returns without synchronizing.
+ *   - Argument errors are detected on the host and returned synchronously before anything is
+ *     enqueued; launch errors are returned as CHAM_EHIP.  No exception crosses the ABI.
+ *   - Layouts are row-major.  W is [N][K] (C_out x C_in, as nn.Linear stores it), X is [M][K],
+ *     Y is [M][N].  MX blocks are 32 contiguous elements along K; NF4 blocks 64.
+ *   - Workspace: calls that take (ws, ws_bytes) need at least cham_workspace_bytes(op, ...)
+ *     bytes of device memory aligned to 256 bytes; its contents need not be initialized.
+ */
+#ifndef CHAMELEON_H_
+#define CHAMELEON_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------------------------------
+ * status codes
+ * ------------------------------------------------------------------------------------- */
+#define CHAM_OK 0
+#define CHAM_EINVAL (-1)     /* NULL pointer, negative or zero size, bad layer/bucket index  */
+#define CHAM_ESHAPE (-2)     /* K not a multiple of 32 (MX) / 64 (NF4) / 2 (4-bit packing)   */
+#define CHAM_EFORMAT (-3)    /* unknown format id, empty or out-of-range palette mask        */
+#define CHAM_EHIP (-4)       /* a HIP launch or runtime call failed                          */
+#define CHAM_EWORKSPACE (-5) /* ws NULL or smaller than cham_workspace_bytes()               */
+
+/* Human-readable message for a status code (static storage, never NULL). */
+const char* cham_status_string(int status);
+
+/* Library version as (major << 16) | (minor << 8) | patch. */
+int cham_version(void);
+
+/* ---------------------------------------------------------------------------------------
+ * number formats (Sec. 4.2)
+ * ------------------------------------------------------------------------------------- */
+/* Weight formats, in the paper's palette order F_w^(8) then F_w^(4).  palette_mask bit f
+ * enables format f. */
+#define CHAM_W_INT8_SYM 0
+#define CHAM_W_INT8_ASYM 1
+#define CHAM_W_MXINT8 2
+#define CHAM_W_INT4_SYM 3
+#define CHAM_W_INT4_ASYM 4
+#define CHAM_W_NF4 5
+#define CHAM_W_FP4 6
+#define CHAM_W_MXINT4 7
+#define CHAM_W_MXFP4 8
+#define CHAM_W_NFMT 9
+/* The few-step 4-bit search set {INT4-asym, NF4, FP4, MXINT4, MXFP4} and F_w^(8). */
+#define CHAM_MASK_W4 0x1F0u
+#define CHAM_MASK_W8 0x007u
+
+/* Activation formats = the runtime LUT codes 0..4. */
+#define CHAM_A_INT8_ASYM 0
+#define CHAM_A_FP8_E4M3 1
+#define CHAM_A_FP8_E5M2 2
+#define CHAM_A_MXFP8_E4M3 3
+#define CHAM_A_MXINT8 4
+#define CHAM_A_NFMT 5
+
+/* ---------------------------------------------------------------------------------------
+ * 1. per-output-channel weight-format search (Sec. 4.5, Eq. weight-argmax)
+ *
+ * For each output channel n, W[n][:] is round-tripped through every enabled format and the
+ * format with the smallest sum of squared reconstruction errors (= the largest SQNR; ties go
+ * to the lowest id) is kept, with its codes and metadata.  Quantizers (App. A.11, App. A.12):
+ *   INT-sym   s = amax/Q (Q = 127, 7), q = clamp(round(w/s), -Q, Q), w^ = q s
+ *   INT-asym  lo/hi widened to contain 0, s = (hi-lo)/L (L = 255, 15), z = round(-lo/s),
+ *             q = clamp(round(w/s) + z, 0, L), w^ = (q - z) s
+ *   FP4 E2M1  per channel s = amax/6, e = E2M1(clamp(w/s, +-6)), w^ = e s
+ *   NF4       per 64-block a = absmax, c = nearest NF4 level to w/a, w^ = v_c a
+ *   MXINT8/4  per 32-block E = floor(log2 amax), k = clamp(round(w 2^(F-E)), +-Q),
+ *             F = 6 / 2, Q = 127 / 7, w^ = k 2^(E-F)
+ *   MXFP4     per 32-block E = floor(log2 amax) - 2 (OCP MX v1.0), e = E2M1(clamp(w/2^E, +-6))
+ * "round" is half-to-even, w/s is computed as w * (1/s) in binary32, and every floating
+ * scale is floored at FLT_MIN; E8M0 exponents are clamped to [-127, 127] (all-zero block
+ * -> -127) and stored biased (E + 127).
+ * ------------------------------------------------------------------------------------- */
+typedef struct cham_wq {
+    int64_t N, K;           /* W is [N][K]; K > 0, even; K % 64 == 0 if NF4 enabled,
+                               K % 32 == 0 if any MX format enabled                          */
+    uint32_t palette_mask;  /* bit f enables format f; nonzero, bits >= 9 must be clear        */
+    int32_t code_bits;      /* 4 if every enabled format is 4-bit, else 8; filled in by
+                               cham_select_weight_formats (the caller may leave it 0)        */
+    uint8_t* fmt;           /* [N]      chosen format id per channel                          */
+    uint8_t* codes;         /* [N][K/2] two 4-bit codes per byte, even k in the low nibble
+                               (code_bits 4), or [N][K] one code per byte (code_bits 8).
+                               Codes: INT-sym, MXINT two's complement; INT-asym unsigned q;
+                               NF4 level index 0..15 (ascending); E2M1 sign|exp(2)|mantissa */
+    float* scale;           /* [N]      s of INT-sym/INT-asym/FP4 channels, 0 otherwise       */
+    int32_t* zero;          /* [N]      z of INT-asym channels, 0 otherwise                   */
+    float* nf4_absmax;      /* [N][K/64] block absmax of NF4 channels, 0 otherwise;
+                               may be NULL iff NF4 is not enabled                             */
+    uint8_t* e8m0;          /* [N][K/32] biased block exponent of MX channels, 0 otherwise;
+                               may be NULL iff no MX format is enabled                        */
+    int32_t* perm;          /* [N]      channels stably sorted by chosen format; NULL = skip   */
+    int32_t* group_off;     /* [10]     start of each format's group in perm, [9] = N;
+                               NULL = skip                                                    */
+    double* err;            /* [N][9]   per-format error sums (diagnostic, relative accuracy
+                               1e-5; -1 for disabled formats); NULL = skip                    */
+} cham_wq;
+
+/* Search the formats of W [N][K] (device, binary32, finite) and fill *wq's buffers.
+ * Ownership: the caller owns W and every buffer in *wq.  Errors: CHAM_EINVAL (NULL W/wq/
+ * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K), CHAM_EHIP. */
+int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream);
+
+/* ---------------------------------------------------------------------------------------
+ * 2. calibration statistics (Sec. 4.4; Alg. 1) and the LUT (Sec. 4.3; Alg. 1)
+ * ------------------------------------------------------------------------------------- */
+typedef struct cham_act_stats {
+    int32_t L, B;  /* layers, timestep buckets                                            */
+    double* nS;    /* [L*B][5] n, sum x, sum x^2, sum x^3, sum x^4 (binary64)               */
+    float* lohi;   /* [L*B][2] running min, max (binary32)                                 */
+} cham_act_stats;
+
+/* Set every accumulator to n = S_k = 0, lo = +inf, hi = -inf. */
+int cham_act_stats_reset(cham_act_stats* st, void* stream);
+
+/* Add one activation tensor X (numel binary32 values, device) of `layer` at a timestep of
+ * `bucket` into the accumulator: n += numel, S_k += sum x^k, lo/hi = min/max.  The sums are
+ * reduced in a fixed order (bitwise reproducible run to run).  ws: CHAM_OP_STATS bytes.
+ * Errors: CHAM_EINVAL (NULL, numel < 1, layer/bucket out of range), CHAM_EWORKSPACE, CHAM_EHIP. */
+int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t layer, int32_t bucket,
+                              cham_act_stats* st, void* ws, size_t ws_bytes, void* stream);
+
+#define CHAM_SCHED_SCALED_LINEAR 0
+#define CHAM_SCHED_LINEAR 1
+typedef struct cham_schedule {
+    int32_t T;                   /* diffusion steps (betas indexed 0..T-1)                    */
+    double beta0, beta1;         /* first and last beta                                        */
+    int32_t kind;                /* CHAM_SCHED_SCALED_LINEAR: (sqrt(b0)+(sqrt(b1)-sqrt(b0))s/(T-1))^2
+                                    CHAM_SCHED_LINEAR:        b0 + (b1-b0) s/(T-1)             */
+    double kappa_lo, kappa_hi;   /* kurtosis gates (3, 5)                                      */
+    double snr_lo, snr_hi;       /* SNR gates (0.2, 2.0)                                       */
+    int32_t snr_gate_on;         /* 0 routes by kurtosis alone                                 */
+} cham_schedule;
+
+/* SDXL's scaled-linear schedule 0.00085 -> 0.012, T = 1000, gates (3, 5, 0.2, 2.0), on. */
+void cham_schedule_default(cham_schedule* s);
+
+typedef struct cham_lut {
+    int32_t L, B, T;  /* layers, buckets, schedule length                                  */
+    uint8_t* F;       /* [L*B] format code 0..4                                             */
+    float* S;         /* [L*B] scale                                                        */
+    float* Z;         /* [L*B] zero point (integral, binary32)                              */
+} cham_lut;
+
+/* For every (l, b): kappa = m4/m2^2 from the power sums; SNR at the bucket midpoint
+ * t_b = floor(b T/B + T/(2B)) with alpha_bar_t = prod_{s<=t} (1 - beta_s) and
+ * SNR = alpha_bar/(1 - alpha_bar) (Sec. 3.1, Eq. snr); Route (Sec. 4.3): shortcut -> 3,
+ * kappa > hi or SNR < lo -> 2, kappa <= lo and SNR > hi -> 0, else 1; ScaleZP (App. A.7) on
+ * the bucket's [lo, hi] (an empty bucket gets S = 1, Z = 0).  is_shortcut: device [L] or
+ * NULL.  kappa: device [L*B] binary64 or NULL.  lut->L, B must equal st's; lut->T = sch->T.
+ * Errors: CHAM_EINVAL, CHAM_EHIP. */
+int cham_build_act_lut(const cham_act_stats* st, const cham_schedule* sch,
+                       const uint8_t* is_shortcut, cham_lut* lut, double* kappa, void* stream);
+
+/* Bucket of timestep t (Alg. 2): min(floor(t B / T), B - 1); -1 if t < 0 or T, B < 1. */
+int32_t cham_bucket(int32_t t, int32_t T, int32_t B);
+
+/* ---------------------------------------------------------------------------------------
+ * 3. activation quantization (Alg. 2 static / Alg. 3 dynamic)
+ * ------------------------------------------------------------------------------------- */
+typedef struct cham_aq {
+    int64_t M, K;     /* X is [M][K]                                                         */
+    int32_t fmt;      /* activation format used (filled in by the quantize call)              */
+    uint8_t* codes;   /* [M][K] INT8-asym unsigned q, FP8 / MXFP8 codes, MXINT8 two's compl.  */
+    uint8_t* e8m0;    /* [M][K/32] biased block exponents (MX formats; may be NULL otherwise) */
+    float* scale;     /* [1] the scale s used (1 for MX formats)                              */
+    float* zero;      /* [1] the zero point z used (0 unless INT8-asym)                       */
+} cham_aq;
+
+/* Quantize X [M][K] (device, finite binary32) to activation format `fmt`:
+ *   INT8-asym  q = clamp(round(x/s) + z, 0, 255)
+ *   FP8        e = E4M3 / E5M2(clamp(x/s, +-448 / +-57344)), round to nearest even
+ *   MXFP8      per 32-block E = floor(log2 amax) (the paper's exponent: values in (-2, 2)),
+ *              e = E4M3(x / 2^E)
+ *   MXINT8     per 32-block E = floor(log2 amax), k = clamp(round(x 2^(6-E)), +-127)
+ * Static (dynamic = 0): s = *s_dev, z = *z_dev (device pointers, e.g. LUT entries).
+ * Dynamic (dynamic = 1): (s, z) = ScaleZP(fmt, min X, max X) of this tensor; s_dev/z_dev
+ * are ignored.  The (s, z) used are written to out->scale / out->zero.  ws: CHAM_OP_QUANT_ACT
+ * bytes.  Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE (K % 32 for MX), CHAM_EWORKSPACE,
+ * CHAM_EHIP. */
+int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev,
+                      const float* z_dev, cham_aq* out, void* ws, size_t ws_bytes, void* stream);
+
+/* The per-step runtime lookup of Alg. 2 / Alg. 3: b = cham_bucket(t, lut->T, lut->B), the
+ * format is F_host[layer*B + b] (a host mirror of lut->F, copied once after calibration, so
+ * no device synchronization is needed per step), and the scale/zero are read on the device
+ * from lut->S/Z[layer*B + b] (static) or computed from X (dynamic). */
+int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_host,
+                          int32_t layer, int32_t t, int32_t dynamic, cham_aq* out, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------------------
+ * 4. the mixed-format linear layer
+ *
+ * Y[m][n] = sum_k x^[m][k] w^[n][k], with x^ = DQ(xq) and w^ = DQ(wq) exactly as the
+ * quantizers above define them, accumulated in binary32 on the matrix cores.  Accuracy:
+ * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element (NF4 levels are carried at half
+ * precision; every other operand is exact).  xq->K must equal wq->K.  Y is written in the
+ * original channel order.  ws: CHAM_OP_LINEAR bytes.
+ * Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE, CHAM_EWORKSPACE, CHAM_EHIP.
+ * ------------------------------------------------------------------------------------- */
+int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* ---------------------------------------------------------------------------------------
+ * workspace sizes
+ * ------------------------------------------------------------------------------------- */
+#define CHAM_OP_SELECT 0
+#define CHAM_OP_STATS 1
+#define CHAM_OP_QUANT_ACT 2
+#define CHAM_OP_LINEAR 3
+/* Bytes of workspace op needs at these sizes (M rows of X / numel for CHAM_OP_STATS in M;
+ * N output channels; K inner size).  0 means no workspace. */
+size_t cham_workspace_bytes(int32_t op, int64_t M, int64_t N, int64_t K);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CHAMELEON_H_ */

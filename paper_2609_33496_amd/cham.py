@@ -1,0 +1,364 @@
+"""Thin Python binding of the HIP library's C ABI (``include/chameleon.h``).
+
+Argument marshalling only: torch tensors supply device memory and the current HIP stream;
+every step of the computation runs in the library's kernels.  There is no fallback: if the
+shared library is missing or a call fails, an exception is raised.
+
+Functions keep the C names without the ``cham_`` prefix:
+``select_weight_formats``, ``act_stats_reset``, ``act_stats_accumulate``,
+``build_act_lut``, ``quantize_act``, ``quantize_act_lut``, ``mixed_linear``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libchameleon.so")
+
+# status codes
+OK, EINVAL, ESHAPE, EFORMAT, EHIP, EWORKSPACE = 0, -1, -2, -3, -4, -5
+# weight formats (palette order) and masks
+W_INT8_SYM, W_INT8_ASYM, W_MXINT8, W_INT4_SYM, W_INT4_ASYM, W_NF4, W_FP4, W_MXINT4, W_MXFP4 = range(9)
+W_NAMES = ["INT8-sym", "INT8-asym", "MXINT8", "INT4-sym", "INT4-asym", "NF4", "FP4", "MXINT4", "MXFP4"]
+MASK_W4 = 0x1F0
+MASK_W8 = 0x007
+# activation formats (LUT codes)
+A_INT8_ASYM, A_FP8_E4M3, A_FP8_E5M2, A_MXFP8, A_MXINT8 = range(5)
+A_NAMES = ["INT8-asym", "FP8-E4M3", "FP8-E5M2", "MXFP8-E4M3", "MXINT8"]
+# workspace ops
+OP_SELECT, OP_STATS, OP_QUANT_ACT, OP_LINEAR = range(4)
+SCHED_SCALED_LINEAR, SCHED_LINEAR = 0, 1
+
+_P = ctypes.c_void_p
+
+
+class _WQ(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("palette_mask", ctypes.c_uint32),
+                ("code_bits", ctypes.c_int32), ("fmt", _P), ("codes", _P), ("scale", _P), ("zero", _P),
+                ("nf4_absmax", _P), ("e8m0", _P), ("perm", _P), ("group_off", _P), ("err", _P)]
+
+
+class _Stats(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("B", ctypes.c_int32), ("nS", _P), ("lohi", _P)]
+
+
+class _Sched(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("beta0", ctypes.c_double), ("beta1", ctypes.c_double),
+                ("kind", ctypes.c_int32), ("kappa_lo", ctypes.c_double), ("kappa_hi", ctypes.c_double),
+                ("snr_lo", ctypes.c_double), ("snr_hi", ctypes.c_double), ("snr_gate_on", ctypes.c_int32)]
+
+
+class _LUT(ctypes.Structure):
+    _fields_ = [("L", ctypes.c_int32), ("B", ctypes.c_int32), ("T", ctypes.c_int32), ("F", _P), ("S", _P),
+                ("Z", _P)]
+
+
+class _AQ(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int32), ("codes", _P),
+                ("e8m0", _P), ("scale", _P), ("zero", _P)]
+
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library {LIB_PATH} is not built; run __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    L.cham_status_string.argtypes = [ctypes.c_int]
+    L.cham_status_string.restype = ctypes.c_char_p
+    L.cham_version.restype = ctypes.c_int
+    L.cham_select_weight_formats.argtypes = [_P, ctypes.POINTER(_WQ), _P]
+    L.cham_act_stats_reset.argtypes = [ctypes.POINTER(_Stats), _P]
+    L.cham_act_stats_accumulate.argtypes = [_P, i64, i32, i32, ctypes.POINTER(_Stats), _P, sz, _P]
+    L.cham_schedule_default.argtypes = [ctypes.POINTER(_Sched)]
+    L.cham_schedule_default.restype = None
+    L.cham_build_act_lut.argtypes = [ctypes.POINTER(_Stats), ctypes.POINTER(_Sched), _P, ctypes.POINTER(_LUT), _P,
+                                     _P]
+    L.cham_bucket.argtypes = [i32, i32, i32]
+    L.cham_bucket.restype = i32
+    L.cham_quantize_act.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P, sz, _P]
+    L.cham_quantize_act_lut.argtypes = [_P, ctypes.POINTER(_LUT), _P, i32, i32, i32, ctypes.POINTER(_AQ), _P, sz,
+                                        _P]
+    L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
+    L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
+    L.cham_workspace_bytes.restype = sz
+    for name in ("cham_select_weight_formats", "cham_act_stats_reset", "cham_act_stats_accumulate",
+                 "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear"):
+        getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+class ChamError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib().cham_status_string(status).decode()} (status {status})")
+
+
+def _check(rc: int, where: str):
+    if rc != OK:
+        raise ChamError(rc, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev_tensor(t: torch.Tensor, dtype, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def workspace_bytes(op: int, M: int, N: int, K: int) -> int:
+    return int(lib().cham_workspace_bytes(op, M, N, K))
+
+
+def _workspace(op, M, N, K, device, ws):
+    nb = workspace_bytes(op, M, N, K)
+    if ws is not None:
+        return ws, ws.numel()
+    if nb == 0:
+        return None, 0
+    return torch.empty(nb, dtype=torch.uint8, device=device), nb
+
+
+# -------------------------------------------------------------------------------------------
+# weight search
+# -------------------------------------------------------------------------------------------
+def code_bits(mask: int) -> int:
+    return 8 if mask & 0x7 else 4
+
+
+@dataclass
+class WQ:
+    """Packed per-channel weights (device tensors, see cham_wq)."""
+    N: int
+    K: int
+    mask: int
+    code_bits: int
+    fmt: torch.Tensor
+    codes: torch.Tensor
+    scale: torch.Tensor
+    zero: torch.Tensor
+    nf4_absmax: Optional[torch.Tensor]
+    e8m0: Optional[torch.Tensor]
+    perm: Optional[torch.Tensor]
+    group_off: Optional[torch.Tensor]
+    err: Optional[torch.Tensor]
+
+    def struct(self) -> _WQ:
+        return _WQ(self.N, self.K, self.mask, self.code_bits, _ptr(self.fmt), _ptr(self.codes), _ptr(self.scale),
+                   _ptr(self.zero), _ptr(self.nf4_absmax), _ptr(self.e8m0), _ptr(self.perm), _ptr(self.group_off),
+                   _ptr(self.err))
+
+
+def alloc_wq(N: int, K: int, mask: int, device="cuda", want_perm=True, want_err=False) -> WQ:
+    cb = code_bits(mask)
+    u8, f32, i32 = torch.uint8, torch.float32, torch.int32
+    nf4 = bool(mask >> W_NF4 & 1)
+    mx = bool(mask & ((1 << W_MXINT8) | (1 << W_MXINT4) | (1 << W_MXFP4)))
+    return WQ(N, K, mask, cb,
+              fmt=torch.empty(N, dtype=u8, device=device),
+              codes=torch.empty((N, K * cb // 8), dtype=u8, device=device),
+              scale=torch.empty(N, dtype=f32, device=device),
+              zero=torch.empty(N, dtype=i32, device=device),
+              nf4_absmax=torch.empty((N, K // 64), dtype=f32, device=device) if nf4 else None,
+              e8m0=torch.empty((N, K // 32), dtype=u8, device=device) if mx else None,
+              perm=torch.empty(N, dtype=i32, device=device) if want_perm else None,
+              group_off=torch.empty(10, dtype=i32, device=device) if want_perm else None,
+              err=torch.empty((N, 9), dtype=torch.float64, device=device) if want_err else None)
+
+
+def select_weight_formats(W: torch.Tensor, mask: int = MASK_W4, out: Optional[WQ] = None, want_perm=True,
+                          want_err=False, stream=None) -> WQ:
+    """Per-output-channel format search of W [N, K] (fp32, device)."""
+    _dev_tensor(W, torch.float32, "W")
+    N, K = W.shape
+    if out is None:
+        out = alloc_wq(N, K, mask, W.device, want_perm, want_err)
+    st = out.struct()
+    _check(lib().cham_select_weight_formats(_ptr(W), ctypes.byref(st), _stream(stream)), "select_weight_formats")
+    out.code_bits = st.code_bits
+    return out
+
+
+# -------------------------------------------------------------------------------------------
+# statistics and LUT
+# -------------------------------------------------------------------------------------------
+@dataclass
+class Stats:
+    L: int
+    B: int
+    nS: torch.Tensor    # [L*B, 5] f64
+    lohi: torch.Tensor  # [L*B, 2] f32
+
+    def struct(self):
+        return _Stats(self.L, self.B, _ptr(self.nS), _ptr(self.lohi))
+
+
+def alloc_stats(L: int, B: int, device="cuda") -> Stats:
+    return Stats(L, B, torch.empty((L * B, 5), dtype=torch.float64, device=device),
+                 torch.empty((L * B, 2), dtype=torch.float32, device=device))
+
+
+def act_stats_reset(st: Stats, stream=None):
+    s = st.struct()
+    _check(lib().cham_act_stats_reset(ctypes.byref(s), _stream(stream)), "act_stats_reset")
+
+
+def act_stats_accumulate(X: torch.Tensor, layer: int, bucket: int, st: Stats, ws=None, stream=None):
+    _dev_tensor(X, torch.float32, "X")
+    n = X.numel()
+    ws, nb = _workspace(OP_STATS, n, 0, 0, X.device, ws)
+    s = st.struct()
+    _check(lib().cham_act_stats_accumulate(_ptr(X), n, layer, bucket, ctypes.byref(s), _ptr(ws), nb,
+                                           _stream(stream)), "act_stats_accumulate")
+
+
+@dataclass
+class Schedule:
+    T: int = 1000
+    beta0: float = 0.00085
+    beta1: float = 0.012
+    kind: int = SCHED_SCALED_LINEAR
+    kappa_lo: float = 3.0
+    kappa_hi: float = 5.0
+    snr_lo: float = 0.2
+    snr_hi: float = 2.0
+    snr_gate_on: int = 1
+
+    def struct(self):
+        return _Sched(self.T, self.beta0, self.beta1, self.kind, self.kappa_lo, self.kappa_hi, self.snr_lo,
+                      self.snr_hi, self.snr_gate_on)
+
+
+@dataclass
+class LUT:
+    L: int
+    B: int
+    T: int
+    F: torch.Tensor       # [L*B] u8 (device)
+    S: torch.Tensor       # [L*B] f32
+    Z: torch.Tensor       # [L*B] f32
+    kappa: Optional[torch.Tensor] = None
+    F_host: Optional[torch.Tensor] = None  # host mirror of F
+
+    def struct(self):
+        return _LUT(self.L, self.B, self.T, _ptr(self.F), _ptr(self.S), _ptr(self.Z))
+
+    def mirror(self):
+        """Copy F to the host once (after calibration); the per-step lookup then needs no sync."""
+        self.F_host = self.F.cpu().contiguous()
+        return self
+
+
+def build_act_lut(st: Stats, sched: Optional[Schedule] = None, is_shortcut: Optional[torch.Tensor] = None,
+                  want_kappa=True, out: Optional[LUT] = None, stream=None) -> LUT:
+    sched = sched or Schedule()
+    dev = st.nS.device
+    n = st.L * st.B
+    if out is None:
+        out = LUT(st.L, st.B, sched.T, torch.empty(n, dtype=torch.uint8, device=dev),
+                  torch.empty(n, dtype=torch.float32, device=dev), torch.empty(n, dtype=torch.float32, device=dev),
+                  torch.empty(n, dtype=torch.float64, device=dev) if want_kappa else None)
+    if is_shortcut is not None:
+        _dev_tensor(is_shortcut, torch.uint8, "is_shortcut")
+    s, sc, l = st.struct(), sched.struct(), out.struct()
+    _check(lib().cham_build_act_lut(ctypes.byref(s), ctypes.byref(sc), _ptr(is_shortcut), ctypes.byref(l),
+                                    _ptr(out.kappa), _stream(stream)), "build_act_lut")
+    out.T = l.T
+    return out
+
+
+def bucket(t: int, T: int, B: int) -> int:
+    return int(lib().cham_bucket(t, T, B))
+
+
+# -------------------------------------------------------------------------------------------
+# activation quantization
+# -------------------------------------------------------------------------------------------
+@dataclass
+class AQ:
+    M: int
+    K: int
+    fmt: int
+    codes: torch.Tensor              # [M, K] u8
+    e8m0: Optional[torch.Tensor]     # [M, K/32] u8
+    scale: torch.Tensor              # [1] f32
+    zero: torch.Tensor               # [1] f32
+
+    def struct(self):
+        return _AQ(self.M, self.K, self.fmt, _ptr(self.codes), _ptr(self.e8m0), _ptr(self.scale), _ptr(self.zero))
+
+
+def alloc_aq(M: int, K: int, device="cuda", with_e8m0=True) -> AQ:
+    return AQ(M, K, -1, torch.empty((M, K), dtype=torch.uint8, device=device),
+              torch.empty((M, K // 32), dtype=torch.uint8, device=device) if with_e8m0 else None,
+              torch.empty(1, dtype=torch.float32, device=device), torch.empty(1, dtype=torch.float32, device=device))
+
+
+def quantize_act(X: torch.Tensor, fmt: int, dynamic: bool = True, s: Optional[torch.Tensor] = None,
+                 z: Optional[torch.Tensor] = None, out: Optional[AQ] = None, ws=None, stream=None) -> AQ:
+    """Quantize X [M, K]; static mode reads the scale/zero from device tensors s, z."""
+    _dev_tensor(X, torch.float32, "X")
+    M, K = X.shape
+    if out is None:
+        out = alloc_aq(M, K, X.device)
+    ws, nb = _workspace(OP_QUANT_ACT, M, 0, K, X.device, ws)
+    a = out.struct()
+    _check(lib().cham_quantize_act(_ptr(X), fmt, int(dynamic), _ptr(s), _ptr(z), ctypes.byref(a), _ptr(ws), nb,
+                                   _stream(stream)), "quantize_act")
+    out.fmt = a.fmt
+    return out
+
+
+def quantize_act_lut(X: torch.Tensor, lut: LUT, layer: int, t: int, dynamic: bool = False,
+                     out: Optional[AQ] = None, ws=None, stream=None) -> AQ:
+    _dev_tensor(X, torch.float32, "X")
+    if lut.F_host is None:
+        lut.mirror()
+    M, K = X.shape
+    if out is None:
+        out = alloc_aq(M, K, X.device)
+    ws, nb = _workspace(OP_QUANT_ACT, M, 0, K, X.device, ws)
+    a, l = out.struct(), lut.struct()
+    _check(lib().cham_quantize_act_lut(_ptr(X), ctypes.byref(l), ctypes.c_void_p(lut.F_host.data_ptr()), layer, t,
+                                       int(dynamic), ctypes.byref(a), _ptr(ws), nb, _stream(stream)),
+           "quantize_act_lut")
+    out.fmt = a.fmt
+    return out
+
+
+# -------------------------------------------------------------------------------------------
+# mixed-format linear layer
+# -------------------------------------------------------------------------------------------
+def mixed_linear(xq: AQ, wq: WQ, Y: Optional[torch.Tensor] = None, ws=None, stream=None) -> torch.Tensor:
+    if Y is None:
+        Y = torch.empty((xq.M, wq.N), dtype=torch.float32, device=xq.codes.device)
+    _dev_tensor(Y, torch.float32, "Y")
+    ws, nb = _workspace(OP_LINEAR, xq.M, wq.N, wq.K, Y.device, ws)
+    a, w = xq.struct(), wq.struct()
+    _check(lib().cham_mixed_linear(ctypes.byref(a), ctypes.byref(w), _ptr(Y), _ptr(ws), nb, _stream(stream)),
+           "mixed_linear")
+    return Y

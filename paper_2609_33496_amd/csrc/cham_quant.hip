@@ -1,0 +1,238 @@
+// Activation quantization (App. A.7: Alg. 2 static scales, Alg. 3 dynamic per-tensor
+// scales; ScaleZP) to the five activation formats of Sec. 4.2.
+//
+// HBM-bound elementwise pass: float4 loads, one packed 32-bit store of four codes per
+// thread.  MX formats: a 32-element block is 8 consecutive lanes; its amax comes from a
+// shuffle reduction and one lane writes the E8M0 byte.  Dynamic mode first reduces
+// min/max into per-workgroup partials (workspace); the quantize kernel folds them (min
+// and max are exact, so the result does not depend on the order).
+#include "cham_device.h"
+
+namespace cham {
+namespace {
+
+constexpr int kQThreads = 256;
+constexpr int kQMaxBlocks = 1024;
+
+__global__ __launch_bounds__(kQThreads) void minmax_partial_kernel(const float* X, int64_t n, float2* part) {
+    float lo = INFINITY, hi = -INFINITY;
+    const int64_t nq = n >> 2;
+    const float4* X4 = reinterpret_cast<const float4*>(X);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
+        float4 t = X4[i];
+        lo = fminf(fminf(lo, t.x), fminf(fminf(t.y, t.z), t.w));
+        hi = fmaxf(fmaxf(hi, t.x), fmaxf(fmaxf(t.y, t.z), t.w));
+    }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    __shared__ float2 wp[kQThreads / kWave];
+    if ((threadIdx.x & 63) == 0) wp[threadIdx.x >> 6] = make_float2(lo, hi);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < kQThreads / kWave; ++i) { lo = fminf(lo, wp[i].x); hi = fmaxf(hi, wp[i].y); }
+        lo = fminf(lo, wp[0].x);
+        hi = fmaxf(hi, wp[0].y);
+        part[blockIdx.x] = make_float2(lo, hi);
+    }
+}
+
+// ScaleZP (App. A.7) for the per-tensor formats.
+CHAM_DEV void scale_zp(int fmt, float lo, float hi, float* s, float* z) {
+    if (fmt == CHAM_A_INT8_ASYM) {
+        float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
+        *s = floor_scale((h0 - l0) / 255.0f);
+        *z = clampf(rne(-l0 / *s), 0.0f, 255.0f);
+    } else if (fmt == CHAM_A_FP8_E4M3) {
+        *s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
+        *z = 0.0f;
+    } else if (fmt == CHAM_A_FP8_E5M2) {
+        *s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 57344.0f);
+        *z = 0.0f;
+    } else {
+        *s = 1.0f;
+        *z = 0.0f;
+    }
+}
+
+struct QArgs {
+    const float* X;
+    int64_t n;          // M*K, multiple of 4
+    int fmt;
+    const float* s_dev;  // static
+    const float* z_dev;
+    const float2* part;  // dynamic partials (or NULL)
+    int nparts;
+    uint8_t* codes;
+    float* scale_out;
+    float* zero_out;
+};
+
+template <int FMT>
+__global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
+    __shared__ float sh_s, sh_z;
+    if (threadIdx.x < kWave) {
+        float s, z;
+        if (a.part) {
+            float lo = INFINITY, hi = -INFINITY;
+            for (int i = threadIdx.x; i < a.nparts; i += kWave) {
+                float2 p = a.part[i];
+                lo = fminf(lo, p.x);
+                hi = fmaxf(hi, p.y);
+            }
+            lo = wave_min(lo);
+            hi = wave_max(hi);
+            scale_zp(FMT, lo, hi, &s, &z);
+        } else {
+            s = *a.s_dev;
+            z = *a.z_dev;
+        }
+        if (threadIdx.x == 0) {
+            sh_s = s;
+            sh_z = z;
+            if (blockIdx.x == 0) { *a.scale_out = s; *a.zero_out = z; }
+        }
+    }
+    __syncthreads();
+    const float s = sh_s, z = sh_z;
+    const float r = 1.0f / s;
+    const int64_t nq = a.n >> 2;
+    const float4* X4 = reinterpret_cast<const float4*>(a.X);
+    uint32_t* C4 = reinterpret_cast<uint32_t*>(a.codes);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
+        float4 t = X4[i];
+        float e[4] = {t.x, t.y, t.z, t.w};
+        uint32_t w = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t c;
+            if (FMT == CHAM_A_INT8_ASYM) {
+                c = (uint32_t)clampf(rne(e[j] * r) + z, 0.0f, 255.0f);
+            } else if (FMT == CHAM_A_FP8_E4M3) {
+                c = e4m3_encode(clampf(e[j] * r, -448.0f, 448.0f));
+            } else {
+                c = e5m2_encode(clampf(e[j] * r, -57344.0f, 57344.0f));
+            }
+            w |= c << (8 * j);
+        }
+        C4[i] = w;
+    }
+}
+
+// MX formats: one 32-block = 8 lanes x float4.  Grid-stride over float4 index i; the
+// 8-lane groups stay aligned because the stride is a multiple of 64.
+template <int FMT>
+__global__ __launch_bounds__(kQThreads) void quant_mx_kernel(const float* X, int64_t n, uint8_t* codes, uint8_t* e8,
+                                                             float* scale_out, float* zero_out) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) { *scale_out = 1.0f; *zero_out = 0.0f; }
+    const int64_t nq = n >> 2;  // multiple of 8
+    const float4* X4 = reinterpret_cast<const float4*>(X);
+    uint32_t* C4 = reinterpret_cast<uint32_t*>(codes);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t iters = (nq + stride - 1) / stride;
+    for (int64_t it = 0; it < iters; ++it) {
+        const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        const bool ok = i < nq;  // whole 8-lane groups are in or out together
+        float4 t = ok ? X4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        float e[4] = {t.x, t.y, t.z, t.w};
+        float m = fmaxf(fmaxf(fabsf(e[0]), fabsf(e[1])), fmaxf(fabsf(e[2]), fabsf(e[3])));
+        m = group_max<8>(m);
+        const int E = mx_exponent(m, 0);
+        uint32_t w = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            uint32_t c;
+            if (FMT == CHAM_A_MXFP8_E4M3) {
+                c = e4m3_encode(clampf(ldexpf(e[j], -E), -448.0f, 448.0f));
+            } else {
+                float k = clampf(rne(ldexpf(e[j], 6 - E)), -127.0f, 127.0f);
+                c = (uint32_t)(int)k & 0xFFu;
+            }
+            w |= c << (8 * j);
+        }
+        if (ok) {
+            C4[i] = w;
+            if ((threadIdx.x & 7) == 0) e8[i >> 3] = (uint8_t)(E + 127);
+        }
+    }
+}
+
+int qblocks(int64_t nq) {
+    int64_t b = (nq + kQThreads * 4 - 1) / (kQThreads * 4);
+    if (b < 1) b = 1;
+    if (b > kQMaxBlocks) b = kQMaxBlocks;
+    return (int)b;
+}
+
+}  // namespace
+}  // namespace cham
+
+using namespace cham;
+
+size_t cham_quant_workspace_bytes(int64_t n) { return sizeof(float2) * (size_t)qblocks(n >> 2); }
+
+extern "C" int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
+                                 cham_aq* out, void* ws, size_t ws_bytes, void* stream) {
+    if (!X || !out || !out->codes || !out->scale || !out->zero) return CHAM_EINVAL;
+    if (out->M < 1 || out->K < 1) return CHAM_EINVAL;
+    if (fmt < 0 || fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
+    if (out->K % 32 != 0) return CHAM_ESHAPE;
+    if (((uintptr_t)X & 15u) != 0 || ((uintptr_t)out->codes & 3u) != 0) return CHAM_EINVAL;
+    const bool mx = fmt == CHAM_A_MXFP8_E4M3 || fmt == CHAM_A_MXINT8;
+    if (mx && !out->e8m0) return CHAM_EINVAL;
+    if (!mx && !dynamic && (!s_dev || !z_dev)) return CHAM_EINVAL;
+    const int64_t n = out->M * out->K;
+    hipStream_t s = (hipStream_t)stream;
+    out->fmt = fmt;
+    const int nb = qblocks(n >> 2);
+    if (mx) {
+        if (fmt == CHAM_A_MXFP8_E4M3)
+            hipLaunchKernelGGL(quant_mx_kernel<CHAM_A_MXFP8_E4M3>, dim3(nb), dim3(kQThreads), 0, s, X, n, out->codes,
+                               out->e8m0, out->scale, out->zero);
+        else
+            hipLaunchKernelGGL(quant_mx_kernel<CHAM_A_MXINT8>, dim3(nb), dim3(kQThreads), 0, s, X, n, out->codes,
+                               out->e8m0, out->scale, out->zero);
+        CHAM_CHECK_LAUNCH();
+        return CHAM_OK;
+    }
+    QArgs a;
+    a.X = X;
+    a.n = n;
+    a.fmt = fmt;
+    a.s_dev = s_dev;
+    a.z_dev = z_dev;
+    a.part = nullptr;
+    a.nparts = 0;
+    a.codes = out->codes;
+    a.scale_out = out->scale;
+    a.zero_out = out->zero;
+    if (dynamic) {
+        if (!ws || ws_bytes < sizeof(float2) * (size_t)nb) return CHAM_EWORKSPACE;
+        float2* part = (float2*)ws;
+        hipLaunchKernelGGL(minmax_partial_kernel, dim3(nb), dim3(kQThreads), 0, s, X, n, part);
+        CHAM_CHECK_LAUNCH();
+        a.part = part;
+        a.nparts = nb;
+    }
+    if (fmt == CHAM_A_INT8_ASYM)
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_INT8_ASYM>, dim3(nb), dim3(kQThreads), 0, s, a);
+    else if (fmt == CHAM_A_FP8_E4M3)
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E4M3>, dim3(nb), dim3(kQThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E5M2>, dim3(nb), dim3(kQThreads), 0, s, a);
+    CHAM_CHECK_LAUNCH();
+    return CHAM_OK;
+}
+
+extern "C" int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_host, int32_t layer,
+                                     int32_t t, int32_t dynamic, cham_aq* out, void* ws, size_t ws_bytes,
+                                     void* stream) {
+    if (!lut || !F_host || !lut->S || !lut->Z) return CHAM_EINVAL;
+    if (layer < 0 || layer >= lut->L) return CHAM_EINVAL;
+    const int32_t b = cham_bucket(t, lut->T, lut->B);
+    if (b < 0) return CHAM_EINVAL;
+    const int64_t i = (int64_t)layer * lut->B + b;
+    const int fmt = F_host[i];
+    return cham_quantize_act(X, fmt, dynamic, lut->S + i, lut->Z + i, out, ws, ws_bytes, stream);
+}

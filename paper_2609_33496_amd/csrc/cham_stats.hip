@@ -1,0 +1,266 @@
+// Calibration statistics (Sec. 4.4; App. A.7, Alg. 1 first loop) and the LUT build
+// (Sec. 4.3 routing, Sec. 3.1 Eq. snr, App. A.3 Eq. kurt, App. A.7 ScaleZP).
+//
+// Accumulation is HBM-bound: one pass over X with float4 loads, binary64 power sums and
+// binary32 min/max per thread, a workgroup reduction, and per-workgroup partials in the
+// workspace.  A one-workgroup finalize kernel adds the partials in a fixed order into the
+// (layer, bucket) accumulator, so the result is bitwise reproducible run to run (no
+// floating atomics).
+#include <math.h>
+
+#include "cham_device.h"
+
+namespace cham {
+namespace {
+
+constexpr int kStatsThreads = 256;
+constexpr int kStatsMaxBlocks = 1024;
+
+struct Partial {
+    double s1, s2, s3, s4;
+    float lo, hi;
+    float pad0, pad1;
+};
+
+__global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const float* X, int64_t numel,
+                                                                       Partial* part) {
+    double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
+    float lo = INFINITY, hi = -INFINITY;
+    const int64_t nq = numel >> 2;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const float4* X4 = reinterpret_cast<const float4*>(X);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
+        float4 t = X4[i];
+        float e[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            double d = (double)e[j];
+            double d2 = d * d;
+            s1 += d;
+            s2 += d2;
+            s3 += d2 * d;
+            s4 += d2 * d2;
+            lo = fminf(lo, e[j]);
+            hi = fmaxf(hi, e[j]);
+        }
+    }
+    // scalar tail (numel % 4), handled by the first threads of workgroup 0
+    if (blockIdx.x == 0 && threadIdx.x < (numel & 3)) {
+        float x = X[(nq << 2) + threadIdx.x];
+        double d = (double)x, d2 = d * d;
+        s1 += d; s2 += d2; s3 += d2 * d; s4 += d2 * d2;
+        lo = fminf(lo, x); hi = fmaxf(hi, x);
+    }
+    s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
+    lo = wave_min(lo); hi = wave_max(hi);
+    __shared__ Partial wp[kStatsThreads / kWave];
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) wp[w] = Partial{s1, s2, s3, s4, lo, hi, 0.f, 0.f};
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        Partial r = wp[0];
+        for (int i = 1; i < kStatsThreads / kWave; ++i) {
+            r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
+            r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
+        }
+        part[blockIdx.x] = r;
+    }
+}
+
+__global__ __launch_bounds__(kWave) void stats_finalize_kernel(const Partial* part, int nparts,
+                                                               int64_t numel, double* nS, float* lohi) {
+    double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
+    float lo = INFINITY, hi = -INFINITY;
+    for (int i = threadIdx.x; i < nparts; i += kWave) {
+        Partial p = part[i];
+        s1 += p.s1; s2 += p.s2; s3 += p.s3; s4 += p.s4;
+        lo = fminf(lo, p.lo); hi = fmaxf(hi, p.hi);
+    }
+    s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
+    lo = wave_min(lo); hi = wave_max(hi);
+    if (threadIdx.x == 0) {
+        nS[0] += (double)numel;
+        nS[1] += s1;
+        nS[2] += s2;
+        nS[3] += s3;
+        nS[4] += s4;
+        lohi[0] = fminf(lohi[0], lo);
+        lohi[1] = fmaxf(lohi[1], hi);
+    }
+}
+
+__global__ void stats_reset_kernel(double* nS, float* lohi, int n) {
+    int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) {
+        for (int k = 0; k < 5; ++k) nS[5 * i + k] = 0.0;
+        lohi[2 * i] = INFINITY;
+        lohi[2 * i + 1] = -INFINITY;
+    }
+}
+
+struct LutArgs {
+    const double* nS;
+    const float* lohi;
+    const uint8_t* is_shortcut;
+    uint8_t* F;
+    float* S;
+    float* Z;
+    double* kappa;
+    int L, B, T, kind;
+    double b0, b1, r0, r1;  // r0, r1 = sqrt(b0), sqrt(b1), correctly rounded on the host
+    double k_lo, k_hi, s_lo, s_hi;
+    int snr_gate_on;
+};
+
+// One thread per (layer, bucket).
+__global__ void lut_kernel(LutArgs a) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= a.L * a.B) return;
+    const int l = i / a.B, b = i % a.B;
+    // kurtosis from raw power sums (population moments)
+    const double* p = a.nS + 5 * (int64_t)i;
+    const double n = p[0];
+    const double mu = p[1] / n;
+    const double e2 = p[2] / n, e3 = p[3] / n, e4 = p[4] / n;
+    const double m2 = e2 - mu * mu;
+    const double m4 = e4 - 4.0 * mu * e3 + 6.0 * mu * mu * e2 - 3.0 * mu * mu * mu * mu;
+    const double kap = m4 / (m2 * m2);
+    // SNR at the bucket midpoint: alpha_bar_t = prod_{s=0..t} (1 - beta_s), sequential
+    const int tb = (int)(((int64_t)(2 * b + 1) * a.T) / (2LL * a.B));
+    double ab = 1.0;
+    for (int s = 0; s <= tb; ++s) {
+        double frac = a.T > 1 ? (double)s / (double)(a.T - 1) : 0.0;
+        double beta;
+        if (a.kind == CHAM_SCHED_SCALED_LINEAR) {
+            double r = a.r0 + (a.r1 - a.r0) * frac;
+            beta = r * r;
+        } else {
+            beta = a.b0 + (a.b1 - a.b0) * frac;
+        }
+        ab *= (1.0 - beta);
+    }
+    const double snr = ab / (1.0 - ab);
+    // route
+    int f;
+    const int sc = a.is_shortcut ? a.is_shortcut[l] : 0;
+    const bool snr_low = a.snr_gate_on ? (snr < a.s_lo) : false;
+    const bool snr_high = a.snr_gate_on ? (snr > a.s_hi) : true;
+    if (sc) f = CHAM_A_MXFP8_E4M3;
+    else if (kap > a.k_hi || snr_low) f = CHAM_A_FP8_E5M2;
+    else if (kap <= a.k_lo && snr_high) f = CHAM_A_INT8_ASYM;
+    else f = CHAM_A_FP8_E4M3;
+    // ScaleZP on the bucket range
+    float s = 1.0f, z = 0.0f;
+    if (n != 0.0) {
+        const float lo = a.lohi[2 * i], hi = a.lohi[2 * i + 1];
+        if (f == CHAM_A_INT8_ASYM) {
+            float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
+            s = floor_scale((h0 - l0) / 255.0f);
+            z = clampf(rne(-l0 / s), 0.0f, 255.0f);
+        } else if (f == CHAM_A_FP8_E4M3) {
+            s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
+        } else if (f == CHAM_A_FP8_E5M2) {
+            s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 57344.0f);
+        }
+    }
+    a.F[i] = (uint8_t)f;
+    a.S[i] = s;
+    a.Z[i] = z;
+    if (a.kappa) a.kappa[i] = kap;
+}
+
+}  // namespace
+}  // namespace cham
+
+using namespace cham;
+
+extern "C" int cham_act_stats_reset(cham_act_stats* st, void* stream) {
+    if (!st || !st->nS || !st->lohi || st->L < 1 || st->B < 1) return CHAM_EINVAL;
+    const int n = st->L * st->B;
+    hipLaunchKernelGGL(stats_reset_kernel, dim3((n + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+                       st->nS, st->lohi, n);
+    CHAM_CHECK_LAUNCH();
+    return CHAM_OK;
+}
+
+static int stats_blocks(int64_t numel) {
+    int64_t nq = numel >> 2;
+    int64_t b = (nq + kStatsThreads * 8 - 1) / (kStatsThreads * 8);  // >= 8 float4 per thread
+    if (b < 1) b = 1;
+    if (b > kStatsMaxBlocks) b = kStatsMaxBlocks;
+    return (int)b;
+}
+
+size_t cham_stats_workspace_bytes(int64_t numel) { return sizeof(Partial) * (size_t)stats_blocks(numel); }
+
+extern "C" int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t layer, int32_t bucket,
+                                         cham_act_stats* st, void* ws, size_t ws_bytes, void* stream) {
+    if (!X || !st || !st->nS || !st->lohi || numel < 1) return CHAM_EINVAL;
+    if (layer < 0 || layer >= st->L || bucket < 0 || bucket >= st->B) return CHAM_EINVAL;
+    if (((uintptr_t)X & 15u) != 0) return CHAM_EINVAL;
+    const int nb = stats_blocks(numel);
+    if (!ws || ws_bytes < sizeof(Partial) * (size_t)nb) return CHAM_EWORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    Partial* part = (Partial*)ws;
+    hipLaunchKernelGGL(stats_partial_kernel, dim3(nb), dim3(kStatsThreads), 0, s, X, numel, part);
+    CHAM_CHECK_LAUNCH();
+    const int64_t i = (int64_t)layer * st->B + bucket;
+    hipLaunchKernelGGL(stats_finalize_kernel, dim3(1), dim3(kWave), 0, s, part, nb, numel, st->nS + 5 * i,
+                       st->lohi + 2 * i);
+    CHAM_CHECK_LAUNCH();
+    return CHAM_OK;
+}
+
+extern "C" void cham_schedule_default(cham_schedule* s) {
+    if (!s) return;
+    s->T = 1000;
+    s->beta0 = 0.00085;
+    s->beta1 = 0.012;
+    s->kind = CHAM_SCHED_SCALED_LINEAR;
+    s->kappa_lo = 3.0;
+    s->kappa_hi = 5.0;
+    s->snr_lo = 0.2;
+    s->snr_hi = 2.0;
+    s->snr_gate_on = 1;
+}
+
+extern "C" int32_t cham_bucket(int32_t t, int32_t T, int32_t B) {
+    if (t < 0 || T < 1 || B < 1) return -1;
+    int64_t b = ((int64_t)t * B) / T;
+    return (int32_t)(b < B - 1 ? b : B - 1);
+}
+
+extern "C" int cham_build_act_lut(const cham_act_stats* st, const cham_schedule* sch, const uint8_t* is_shortcut,
+                                  cham_lut* lut, double* kappa, void* stream) {
+    if (!st || !sch || !lut || !st->nS || !st->lohi || !lut->F || !lut->S || !lut->Z) return CHAM_EINVAL;
+    if (st->L < 1 || st->B < 1 || lut->L != st->L || lut->B != st->B) return CHAM_EINVAL;
+    if (sch->T < 1 || sch->T > (1 << 20) || st->B > sch->T) return CHAM_EINVAL;
+    if (!(sch->beta0 >= 0.0 && sch->beta0 < 1.0 && sch->beta1 >= 0.0 && sch->beta1 < 1.0)) return CHAM_EINVAL;
+    if (sch->kind != CHAM_SCHED_SCALED_LINEAR && sch->kind != CHAM_SCHED_LINEAR) return CHAM_EINVAL;
+    lut->T = sch->T;
+    LutArgs a;
+    a.nS = st->nS;
+    a.lohi = st->lohi;
+    a.is_shortcut = is_shortcut;
+    a.F = lut->F;
+    a.S = lut->S;
+    a.Z = lut->Z;
+    a.kappa = kappa;
+    a.L = st->L;
+    a.B = st->B;
+    a.T = sch->T;
+    a.kind = sch->kind;
+    a.b0 = sch->beta0;
+    a.b1 = sch->beta1;
+    a.r0 = sqrt(sch->beta0);
+    a.r1 = sqrt(sch->beta1);
+    a.k_lo = sch->kappa_lo;
+    a.k_hi = sch->kappa_hi;
+    a.s_lo = sch->snr_lo;
+    a.s_hi = sch->snr_hi;
+    a.snr_gate_on = sch->snr_gate_on;
+    const int n = st->L * st->B;
+    hipLaunchKernelGGL(lut_kernel, dim3((n + 63) / 64), dim3(64), 0, (hipStream_t)stream, a);
+    CHAM_CHECK_LAUNCH();
+    return CHAM_OK;
+}

@@ -1,0 +1,98 @@
+"""CPU checks of the C ABI: the HIP library loads, exports every function the header
+declares, and validates arguments on the host (no kernel is launched by these calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_33496_amd import cham
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "chameleon.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cham_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = cham.lib()
+    names = _declared_functions()
+    assert len(names) >= 12
+    missing = [n for n in names if not hasattr(L, n)]
+    assert not missing, missing
+
+
+def test_host_only_helpers():
+    L = cham.lib()
+    assert L.cham_version() >= (0 << 16) | (1 << 8)
+    for s in (0, -1, -2, -3, -4, -5, 7):
+        assert L.cham_status_string(s)
+    assert [cham.bucket(t, 1000, 10) for t in (0, 99, 100, 999, 5000)] == [0, 0, 1, 9, 9]
+    assert cham.bucket(-1, 1000, 10) == -1
+    s = cham._Sched()
+    L.cham_schedule_default(ctypes.byref(s))
+    assert (s.T, s.beta0, s.beta1, s.kind) == (1000, 0.00085, 0.012, 0)
+    assert (s.kappa_lo, s.kappa_hi, s.snr_lo, s.snr_hi, s.snr_gate_on) == (3.0, 5.0, 0.2, 2.0, 1)
+    assert cham.workspace_bytes(cham.OP_STATS, 1 << 20, 0, 0) > 0
+    assert cham.workspace_bytes(cham.OP_QUANT_ACT, 2048, 0, 1280) > 0
+    assert cham.workspace_bytes(cham.OP_SELECT, 10, 10, 64) == 0
+
+
+def _wq(**kw):
+    d = dict(N=4, K=64, palette_mask=cham.MASK_W4, code_bits=0, fmt=16, codes=16, scale=16, zero=16,
+             nf4_absmax=16, e8m0=16, perm=None, group_off=None, err=None)
+    d.update(kw)
+    return cham._WQ(d["N"], d["K"], d["palette_mask"], d["code_bits"], *[d[k] for k in (
+        "fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err")])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(palette_mask=0), cham.EFORMAT),
+    (dict(palette_mask=1 << 9), cham.EFORMAT),
+    (dict(N=0), cham.EINVAL),
+    (dict(K=48), cham.ESHAPE),            # not a multiple of 32
+    (dict(K=96), cham.ESHAPE),            # NF4 enabled: multiple of 64 needed
+    (dict(nf4_absmax=None), cham.EINVAL),
+    (dict(e8m0=None), cham.EINVAL),
+    (dict(fmt=None), cham.EINVAL),
+])
+def test_select_weight_formats_argument_errors(kw, status):
+    w = _wq(**kw)
+    rc = cham.lib().cham_select_weight_formats(ctypes.c_void_p(16), ctypes.byref(w), None)
+    assert rc == status
+
+
+def test_other_argument_errors():
+    L = cham.lib()
+    st = cham._Stats(2, 3, ctypes.c_void_p(16), ctypes.c_void_p(16))
+    P = ctypes.c_void_p
+    assert L.cham_act_stats_accumulate(P(16), 100, 2, 0, ctypes.byref(st), P(256), 1 << 20, None) == cham.EINVAL
+    assert L.cham_act_stats_accumulate(P(16), 100, 0, 3, ctypes.byref(st), P(256), 1 << 20, None) == cham.EINVAL
+    assert L.cham_act_stats_accumulate(P(16), 1 << 20, 0, 0, ctypes.byref(st), None, 0, None) == cham.EWORKSPACE
+    aq = cham._AQ(4, 64, 0, P(16), P(16), P(16), P(16))
+    assert L.cham_quantize_act(P(16), 7, 1, None, None, ctypes.byref(aq), P(256), 1 << 20, None) == cham.EFORMAT
+    aq48 = cham._AQ(4, 48, 0, P(16), P(16), P(16), P(16))
+    assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aq48), P(256), 1 << 20, None) == cham.ESHAPE
+    assert L.cham_quantize_act(P(16), 1, 0, None, None, ctypes.byref(aq), None, 0, None) == cham.EINVAL
+    assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aq), None, 0, None) == cham.EWORKSPACE
+    w = _wq(code_bits=4)
+    aqk = cham._AQ(4, 128, 1, P(16), P(16), P(16), P(16))
+    assert L.cham_mixed_linear(ctypes.byref(aqk), ctypes.byref(w), P(16), None, 0, None) == cham.EINVAL  # K mismatch
+    aqf = cham._AQ(4, 64, 9, P(16), P(16), P(16), P(16))
+    assert L.cham_mixed_linear(ctypes.byref(aqf), ctypes.byref(w), P(16), None, 0, None) == cham.EFORMAT
+    w8 = _wq(code_bits=4, palette_mask=cham.MASK_W8)
+    assert L.cham_mixed_linear(ctypes.byref(aq), ctypes.byref(w8), P(16), None, 0, None) == cham.EFORMAT
+    sch = cham.Schedule().struct()
+    lut = cham._LUT(2, 4, 0, P(16), P(16), P(16))
+    assert L.cham_build_act_lut(ctypes.byref(st), ctypes.byref(sch), None, ctypes.byref(lut), None, None) == cham.EINVAL
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(cham, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(cham, "_lib", None)
+    with pytest.raises(RuntimeError):
+        cham.lib()

@@ -1,0 +1,363 @@
+"""GPU parity: the HIP library (through the C ABI) against the CPU oracle on the same seeded
+inputs.  Bit-exact for formats, codes, scales, zero points, block metadata, perm and the LUT;
+kurtosis within 1e-4 relative; the linear layer within 1e-3 * sum|x^ w^| per element."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_33496_amd import cham, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def case(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _search_both(W, mask, want_err=True):
+    case(f"select_weight_formats N={W.shape[0]} K={W.shape[1]} mask={mask:#x}")
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask, want_err=want_err)
+    torch.cuda.synchronize()
+    ref = oracle.select_weight_formats(W, mask, want_err=want_err)
+    return wq, ref
+
+
+def _assert_search_equal(wq, ref, check_perm=True):
+    f = _np(wq.fmt)
+    bad = np.nonzero(f != ref["fmt"])[0]
+    if bad.size and ref["err"] is not None:
+        # report near-ties (errors equal to ~1e-12) separately from real mismatches
+        e = ref["err"][bad]
+        ties = [np.sort(r[r >= 0])[:2] for r in e]
+        rel = [abs(t[1] - t[0]) / max(t[0], 1e-300) for t in ties]
+        assert all(r < 1e-12 for r in rel), (bad[:10], f[bad[:10]], ref["fmt"][bad[:10]], rel[:10])
+    assert bad.size == 0, bad[:10]
+    assert np.array_equal(_np(wq.codes), ref["codes"])
+    assert np.array_equal(_np(wq.scale).view(np.uint32), ref["scale"].view(np.uint32))
+    assert np.array_equal(_np(wq.zero), ref["zero"])
+    if wq.nf4_absmax is not None:
+        assert np.array_equal(_np(wq.nf4_absmax).view(np.uint32), ref["nf4_absmax"].view(np.uint32))
+    if wq.e8m0 is not None:
+        assert np.array_equal(_np(wq.e8m0), ref["e8m0"])
+    if check_perm and wq.perm is not None:
+        assert np.array_equal(_np(wq.perm), ref["perm"])
+        assert np.array_equal(_np(wq.group_off), ref["group_off"])
+    if wq.err is not None and ref["err"] is not None:
+        g, r = _np(wq.err), ref["err"]
+        assert np.allclose(g, r, rtol=1e-9, atol=0), np.max(np.abs(g - r) / np.maximum(np.abs(r), 1e-300))
+
+
+# ---------------------------------------------------------------------------------------
+# weight-format search
+# ---------------------------------------------------------------------------------------
+def test_search_single_layer_w4():
+    X, W = synth.single_layer(0)
+    wq, ref = _search_both(W, oracle.MASK_W4)
+    _assert_search_equal(wq, ref)
+    assert np.all(ref["fmt"] == oracle.W_NF4)
+
+
+@pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8, oracle.MASK_W4_FULL,
+                                  (1 << oracle.W_INT4_SYM) | (1 << oracle.W_FP4) | (1 << oracle.W_MXFP4),
+                                  0x1FF])
+@pytest.mark.parametrize("N,K", [(37, 640), (300, 1280), (20, 1152), (24, 4608), (9, 5120), (5, 8192), (3, 64)])
+def test_search_hetero_rows(mask, N, K):
+    if (mask >> oracle.W_NF4) & 1 and K % 64:
+        pytest.skip("NF4 needs K % 64 == 0")
+    W, fam = synth.hetero_weights(N * 7 + K, N, K)
+    wq, ref = _search_both(W, mask)
+    _assert_search_equal(wq, ref)
+
+
+def test_search_known_winners_and_degenerate_rows():
+    K = 256
+    g = np.random.default_rng(0)
+    rows = []
+    v = oracle.nf4_table()
+    r = v[g.integers(0, 16, K)]
+    r[::64] = 1.0
+    rows.append(r * 2.0 ** -5)
+    q = g.integers(0, 16, K); q[:2] = (0, 15)
+    rows.append((q - 5) * 0.0625)
+    e2 = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6])
+    r = e2[g.integers(0, 8, K)] * g.choice([-1, 1], K); r[::32] = 6
+    rows.append(r * 2.0 ** -6)
+    r = e2[g.integers(0, 8, K)] * g.choice([-1, 1], K); r[::32] = 6
+    rows.append(r * np.repeat(2.0 ** (-3.0 * np.arange(K // 32)), 32))
+    rows.append(np.zeros(K))                                   # all zero
+    rows.append(np.full(K, 0.37))                              # constant positive
+    rows.append(np.full(K, -2.5e-3))                           # constant negative
+    rows.append(g.normal(size=K) * 1e-39)                      # subnormal
+    rows.append(g.normal(size=K) * 1e30)                       # huge
+    rr = g.normal(size=K) * 0.02; rr[17] = 3.0                 # one outlier
+    rows.append(rr)
+    rr = g.normal(size=K); rr[:128] = 0                        # half zero (all-zero blocks)
+    rows.append(rr)
+    rows.append(np.where(g.random(K) < 0.5, -0.0, 0.0))       # signed zeros
+    W = np.stack(rows).astype(np.float32)
+    for mask in (oracle.MASK_W4, oracle.MASK_W8, 0x1FF):
+        wq, ref = _search_both(W, mask)
+        _assert_search_equal(wq, ref)
+
+
+def test_search_full_size_sampled():
+    """SDXL-like GEGLU weight (N = 10240, K = 1280) and FF-out (N = 1280, K = 5120): the
+    whole matrix is searched on the GPU; sampled channels are checked against the oracle."""
+    for name, K, N in (("geglu", 1280, 10240), ("ff_out", 5120, 1280)):
+        W, _ = synth.hetero_weights(11, N, K)
+        case(f"select_weight_formats full-size {name} N={N} K={K}")
+        wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), oracle.MASK_W4)
+        torch.cuda.synchronize()
+        rows = np.sort(np.random.default_rng(1).choice(N, 256, replace=False))
+        ref = oracle.select_weight_formats(W[rows], oracle.MASK_W4)
+        f = _np(wq.fmt)
+        assert np.array_equal(f[rows], ref["fmt"])
+        assert np.array_equal(_np(wq.codes)[rows], ref["codes"])
+        assert np.array_equal(_np(wq.scale)[rows], ref["scale"])
+        assert np.array_equal(_np(wq.nf4_absmax)[rows], ref["nf4_absmax"])
+        assert np.array_equal(_np(wq.e8m0)[rows], ref["e8m0"])
+        # perm is a stable sort of the GPU's own format vector
+        assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable"))
+
+
+# ---------------------------------------------------------------------------------------
+# activation statistics and LUT
+# ---------------------------------------------------------------------------------------
+def _calibrate(L, B, M, K, seed=0, T=1000, steps_per_bucket=2):
+    st = cham.alloc_stats(L, B, DEV)
+    cham.act_stats_reset(st)
+    ost = oracle.Stats(L, B)
+    for b in range(B):
+        for i in range(steps_per_bucket):
+            t = (b * T) // B + (i * T) // (B * steps_per_bucket) + 3
+            for l in range(L):
+                x = synth.diffusion_acts(seed, l, t, M, K)
+                case(f"act_stats_accumulate layer={l} bucket={b} t={t} numel={x.size}")
+                cham.act_stats_accumulate(torch.from_numpy(x).to(DEV), l, b, st)
+                ost.accumulate(x, l, b)
+    return st, ost
+
+
+def test_stats_and_lut_match_oracle():
+    L, B = 6, 4
+    st, ost = _calibrate(L, B, 96, 320)
+    torch.cuda.synchronize()
+    nS = _np(st.nS)
+    assert np.allclose(nS, ost.nS, rtol=1e-12, atol=0)
+    assert np.array_equal(_np(st.lohi), ost.lohi)
+    for sched, name in ((oracle.BETAS_SDXL, "sdxl"), (oracle.BETAS_PIXART, "pixart")):
+        T, b0, b1, kind = sched
+        s = cham.Schedule(T=T, beta0=b0, beta1=b1, kind=kind)
+        shortcut = torch.tensor([0, 0, 1, 0, 0, 0], dtype=torch.uint8, device=DEV)
+        case(f"build_act_lut {name} L={L} B={B}")
+        lut = cham.build_act_lut(st, s, is_shortcut=shortcut)
+        torch.cuda.synchronize()
+        F, S, Z, kap = oracle.build_lut(ost, sched, is_shortcut=np.array([0, 0, 1, 0, 0, 0], np.uint8))
+        kg = _np(lut.kappa)
+        assert np.allclose(kg, kap, rtol=1e-4)
+        near_gate = np.any(np.abs(kap[:, None] - np.array([3.0, 5.0])[None, :]) < 1e-9 * np.abs(kap[:, None]), axis=1)
+        ok = (_np(lut.F) == F) | near_gate
+        assert ok.all(), (_np(lut.F), F)
+        assert np.array_equal(_np(lut.S).view(np.uint32), S.view(np.uint32))
+        assert np.array_equal(_np(lut.Z), Z)
+    # the kurtosis-only arm (SNR gate off) and an empty bucket
+    st2 = cham.alloc_stats(2, 3, DEV)
+    cham.act_stats_reset(st2)
+    ost2 = oracle.Stats(2, 3)
+    for l in range(2):
+        x = synth.diffusion_acts(1, l, 900, 64, 128)
+        cham.act_stats_accumulate(torch.from_numpy(x).to(DEV), l, 0, st2)
+        ost2.accumulate(x, l, 0)
+    lut2 = cham.build_act_lut(st2, cham.Schedule(snr_gate_on=0))
+    torch.cuda.synchronize()
+    F2, S2, Z2, _ = oracle.build_lut(ost2, snr_gate_on=0)
+    assert np.array_equal(_np(lut2.F), F2) and np.array_equal(_np(lut2.S), S2) and np.array_equal(_np(lut2.Z), Z2)
+
+
+def test_stats_ragged_and_tiny():
+    for n in (1, 3, 5, 1023, 4097, 1_000_003):
+        x = np.random.default_rng(n).standard_t(4, n).astype(np.float32)
+        st = cham.alloc_stats(1, 1, DEV)
+        cham.act_stats_reset(st)
+        case(f"act_stats_accumulate ragged numel={n}")
+        cham.act_stats_accumulate(torch.from_numpy(x).to(DEV), 0, 0, st)
+        torch.cuda.synchronize()
+        ost = oracle.Stats(1, 1)
+        ost.accumulate(x, 0, 0)
+        assert np.allclose(_np(st.nS), ost.nS, rtol=1e-12)
+        assert np.array_equal(_np(st.lohi), ost.lohi)
+
+
+# ---------------------------------------------------------------------------------------
+# activation quantization
+# ---------------------------------------------------------------------------------------
+def _check_aq(aq, X, fmt, s=None, z=None, dynamic=True):
+    if dynamic:
+        codes, e8, xh, s_ref, z_ref = oracle.quantize_act_dynamic(X, fmt)
+    else:
+        codes, e8, xh = oracle.quantize_act(X, fmt, s, z)
+        s_ref, z_ref = (np.float32(s), np.float32(z)) if fmt < 3 else (np.float32(1), np.float32(0))
+    gc = _np(aq.codes)
+    bad = np.argwhere(gc != codes)
+    assert bad.shape[0] == 0, (fmt, bad[:5], gc[tuple(bad[:5].T)], codes[tuple(bad[:5].T)], X[tuple(bad[:5].T)])
+    assert _np(aq.scale)[0] == s_ref and _np(aq.zero)[0] == z_ref
+    if fmt >= 3:
+        assert np.array_equal(_np(aq.e8m0), e8)
+
+
+@pytest.mark.parametrize("fmt", range(5))
+def test_quantize_act_dynamic(fmt):
+    X, _ = synth.single_layer(0)
+    case(f"quantize_act dynamic fmt={fmt} M={X.shape[0]} K={X.shape[1]}")
+    aq = cham.quantize_act(torch.from_numpy(X).to(DEV), fmt, dynamic=True)
+    torch.cuda.synchronize()
+    _check_aq(aq, X, fmt)
+
+
+@pytest.mark.parametrize("fmt", range(5))
+def test_quantize_act_static_with_saturation(fmt):
+    X = synth.diffusion_acts(0, 1, 500, 200, 384)
+    lo, hi = oracle.minmax(X)
+    s, z = oracle.scale_zp(fmt, lo * 0.5, hi * 0.5)  # calibrated range narrower than X: saturation
+    sd = torch.tensor([s], dtype=torch.float32, device=DEV)
+    zd = torch.tensor([z], dtype=torch.float32, device=DEV)
+    case(f"quantize_act static fmt={fmt}")
+    aq = cham.quantize_act(torch.from_numpy(X).to(DEV), fmt, dynamic=False, s=sd, z=zd)
+    torch.cuda.synchronize()
+    _check_aq(aq, X, fmt, s, z, dynamic=False)
+
+
+def test_fp8_conversion_on_every_tie_and_boundary():
+    """Every midpoint between neighbouring E4M3 / E5M2 values, the floats next to it, the
+    subnormal range and the saturation edge, quantized with s = 1 (static)."""
+    for fmt, which, mx in ((cham.A_FP8_E4M3, oracle.MF_E4M3, 448.0), (cham.A_FP8_E5M2, oracle.MF_E5M2, 57344.0)):
+        maxc = 0x7E if which == oracle.MF_E4M3 else 0x7B
+        vals = sorted(set(oracle.mf_decode(which, c) for c in range(maxc + 1)))
+        xs = []
+        for a_, b_ in zip(vals[:-1], vals[1:]):
+            m = np.float32((a_ + b_) / 2)
+            xs += [a_, m, np.nextafter(m, np.float32(0)), np.nextafter(m, np.float32(1e30))]
+        xs += [mx, mx * 1.01, 1e30, 1e-45, 0.0]
+        xs = np.array(xs + [-x for x in xs], np.float32)
+        xs = np.concatenate([xs, np.zeros((-xs.size) % 64, np.float32)]).reshape(-1, 64)
+        sd = torch.ones(1, device=DEV)
+        zd = torch.zeros(1, device=DEV)
+        case(f"quantize_act fp8 boundaries fmt={fmt}")
+        aq = cham.quantize_act(torch.from_numpy(xs).to(DEV), fmt, dynamic=False, s=sd, z=zd)
+        torch.cuda.synchronize()
+        _check_aq(aq, xs, fmt, 1.0, 0.0, dynamic=False)
+
+
+def test_quantize_act_lut_lookup():
+    L, B = 3, 4
+    st, ost = _calibrate(L, B, 64, 256, seed=2, steps_per_bucket=1)
+    lut = cham.build_act_lut(st).mirror()
+    F, S, Z, _ = oracle.build_lut(ost)
+    for l in range(L):
+        for t in (0, 260, 600, 999):
+            X = synth.diffusion_acts(5, l, t, 64, 256)
+            case(f"quantize_act_lut layer={l} t={t}")
+            aq = cham.quantize_act_lut(torch.from_numpy(X).to(DEV), lut, l, t, dynamic=False)
+            torch.cuda.synchronize()
+            i = l * B + oracle.bucket(t, 1000, B)
+            assert aq.fmt == F[i]
+            _check_aq(aq, X, int(F[i]), S[i], Z[i], dynamic=False)
+
+
+# ---------------------------------------------------------------------------------------
+# mixed-format linear layer
+# ---------------------------------------------------------------------------------------
+def _linear_case(X, W, mask, afmt, dynamic=True):
+    M, K = X.shape
+    N = W.shape[0]
+    case(f"mixed_linear M={M} N={N} K={K} mask={mask:#x} afmt={afmt}")
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask)
+    xq = cham.quantize_act(torch.from_numpy(X).to(DEV), afmt, dynamic=True)
+    Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+    ref = oracle.select_weight_formats(W, mask, want_err=False, want_perm=False)
+    Wh = oracle.dequant_weights(ref, K)
+    codes, e8, xh, s, z = oracle.quantize_act_dynamic(X, afmt, want_xhat=True)
+    assert np.array_equal(_np(wq.fmt), ref["fmt"])
+    assert np.array_equal(_np(xq.codes), codes)
+    Yr, Bm = oracle.linear(xh, Wh)
+    err = np.abs(Y - Yr)
+    bad = err > 1e-3 * Bm
+    assert not bad.any(), (np.argwhere(bad)[:5], (err / np.maximum(Bm, 1e-300)).max())
+    return (err / np.maximum(Bm, 1e-300)).max()
+
+
+@pytest.mark.parametrize("afmt", range(5))
+def test_linear_single_layer(afmt):
+    X, W = synth.single_layer(0)
+    _linear_case(X, W, oracle.MASK_W4, afmt)
+
+
+@pytest.mark.parametrize("wf", range(9))
+def test_linear_each_weight_format(wf):
+    """Every GEMM decode path, one weight format at a time (ragged M and N)."""
+    X, _ = synth.single_layer(3, M=200, K=640, N=8)
+    W, _ = synth.hetero_weights(4, 300, 640)
+    for afmt in (cham.A_INT8_ASYM, cham.A_FP8_E4M3, cham.A_FP8_E5M2, cham.A_MXFP8):
+        _linear_case(X, W, 1 << wf, afmt)
+
+
+@pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8, 0x1FF])
+def test_linear_hetero_mixed(mask):
+    X = synth.diffusion_acts(0, 2, 400, 130, 1280)
+    W, _ = synth.hetero_weights(8, 333, 1280)
+    for afmt in range(5):
+        _linear_case(X, W, mask, afmt)
+
+
+def test_linear_exact_grid_inputs():
+    """Activations and weights on exact grids with power-of-two scales: every product and
+    partial sum is exact in binary32, so Y equals the binary64 reference exactly."""
+    g = np.random.default_rng(0)
+    M, N, K = 64, 96, 256
+    X = (g.integers(-6, 7, (M, K)) * 0.25).astype(np.float32)   # E4M3-exact values
+    e2 = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6], np.float32)
+    W = (e2[g.integers(0, 8, (N, K))] * g.choice([-1, 1], (N, K))).astype(np.float32)
+    W[:, 0] = 6.0
+    sd = torch.tensor([2.0 ** -4], device=DEV)  # static power-of-two scale: x/s = 4k, exact in E4M3
+    zd = torch.zeros(1, device=DEV)
+    case("mixed_linear exact-grid inputs")
+    xq = cham.quantize_act(torch.from_numpy(X).to(DEV), cham.A_FP8_E4M3, dynamic=False, s=sd, z=zd)
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), 1 << cham.W_MXFP4)
+    Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+    Yr = X.astype(np.float64) @ W.astype(np.float64).T
+    assert np.array_equal(Y, Yr)
+
+
+def test_linear_full_size_sampled():
+    """SDXL-like out-proj and GEGLU at M = 2048 tokens (CFG batch 2 x 1024): sampled
+    outputs against the oracle computed one by one."""
+    for name, K, N in (("out", 1280, 1280), ("geglu", 1280, 10240), ("ff_out", 5120, 1280)):
+        M = 2048
+        X = synth.diffusion_acts(0, 1, 375, M, K)
+        W, _ = synth.hetero_weights(21, N, K)
+        case(f"mixed_linear full-size {name} M={M} N={N} K={K}")
+        wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), oracle.MASK_W4)
+        for afmt in (cham.A_FP8_E4M3, cham.A_INT8_ASYM):
+            xq = cham.quantize_act(torch.from_numpy(X).to(DEV), afmt, dynamic=True)
+            Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+            g = np.random.default_rng(afmt)
+            mm = g.integers(0, M, 2048)
+            nn = g.integers(0, N, 2048)
+            rows = np.unique(nn)
+            ref = oracle.select_weight_formats(W[rows], oracle.MASK_W4, want_err=False, want_perm=False)
+            Wh = np.zeros((N, K), np.float32)
+            Wh[rows] = oracle.dequant_weights(ref, K)
+            lo, hi = oracle.minmax(X)
+            s, z = oracle.scale_zp(afmt, lo, hi)
+            mrows = np.unique(mm)
+            xh = np.zeros_like(X)
+            xh[mrows] = oracle.quantize_act(X[mrows], afmt, s, z, want_xhat=True)[2]
+            yr, bm = oracle.linear_pairs(xh, Wh, mm, nn)
+            err = np.abs(Y[mm, nn] - yr)
+            assert np.all(err <= 1e-3 * bm), (name, afmt, (err / bm).max())
