@@ -103,6 +103,8 @@ def main():
                             device=dev) for X in Xs]
     ws_q = [torch.empty(max(cham.workspace_bytes(cham.OP_QUANT_ACT, M_TOKENS, 0, X.shape[1]), 256),
                         dtype=torch.uint8, device=dev) for X in Xs]
+    ws_lin = [torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=dev)
+              for (_, K, N) in layers]
     wq_s = [w.struct() for w in wqs]
     st_s = stats.struct()
     sc_s = sched.struct()
@@ -139,7 +141,8 @@ def main():
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
         for li in range(len(layers)):
-            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), None, 0, S)
+            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin[li]),
+                                     ws_lin[li].numel(), S)
             assert rc == 0, rc
         if record:
             e3 = torch.cuda.Event(enable_timing=True)
@@ -194,7 +197,7 @@ def main():
         "search_ms": round(ms_search, 4),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4), "traffic": None,
-                     "kernel": "gemm_f16_kernel (4 launches/step, flop-weighted)"},
+                     "kernel": "mixed_linear = act decode + gemm_kernel (4 calls/step, flop-weighted)"},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, Ws, Xs, fmts, args.cpu_budget_s)

@@ -43,7 +43,8 @@ extern "C" {
  * ------------------------------------------------------------------------------------- */
 #define CHAM_OK 0
 #define CHAM_EINVAL (-1)     /* NULL pointer, negative or zero size, bad layer/bucket index  */
-#define CHAM_ESHAPE (-2)     /* K not a multiple of 32 (MX) / 64 (NF4) / 2 (4-bit packing)   */
+#define CHAM_ESHAPE (-2)     /* K not a multiple of 32 (every call) or of 64 (NF4 enabled;
+                                mixed_linear)                                                */
 #define CHAM_EFORMAT (-3)    /* unknown format id, empty or out-of-range palette mask        */
 #define CHAM_EHIP (-4)       /* a HIP launch or runtime call failed                          */
 #define CHAM_EWORKSPACE (-5) /* ws NULL or smaller than cham_workspace_bytes()               */
@@ -140,7 +141,7 @@ typedef struct cham_act_stats {
 /* Set every accumulator to n = S_k = 0, lo = +inf, hi = -inf. */
 int cham_act_stats_reset(cham_act_stats* st, void* stream);
 
-/* Add one activation tensor X (numel binary32 values, device) of `layer` at a timestep of
+/* Add one activation tensor X (numel binary32 values, device, 16-byte aligned) of `layer` at a timestep of
  * `bucket` into the accumulator: n += numel, S_k += sum x^k, lo/hi = min/max.  The sums are
  * reduced in a fixed order (bitwise reproducible run to run).  ws: CHAM_OP_STATS bytes.
  * Errors: CHAM_EINVAL (NULL, numel < 1, layer/bucket out of range), CHAM_EWORKSPACE, CHAM_EHIP. */
@@ -194,7 +195,8 @@ typedef struct cham_aq {
     float* zero;      /* [1] the zero point z used (0 unless INT8-asym)                       */
 } cham_aq;
 
-/* Quantize X [M][K] (device, finite binary32) to activation format `fmt`:
+/* Quantize X [M][K] (device, finite binary32, 16-byte aligned; out->codes 4-byte aligned)
+ * to activation format `fmt`:
  *   INT8-asym  q = clamp(round(x/s) + z, 0, 255)
  *   FP8        e = E4M3 / E5M2(clamp(x/s, +-448 / +-57344)), round to nearest even
  *   MXFP8      per 32-block E = floor(log2 amax) (the paper's exponent: values in (-2, 2)),
@@ -222,8 +224,10 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  * Y[m][n] = sum_k x^[m][k] w^[n][k], with x^ = DQ(xq) and w^ = DQ(wq) exactly as the
  * quantizers above define them, accumulated in binary32 on the matrix cores.  Accuracy:
  * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element (NF4 levels are carried at half
- * precision; every other operand is exact).  xq->K must equal wq->K.  Y is written in the
- * original channel order.  ws: CHAM_OP_LINEAR bytes.
+ * precision; every other operand is exact).  xq->K must equal wq->K and be a multiple of
+ * 64; xq->codes and wq->codes must be 16-byte aligned.  Y [M][N] is written in the original
+ * channel order.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of the decoded
+ * activations and per-row scales), 256-byte aligned.
  * Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE, CHAM_EWORKSPACE, CHAM_EHIP.
  * ------------------------------------------------------------------------------------- */
 int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
@@ -236,8 +240,8 @@ int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, 
 #define CHAM_OP_STATS 1
 #define CHAM_OP_QUANT_ACT 2
 #define CHAM_OP_LINEAR 3
-/* Bytes of workspace op needs at these sizes (M rows of X / numel for CHAM_OP_STATS in M;
- * N output channels; K inner size).  0 means no workspace. */
+/* Bytes of workspace op needs at these sizes (M rows of X -- numel for CHAM_OP_STATS --,
+ * N output channels, K inner size).  0 means no workspace. */
 size_t cham_workspace_bytes(int32_t op, int64_t M, int64_t N, int64_t K);
 
 #ifdef __cplusplus

@@ -1,12 +1,18 @@
 // Per-output-channel weight-format search (Sec. 4.5, Eq. weight-argmax) and the stable
 // grouping of channels by chosen format.
 //
-// One wavefront owns one output channel.  The row is read from HBM once (coalesced
-// float4 loads) and held in registers; lane l holds elements 4(l + 64c) .. +3 of chunk c,
-// so an MX block (32 elements) is 8 consecutive lanes and an NF4 block (64) 16 lanes.
-// Row and block statistics come from shuffle reductions; every enabled format's round
-// trip is evaluated from the registers, its squared error summed in binary64, and the
-// winner's codes and metadata are written packed.  Nothing is re-read.
+// One wavefront owns one output channel.  The row is read from HBM once (coalesced float4
+// loads) and held in registers: lane l holds elements 4(l + 64c) .. +3 of chunk c, so an MX
+// block (32 elements) is 8 consecutive lanes and an NF4 block (64) 16 lanes.  Row and block
+// statistics come from DPP reductions.  One fused pass round-trips every element through
+// every enabled format and accumulates the squared reconstruction errors in binary32; the
+// per-element reconstructions are the exact binary32 values the format defines (E2M1 via
+// the gfx950 FP4 converters, which round to nearest even and saturate exactly as the format
+// requires; NF4 through a 33-cell table in LDS plus one exact threshold comparison).  If
+// the two smallest error sums are within 2^-12 of each other -- far above the binary32
+// summation error -- the errors of every enabled format are recomputed with binary64 sums,
+// so the choice is always the binary64 argmin.  The winner's codes and metadata are then
+// written packed.  Nothing is re-read from HBM.
 #include "cham_device.h"
 
 namespace cham {
@@ -27,7 +33,7 @@ struct SearchArgs {
     double* err;
 };
 
-// per-channel parameters of every format, computed from the row statistics
+// per-channel parameters of the per-channel formats
 struct RowParams {
     float s_sym8, r_sym8, s_sym4, r_sym4;  // INT-sym
     float s_as8, r_as8, z_as8;             // INT-asym 8
@@ -35,10 +41,84 @@ struct RowParams {
     float s_fp4, r_fp4;                    // FP4
 };
 
-// Quantize-dequantize of one element in format f.  blk32 = the element's 32-block absmax,
-// blk64 = its 64-block absmax.  Returns the code (low bits) and writes the reconstruction.
+// ------------------------------------------------------------------------------------
+// DPP reductions
+// ------------------------------------------------------------------------------------
+template <int CTRL>
+CHAM_DEV float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+// max over the aligned 8-lane group (quad_perm 1,0,3,2; quad_perm 2,3,0,1; row_half_mirror)
+CHAM_DEV float max8(float v) {
+    v = fmaxf(v, dpp<0xB1>(v));
+    v = fmaxf(v, dpp<0x4E>(v));
+    return fmaxf(v, dpp<0x141>(v));
+}
+CHAM_DEV float max16_from8(float v) { return fmaxf(v, dpp<0x140>(v)); }  // row_mirror
+// reductions over the wave: within rows of 16 by DPP, then the 4 rows by readlane
+CHAM_DEV float row_sum16(float v) {
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0x141>(v);
+    return v + dpp<0x140>(v);
+}
+CHAM_DEV float lane_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+CHAM_DEV float wave_sum_dpp(float v) {
+    v = row_sum16(v);
+    return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+CHAM_DEV float wave_min_dpp(float v) {
+    v = fminf(v, dpp<0xB1>(v));
+    v = fminf(v, dpp<0x4E>(v));
+    v = fminf(v, dpp<0x141>(v));
+    v = fminf(v, dpp<0x140>(v));
+    return fminf(fminf(lane_f(v, 0), lane_f(v, 16)), fminf(lane_f(v, 32), lane_f(v, 48)));
+}
+CHAM_DEV float wave_max_dpp(float v) {
+    v = max16_from8(max8(v));
+    return fmaxf(fmaxf(lane_f(v, 0), lane_f(v, 16)), fmaxf(lane_f(v, 32), lane_f(v, 48)));
+}
+
+// ------------------------------------------------------------------------------------
+// NF4 lookup: cell i of [-1, 1] (width 1/16) holds cnt = number of decision thresholds
+// below the cell's lower bound, the first threshold at or above it (+inf if none), and
+// the levels cnt and cnt+1.  Consecutive thresholds are more than 1/16 apart and none is
+// within 1e-3 of a cell boundary, so for y in the cell the nearest level is
+// cnt + (y > thr); an index computed one cell off near a boundary gives the same code.
+// ------------------------------------------------------------------------------------
+struct NF4Cell {
+    float thr, vlo, vhi;
+    uint32_t cnt;
+};
+
+CHAM_DEV void nf4_cells_init(NF4Cell* cells) {
+    const int i = threadIdx.x;
+    if (i < 33) {
+        const float b = -1.0f + (float)i * 0.0625f;
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int j = 0; j < 15; ++j) cnt += (__uint_as_float(kNF4ThrBits[j]) < b) ? 1u : 0u;
+        NF4Cell c;
+        c.cnt = cnt;
+        c.thr = cnt < 15 ? __uint_as_float(kNF4ThrBits[cnt]) : INFINITY;
+        c.vlo = nf4_level(cnt);
+        c.vhi = nf4_level(cnt < 15 ? cnt + 1 : 15);
+        cells[i] = c;
+    }
+}
+
+CHAM_DEV NF4Cell nf4_cell(const NF4Cell* cells, float y) {
+    int i = (int)__builtin_fmaf(y, 16.0f, 16.0f);  // y in [-1, 1] -> [0, 32]
+    i = i < 0 ? 0 : (i > 32 ? 32 : i);
+    return cells[i];
+}
+
+// ------------------------------------------------------------------------------------
+// exact per-element quantize-dequantize of format F (used for the emitted codes and for
+// the binary64 re-check); blk32 / blk64 = the element's 32- / 64-block absmax
+// ------------------------------------------------------------------------------------
 template <int F>
-CHAM_DEV uint32_t quant_one(float w, const RowParams& p, float blk32, float blk64, float* wh) {
+CHAM_DEV uint32_t quant_one(float w, const RowParams& p, float blk32, float blk64, const NF4Cell* cells, float* wh) {
     switch (F) {
     case CHAM_W_INT8_SYM: {
         float q = clampf(rne(w * p.r_sym8), -127.0f, 127.0f);
@@ -69,10 +149,11 @@ CHAM_DEV uint32_t quant_one(float w, const RowParams& p, float blk32, float blk6
     }
     case CHAM_W_NF4: {
         float a = floor_scale(blk64);
-        float r = 1.0f / a;
-        uint32_t c = nf4_encode(w * r);
-        *wh = nf4_level(c) * a;
-        return c;
+        float y = w * (1.0f / a);
+        const NF4Cell cl = nf4_cell(cells, y);
+        const bool up = y > cl.thr;
+        *wh = (up ? cl.vhi : cl.vlo) * a;
+        return cl.cnt + (up ? 1u : 0u);
     }
     case CHAM_W_MXINT8: {
         int E = mx_exponent(blk32, 0);
@@ -97,42 +178,154 @@ CHAM_DEV uint32_t quant_one(float w, const RowParams& p, float blk32, float blk6
     }
 }
 
+// ------------------------------------------------------------------------------------
+// fast binary32 error accumulation of one chunk (4 elements) in format F
+// ------------------------------------------------------------------------------------
+typedef float v2f __attribute__((ext_vector_type(2)));
+
+// 2^E as the binary32 scale operand of the FP4 converters (they read its exponent field)
+CHAM_DEV float e8m0_scale(int E) { return __uint_as_float((uint32_t)(E + 127) << 23); }
+
+// E2M1 round trip of a pair through the hardware converter with a power-of-two scale.
+CHAM_DEV v2f fp4_pair(float a, float b, float scale) {
+    const uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, a, b, scale, 0);
+    return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, scale, 0);
+}
+
+template <int F>
+CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, float blk64, const NF4Cell* cells) {
+    float e = 0.0f;
+    if (F == CHAM_W_INT8_ASYM || F == CHAM_W_INT4_ASYM) {
+        const float r = F == CHAM_W_INT8_ASYM ? p.r_as8 : p.r_as4;
+        const float s = F == CHAM_W_INT8_ASYM ? p.s_as8 : p.s_as4;
+        const float z = F == CHAM_W_INT8_ASYM ? p.z_as8 : p.z_as4;
+        const float L = F == CHAM_W_INT8_ASYM ? 255.0f : 15.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            // clamp(round(w r) + z, 0, L) - z == clamp(round(w r), -z, L - z) on these integers
+            const float u = __builtin_amdgcn_fmed3f(rne(w[j] * r), -z, L - z);
+            const float d = w[j] - u * s;
+            e = __builtin_fmaf(d, d, e);
+        }
+    } else if (F == CHAM_W_INT8_SYM || F == CHAM_W_INT4_SYM) {
+        const float r = F == CHAM_W_INT8_SYM ? p.r_sym8 : p.r_sym4;
+        const float s = F == CHAM_W_INT8_SYM ? p.s_sym8 : p.s_sym4;
+        const float Q = F == CHAM_W_INT8_SYM ? 127.0f : 7.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float q = __builtin_amdgcn_fmed3f(rne(w[j] * r), -Q, Q);
+            const float d = w[j] - q * s;
+            e = __builtin_fmaf(d, d, e);
+        }
+    } else if (F == CHAM_W_FP4) {
+#pragma unroll
+        for (int j = 0; j < 4; j += 2) {
+            const v2f v = fp4_pair(w[j] * p.r_fp4, w[j + 1] * p.r_fp4, 1.0f);
+            const float d0 = w[j] - v.x * p.s_fp4, d1 = w[j + 1] - v.y * p.s_fp4;
+            e = __builtin_fmaf(d0, d0, e);
+            e = __builtin_fmaf(d1, d1, e);
+        }
+    } else if (F == CHAM_W_MXFP4) {
+        const float sc = e8m0_scale(mx_exponent(blk32, 2));
+#pragma unroll
+        for (int j = 0; j < 4; j += 2) {
+            const v2f v = fp4_pair(w[j], w[j + 1], sc);
+            const float d0 = w[j] - v.x, d1 = w[j + 1] - v.y;
+            e = __builtin_fmaf(d0, d0, e);
+            e = __builtin_fmaf(d1, d1, e);
+        }
+    } else if (F == CHAM_W_MXINT4 || F == CHAM_W_MXINT8) {
+        // in the block's scaled domain: y = w 2^(F-E) exactly, d = y - k exactly
+        const int Fb = F == CHAM_W_MXINT8 ? 6 : 2;
+        const float Q = F == CHAM_W_MXINT8 ? 127.0f : 7.0f;
+        const int E = mx_exponent(blk32, 0);
+        float es = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float y = ldexpf(w[j], Fb - E);
+            const float k = __builtin_amdgcn_fmed3f(rne(y), -Q, Q);
+            const float d = y - k;
+            es = __builtin_fmaf(d, d, es);
+        }
+        e = ldexpf(es, 2 * (E - Fb));
+    } else {  // NF4
+        const float a = floor_scale(blk64);
+        const float r = 1.0f / a;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float y = w[j] * r;
+            const NF4Cell cl = nf4_cell(cells, y);
+            const float d = w[j] - (y > cl.thr ? cl.vhi : cl.vlo) * a;
+            e = __builtin_fmaf(d, d, e);
+        }
+    }
+    return e;
+}
+
 template <int F, int NCH>
 CHAM_DEV void row_codes(const float (&v)[NCH][4], const RowParams& p, const float (&b32)[NCH],
-                        const float (&b64)[NCH], int code_bits, uint32_t (&cws)[NCH]) {
+                        const float (&b64)[NCH], const NF4Cell* cells, int code_bits, uint32_t (&cws)[NCH]) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         uint32_t cw = 0;
+        if (F == CHAM_W_MXFP4 || F == CHAM_W_FP4) {
+            // hardware converter: two codes per byte, even element in the low nibble
+            uint32_t c01, c23;
+            if (F == CHAM_W_MXFP4) {
+                const float sc = e8m0_scale(mx_exponent(b32[c], 2));
+                c01 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v[c][0], v[c][1], sc, 0) & 0xFFu;
+                c23 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v[c][2], v[c][3], sc, 0) & 0xFFu;
+            } else {
+                c01 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v[c][0] * p.r_fp4, v[c][1] * p.r_fp4, 1.0f, 0) & 0xFFu;
+                c23 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v[c][2] * p.r_fp4, v[c][3] * p.r_fp4, 1.0f, 0) & 0xFFu;
+            }
+            if (code_bits == 4) cw = c01 | (c23 << 8);
+            else cw = (c01 & 15u) | ((c01 >> 4) << 8) | ((c23 & 15u) << 16) | ((c23 >> 4) << 24);
+        } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            float wh;
-            uint32_t code = quant_one<F>(v[c][j], p, b32[c], b64[c], &wh);
-            cw |= code_bits == 4 ? (code & 15u) << (4 * j) : (code & 255u) << (8 * j);
+            for (int j = 0; j < 4; ++j) {
+                float wh;
+                uint32_t code = quant_one<F>(v[c][j], p, b32[c], b64[c], cells, &wh);
+                cw |= code_bits == 4 ? (code & 15u) << (4 * j) : (code & 255u) << (8 * j);
+            }
         }
         cws[c] = cw;
     }
 }
 
-// Squared reconstruction error of one element in format F, accumulated in binary64.  The
-// square of a binary32 difference is exact in binary64, so fma(d, d, e) == e + d*d.
-template <int F>
-CHAM_DEV void acc_err(float w, const RowParams& p, float blk32, float blk64, double& e) {
-    float wh;
-    (void)quant_one<F>(w, p, blk32, blk64, &wh);
-    const double d = (double)(w - wh);
-    e = fma(d, d, e);
+template <int F, int NCH>
+CHAM_DEV double row_err64(const float (&v)[NCH][4], const bool (&valid)[NCH], const RowParams& p,
+                          const float (&b32)[NCH], const float (&b64)[NCH], const NF4Cell* cells) {
+    double e = 0.0;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!valid[c]) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float wh;
+            (void)quant_one<F>(v[c][j], p, b32[c], b64[c], cells, &wh);
+            const double d = (double)(v[c][j] - wh);
+            e = fma(d, d, e);
+        }
+    }
+    return wave_sum(e);
 }
 
 CHAM_DEV float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 
 template <uint32_t MASK, int NCH>
 __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
+    __shared__ NF4Cell cells[33];
+    nf4_cells_init(cells);
+    __syncthreads();
+
     const int lane = threadIdx.x & 63;
     const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (n >= a.N) return;  // wave-uniform
     const int K = a.K;
     const int nq = K >> 2;  // float4 per row
     const float* row = a.W + n * (int64_t)K;
+    const uint32_t mask = MASK ? MASK : a.mask;
 
     float v[NCH][4];
     bool valid[NCH];
@@ -149,17 +342,16 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     float b32[NCH], b64[NCH];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        float m = 0.0f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            m = fmaxf(m, fabsf(v[c][j]));
-            if (valid[c]) { lo = fminf(lo, v[c][j]); hi = fmaxf(hi, v[c][j]); }
+        float m = fmaxf(fmaxf(fabsf(v[c][0]), fabsf(v[c][1])), fmaxf(fabsf(v[c][2]), fabsf(v[c][3])));
+        if (valid[c]) {
+            lo = fminf(lo, fminf(fminf(v[c][0], v[c][1]), fminf(v[c][2], v[c][3])));
+            hi = fmaxf(hi, fmaxf(fmaxf(v[c][0], v[c][1]), fmaxf(v[c][2], v[c][3])));
         }
-        b32[c] = group_max<8>(m);
-        b64[c] = fmaxf(b32[c], __shfl_xor(b32[c], 8, kWave));
+        b32[c] = max8(m);
+        b64[c] = max16_from8(b32[c]);
     }
-    lo = wave_min(lo);
-    hi = wave_max(hi);
+    lo = wave_min_dpp(lo);
+    hi = wave_max_dpp(hi);
     const float amax = fmaxf(fabsf(lo), fabsf(hi));
 
     RowParams p;
@@ -174,39 +366,68 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     }
     p.s_fp4 = floor_scale(amax / 6.0f); p.r_fp4 = 1.0f / p.s_fp4;
 
-    // ---- error of every enabled format: one fused pass over the row held in registers
-    const uint32_t mask = MASK ? MASK : a.mask;
-    double e[CHAM_W_NFMT];
+    // ---- binary32 error sums of every enabled format, one fused pass
+    float e[CHAM_W_NFMT];
 #pragma unroll
-    for (int f = 0; f < CHAM_W_NFMT; ++f) e[f] = 0.0;
+    for (int f = 0; f < CHAM_W_NFMT; ++f) e[f] = 0.0f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!valid[c]) continue;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float w = v[c][j];
-            if (mask & (1u << 0)) acc_err<0>(w, p, b32[c], b64[c], e[0]);
-            if (mask & (1u << 1)) acc_err<1>(w, p, b32[c], b64[c], e[1]);
-            if (mask & (1u << 2)) acc_err<2>(w, p, b32[c], b64[c], e[2]);
-            if (mask & (1u << 3)) acc_err<3>(w, p, b32[c], b64[c], e[3]);
-            if (mask & (1u << 4)) acc_err<4>(w, p, b32[c], b64[c], e[4]);
-            if (mask & (1u << 5)) acc_err<5>(w, p, b32[c], b64[c], e[5]);
-            if (mask & (1u << 6)) acc_err<6>(w, p, b32[c], b64[c], e[6]);
-            if (mask & (1u << 7)) acc_err<7>(w, p, b32[c], b64[c], e[7]);
-            if (mask & (1u << 8)) acc_err<8>(w, p, b32[c], b64[c], e[8]);
-        }
+        if (mask & (1u << 0)) e[0] += chunk_err<0>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 1)) e[1] += chunk_err<1>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 2)) e[2] += chunk_err<2>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 3)) e[3] += chunk_err<3>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 4)) e[4] += chunk_err<4>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 5)) e[5] += chunk_err<5>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 6)) e[6] += chunk_err<6>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 7)) e[7] += chunk_err<7>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 8)) e[8] += chunk_err<8>(v[c], p, b32[c], b64[c], cells);
     }
-    int best = -1;
-    double best_err = 0.0;
+    int best = -1, second = -1;
+    float eb = 0.0f, es = 0.0f;
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) {
-        if (!(mask & (1u << f))) {
-            if (a.err && lane == 0) a.err[n * CHAM_W_NFMT + f] = -1.0;
-            continue;
+        if (!(mask & (1u << f))) continue;
+        e[f] = wave_sum_dpp(e[f]);
+        if (best < 0 || e[f] < eb) {
+            second = best; es = eb;
+            best = f; eb = e[f];
+        } else if (second < 0 || e[f] < es) {
+            second = f; es = e[f];
         }
-        const double ef = wave_sum(e[f]);
-        if (a.err && lane == 0) a.err[n * CHAM_W_NFMT + f] = ef;
-        if (best < 0 || ef < best_err) { best = f; best_err = ef; }
+    }
+    double ed[CHAM_W_NFMT];
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) ed[f] = (double)e[f];
+    // ---- near tie (or exact tie), or sums outside binary32's comfortable range (tiny or
+    // huge rows): binary64 re-check of every enabled format
+    if (second >= 0 && (!(es - eb > 0x1p-12f * es) || !(eb > 0x1p-100f) || !(es < 0x1p100f))) {
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            if (!(mask & (1u << f))) continue;
+            switch (f) {
+            case 0: ed[0] = row_err64<0, NCH>(v, valid, p, b32, b64, cells); break;
+            case 1: ed[1] = row_err64<1, NCH>(v, valid, p, b32, b64, cells); break;
+            case 2: ed[2] = row_err64<2, NCH>(v, valid, p, b32, b64, cells); break;
+            case 3: ed[3] = row_err64<3, NCH>(v, valid, p, b32, b64, cells); break;
+            case 4: ed[4] = row_err64<4, NCH>(v, valid, p, b32, b64, cells); break;
+            case 5: ed[5] = row_err64<5, NCH>(v, valid, p, b32, b64, cells); break;
+            case 6: ed[6] = row_err64<6, NCH>(v, valid, p, b32, b64, cells); break;
+            case 7: ed[7] = row_err64<7, NCH>(v, valid, p, b32, b64, cells); break;
+            default: ed[8] = row_err64<8, NCH>(v, valid, p, b32, b64, cells); break;
+            }
+        }
+        best = -1;
+        double bd = 0.0;
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            if (!(mask & (1u << f))) continue;
+            if (best < 0 || ed[f] < bd) { best = f; bd = ed[f]; }
+        }
+    }
+    if (a.err && lane == 0) {
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) a.err[n * CHAM_W_NFMT + f] = (mask & (1u << f)) ? ed[f] : -1.0;
     }
 
     // ---- emit the winner's codes and metadata
@@ -226,15 +447,15 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     const bool is_mx = f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4;
     uint32_t cws[NCH];
     switch (f) {
-    case 0: row_codes<0, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 1: row_codes<1, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 2: row_codes<2, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 3: row_codes<3, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 4: row_codes<4, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 5: row_codes<5, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 6: row_codes<6, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    case 7: row_codes<7, NCH>(v, p, b32, b64, a.code_bits, cws); break;
-    default: row_codes<8, NCH>(v, p, b32, b64, a.code_bits, cws); break;
+    case 0: row_codes<0, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 1: row_codes<1, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 2: row_codes<2, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 3: row_codes<3, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 4: row_codes<4, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 5: row_codes<5, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 6: row_codes<6, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 7: row_codes<7, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    default: row_codes<8, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
     }
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
@@ -338,6 +559,7 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     if (nf4 && K % 64 != 0) return CHAM_ESHAPE;
     if (!wq->fmt || !wq->codes || !wq->scale || !wq->zero) return CHAM_EINVAL;
     if ((nf4 && !wq->nf4_absmax) || (mx && !wq->e8m0)) return CHAM_EINVAL;
+    if (((uintptr_t)W & 15u) || ((uintptr_t)wq->codes & 3u)) return CHAM_EINVAL;
     if (K > 32 * 256) return CHAM_ESHAPE;  // rows up to 8192 are held in registers
     wq->code_bits = mask_code_bits(mask);
 

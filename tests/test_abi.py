@@ -40,6 +40,7 @@ def test_host_only_helpers():
     assert cham.workspace_bytes(cham.OP_STATS, 1 << 20, 0, 0) > 0
     assert cham.workspace_bytes(cham.OP_QUANT_ACT, 2048, 0, 1280) > 0
     assert cham.workspace_bytes(cham.OP_SELECT, 10, 10, 64) == 0
+    assert cham.workspace_bytes(cham.OP_LINEAR, 2048, 1280, 1280) >= 2048 * 1280 * 2 + 2048 * 4
 
 
 def _wq(**kw):
@@ -80,7 +81,7 @@ def test_other_argument_errors():
     assert L.cham_quantize_act(P(16), 1, 0, None, None, ctypes.byref(aq), None, 0, None) == cham.EINVAL
     assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aq), None, 0, None) == cham.EWORKSPACE
     w = _wq(code_bits=4)
-    aqk = cham._AQ(4, 128, 1, P(16), P(16), P(16), P(16))
+    aqk = cham._AQ(4, 128, 1, P(16), P(16), P(16), P(16))  # K = 128 vs wq K = 64
     assert L.cham_mixed_linear(ctypes.byref(aqk), ctypes.byref(w), P(16), None, 0, None) == cham.EINVAL  # K mismatch
     aqf = cham._AQ(4, 64, 9, P(16), P(16), P(16), P(16))
     assert L.cham_mixed_linear(ctypes.byref(aqf), ctypes.byref(w), P(16), None, 0, None) == cham.EFORMAT

@@ -50,7 +50,8 @@ def _assert_search_equal(wq, ref, check_perm=True):
         assert np.array_equal(_np(wq.group_off), ref["group_off"])
     if wq.err is not None and ref["err"] is not None:
         g, r = _np(wq.err), ref["err"]
-        assert np.allclose(g, r, rtol=1e-9, atol=0), np.max(np.abs(g - r) / np.maximum(np.abs(r), 1e-300))
+        # binary32 sums unless a near tie forced the binary64 re-check (documented accuracy 1e-5)
+        assert np.allclose(g, r, rtol=1e-5, atol=1e-30), np.max(np.abs(g - r) / np.maximum(np.abs(r), 1e-300))
 
 
 # ---------------------------------------------------------------------------------------
