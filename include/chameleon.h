@@ -175,7 +175,8 @@ typedef struct cham_lut {
  * SNR = alpha_bar/(1 - alpha_bar) (Sec. 3.1, Eq. snr); Route (Sec. 4.3): shortcut -> 3,
  * kappa > hi or SNR < lo -> 2, kappa <= lo and SNR > hi -> 0, else 1; ScaleZP (App. A.7) on
  * the bucket's [lo, hi] (an empty bucket gets S = 1, Z = 0).  is_shortcut: device [L] or
- * NULL.  kappa: device [L*B] binary64 or NULL.  lut->L, B must equal st's; lut->T = sch->T.
+ * NULL.  kappa: device [L*B] binary64 or NULL.  lut->L, B must equal st's (B <= 1024); lut->T
+ * is set to sch->T.  The SNR product is evaluated as a tree of binary64 products.
  * Errors: CHAM_EINVAL, CHAM_EHIP. */
 int cham_build_act_lut(const cham_act_stats* st, const cham_schedule* sch,
                        const uint8_t* is_shortcut, cham_lut* lut, double* kappa, void* stream);
@@ -225,8 +226,10 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  * quantizers above define them, accumulated in binary32 on the matrix cores.  Accuracy:
  * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element (NF4 levels are carried at half
  * precision; every other operand is exact).  xq->K must equal wq->K and be a multiple of
- * 64; xq->codes and wq->codes must be 16-byte aligned.  Y [M][N] is written in the original
- * channel order.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of the decoded
+ * 64; xq->codes, wq->codes and Y must be 16-byte aligned.  Y [M][N] is written in the
+ * original channel order.  When the output has too few 256x256/128x128 tiles to fill the
+ * GPU, K is split across workgroups whose partial sums are added into Y with binary32
+ * atomics (Y is zeroed first), so such outputs are not bitwise reproducible run to run.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of the decoded
  * activations and per-row scales), 256-byte aligned.
  * Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE, CHAM_EWORKSPACE, CHAM_EHIP.
  * ------------------------------------------------------------------------------------- */

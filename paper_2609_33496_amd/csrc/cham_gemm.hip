@@ -2,51 +2,83 @@
 // weight format (Sec. 4.5) and one activation format per call (Sec. 4.3).
 //
 // Per-channel formats do not map onto one native MFMA operand type (Sec. 6), so the
-// weights are dequantized on the fly into a common half-precision operand: every code of
-// every 4-bit format becomes an entry of a 16-value table built per (channel, scale block)
-// -- base value (NF4 level, E2M1 value, integer, q - z) times the block factor (NF4 block
-// absmax, MX 2^E) relative to the channel's largest block, rounded once to half precision.
-// The table lives in registers as two byte planes and is read with v_perm_b32, so decoding
-// needs no LDS traffic.  Integers, E2M1 values and MX mantissas are exact in half precision;
-// NF4 levels times their block absmax carry one rounding (relative error <= 2^-11).  8-bit
-// integer formats are decoded arithmetically (1024 + c trick, exact).
+// weights are dequantized on the fly into a common half-precision operand.  Every 4-bit
+// code of every format is an entry of a 16-value decode table per (k-step of 64, channel,
+// half k-step of 32): base value (NF4 level, E2M1 value, integer, q - z) times the block
+// factor (NF4 block absmax, MX 2^E) relative to the channel's largest block, rounded once
+// to half precision.  A pre-pass packs, per (k-step, channel, half), the codes and this
+// table (two byte planes) into one record; the main kernel decodes with v_perm_b32, so
+// every 4-bit format decodes with the same instructions.  Integers, E2M1 values and MX
+// mantissas are exact in half precision; NF4 levels times their block absmax carry one
+// rounding (relative error <= 2^-11).  8-bit integer formats are decoded arithmetically
+// (1024 + c trick, exact) with parameters from the same table slot.
 //
-// Activations are decoded once per call by a small pre-pass into a half-precision copy in
-// the workspace (exact for every activation format), with the per-row scale.  The main
-// kernel tiles BM x BN x 64 over 4 wavefronts (2 x 2), runs v_mfma_f32_32x32x16_f16 with
-// binary32 accumulation, streams the activation tile through double-buffered LDS, and keeps
-// each wavefront's weight operand in registers.  Inside a tile the output channels are
-// sorted by format, so a 32-channel MFMA column block almost always decodes one format
-// (wave-uniform branches); every output line of the tile is still written by the tile.
+// The same pre-pass decodes the activations once per call into a half-precision copy in
+// the workspace (exact for every activation format) with a per-row scale.
 //
-// The MFMA contracts over k in any order as long as both operands agree: a lane's 8 values
-// of one k-step are the codes of 8 consecutive k in the order (0,2,4,6,1,3,5,7) when codes
-// are packed two per byte (even/odd nibbles), and the activation copy stores its columns in
-// that same order.
+// Main kernel: BM x 256 output tiles (BM = 256, 128 or 64), k-steps of 64, four
+// wavefronts that each own BM rows x 64 channels (BM/32 x 2 blocks of
+// v_mfma_f32_32x32x16_f16, binary32 accumulation), so a decoded weight feeds BM/16 MFMAs.
+// The activation tile and the weight records of step k + 2 go global -> registers with
+// coalesced 16-byte loads while step k computes, and into one of two LDS buffers at the
+// end of step k + 1; the activation tile is stored with its 16-byte chunks XOR-swizzled
+// per row pair and the records piece-major, so all LDS reads are free of bank conflicts.
+// Barriers fence LDS only, so the prefetch stays in flight across them.  Each output
+// element is written once (no atomics), so results do not depend on scheduling.
+//
+// The MFMA contracts over k in any order as long as both operands agree: lane half h of a
+// k-step takes k = 32h .. 32h+31, sub-step s the 8 k at 32h + 8s, and with two codes per
+// byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation copy stores its
+// columns in that same order.
 #include "cham_device.h"
 
 namespace cham {
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
-constexpr int BK = 64;
-constexpr int LDA = BK + 8;  // LDS row stride of the activation tile (halves)
+constexpr int BN = 256, BK = 64;
+constexpr int kThreads = 256;
+constexpr int TN = 2;                     // 32-channel MFMA blocks per wavefront
+constexpr int kBufferFlags = 0x00020000;  // buffer descriptor word 3: 32-bit data, raw
+
+CHAM_DEV bool is_mx(int f) { return f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4; }
+CHAM_DEV bool is_8bit(int f) { return f == CHAM_W_INT8_SYM || f == CHAM_W_INT8_ASYM || f == CHAM_W_MXINT8; }
+CHAM_DEV int mx_F(int f) { return f == CHAM_W_MXINT8 ? 6 : (f == CHAM_W_MXINT4 ? 2 : 0); }
+
+// Per-channel parameters, computed by the pre-pass for every output channel.
+struct ColPrep {
+    int fmt;         // CHAM_W_NFMT: not a valid format of the palette (decodes as zero)
+    int eref;        // exponent removed from block-scaled values (NF4 / MX), 0 otherwise
+    float zero;      // INT-asym zero point
+    float colscale;  // epilogue factor: INT/FP4 scale, or 2^eref
+};
 
 // ------------------------------------------------------------------------------------
-// activation pre-pass: codes -> half precision (exact), k permuted within groups of 8
+// pre-pass 1: activations -> half precision; channel parameters
 // ------------------------------------------------------------------------------------
-struct DecodeArgs {
+struct PrepArgs {
+    // activations
     const uint8_t* xc;
     const uint8_t* xe8;
     const float* xs;
     const float* xz;
     int afmt;
     int M, K;
-    int perm4;  // 1: store each group of 8 columns in the order 0,2,4,6,1,3,5,7
+    int perm4;  // 1: store each group of 8 columns in the order 0,4,1,5,2,6,3,7
     _Float16* Xh;
     float* rowscale;
+    // channels
+    const uint8_t* wfmt;
+    const float* wscale;
+    const int32_t* wzero;
+    const float* wnf4;
+    const uint8_t* we8;
+    int N;
+    uint32_t mask;
+    ColPrep* cols;
 };
 
 CHAM_DEV float adecode(int afmt, uint32_t c, float z, int kblk_e, int eref) {
@@ -59,73 +91,50 @@ CHAM_DEV float adecode(int afmt, uint32_t c, float z, int kblk_e, int eref) {
     }
 }
 
-// Per-channel decode parameters, computed by the pre-pass for every output channel.
-struct ColPrep {
-    int fmt;         // CHAM_W_NFMT: not a valid format of the palette (decodes as zero)
-    int eref;        // exponent removed from block-scaled values (NF4 / MX), 0 otherwise
-    float zero;      // INT-asym zero point
-    float colscale;  // epilogue factor: INT/FP4 scale, or 2^eref
-};
+constexpr int kColsPerBlock = 4;  // one wavefront per channel
 
-struct PrepArgs {
-    DecodeArgs d;
-    const uint8_t* wfmt;
-    const float* wscale;
-    const int32_t* wzero;
-    const float* wnf4;
-    const uint8_t* we8;
-    int N;
-    uint32_t mask;
-    ColPrep* cols;
-};
-
-// Workgroups [0, M): activation row m -> half precision.  Workgroups [M, M + ceil(N/256)):
-// one thread per output channel computes its ColPrep.
+// Workgroups [0, M): activation row m.  Next ceil(N/4): one wavefront per channel reduces
+// its block metadata to the channel's reference exponent.
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
-    const DecodeArgs& a = p.d;
-    if ((int)blockIdx.x >= a.M) {
-        const int n = ((int)blockIdx.x - a.M) * 256 + (int)threadIdx.x;
+    const int K = p.K;
+    const int bid = (int)blockIdx.x;
+    if (bid >= p.M) {
+        const int lane = threadIdx.x & 63;
+        const int n = (bid - p.M) * kColsPerBlock + (int)(threadIdx.x >> 6);
         if (n >= p.N) return;
-        const int K = a.K;
         ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
         const int f = p.wfmt[n];
         if (f < CHAM_W_NFMT && ((p.mask >> f) & 1u)) {
             c.fmt = f;
             c.zero = (float)p.wzero[n];
             if (f == CHAM_W_NF4) {
-                float mx = 0.0f;
                 const float* r = p.wnf4 + (int64_t)n * (K / 64);
-#pragma unroll 8
-                for (int b = 0; b < K / 64; ++b) mx = fmaxf(mx, r[b]);
+                float mx = 0.0f;
+                for (int b = lane; b < K / 64; b += 64) mx = fmaxf(mx, r[b]);
+                mx = wave_max(mx);
                 c.eref = floor_log2(floor_scale(mx));
                 c.colscale = ldexpf(1.0f, c.eref);
-            } else if (f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4) {
+            } else if (is_mx(f)) {
+                const uint8_t* r = p.we8 + (int64_t)n * (K / 32);
                 int mx = 0;
-                const uint32_t* r = reinterpret_cast<const uint32_t*>(p.we8 + (int64_t)n * (K / 32));
-#pragma unroll 8
-                for (int b = 0; b < K / 128; ++b) {
-                    const uint32_t w = r[b];
-                    mx = max(mx, (int)max(max(w & 255u, (w >> 8) & 255u), max((w >> 16) & 255u, w >> 24)));
-                }
-                for (int b = (K / 128) * 4; b < K / 32; ++b) mx = max(mx, (int)p.we8[(int64_t)n * (K / 32) + b]);
-                const int F = f == CHAM_W_MXINT8 ? 6 : (f == CHAM_W_MXINT4 ? 2 : 0);
-                c.eref = mx - 127 - F;
+                for (int b = lane; b < K / 32; b += 64) mx = max(mx, (int)r[b]);
+                for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o, kWave));
+                c.eref = mx - 127 - mx_F(f);
                 c.colscale = ldexpf(1.0f, c.eref);
             } else {
                 c.colscale = p.wscale[n];
             }
         }
-        p.cols[n] = c;
+        if (lane == 0) p.cols[n] = c;
         return;
     }
-    const int m = blockIdx.x;
-    const int K = a.K;
-    const bool mx = a.afmt == CHAM_A_MXFP8_E4M3 || a.afmt == CHAM_A_MXINT8;
+    const int m = bid;
+    const bool mx = p.afmt == CHAM_A_MXFP8_E4M3 || p.afmt == CHAM_A_MXINT8;
     __shared__ int sh_e;
     int eref = 0;
     if (mx) {
         int mx_e = 0;
-        for (int b = threadIdx.x; b < K / 32; b += blockDim.x) mx_e = max(mx_e, (int)a.xe8[(int64_t)m * (K / 32) + b]);
+        for (int b = threadIdx.x; b < K / 32; b += blockDim.x) mx_e = max(mx_e, (int)p.xe8[(int64_t)m * (K / 32) + b]);
         for (int o = 32; o > 0; o >>= 1) mx_e = max(mx_e, __shfl_xor(mx_e, o, kWave));
         if (threadIdx.x == 0) sh_e = 0;
         __syncthreads();
@@ -133,107 +142,141 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
         __syncthreads();
         eref = sh_e - 127;
     }
-    const float z = *a.xz;
-    const uint8_t* row = a.xc + (int64_t)m * K;
-    _Float16* out = a.Xh + (int64_t)m * K;
+    const float z = *p.xz;
+    const uint8_t* row = p.xc + (int64_t)m * K;
+    _Float16* out = p.Xh + (int64_t)m * K;
     for (int g = threadIdx.x; g < K / 8; g += blockDim.x) {
         const uint2 c2 = *reinterpret_cast<const uint2*>(row + 8 * g);
-        const int kb = mx ? (int)a.xe8[(int64_t)m * (K / 32) + (g >> 2)] - 127 : 0;
+        const int kb = mx ? (int)p.xe8[(int64_t)m * (K / 32) + (g >> 2)] - 127 : 0;
         float v[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             uint32_t c = ((j < 4 ? c2.x : c2.y) >> (8 * (j & 3))) & 0xFFu;
-            v[j] = adecode(a.afmt, c, z, kb, eref);
+            v[j] = adecode(p.afmt, c, z, kb, eref);
         }
         half8 h;
-        if (a.perm4) {
-            h[0] = (_Float16)v[0]; h[1] = (_Float16)v[2]; h[2] = (_Float16)v[4]; h[3] = (_Float16)v[6];
-            h[4] = (_Float16)v[1]; h[5] = (_Float16)v[3]; h[6] = (_Float16)v[5]; h[7] = (_Float16)v[7];
+        if (p.perm4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[2 * j] = (_Float16)v[j];
+                h[2 * j + 1] = (_Float16)v[j + 4];
+            }
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j) h[j] = (_Float16)v[j];
         }
         *reinterpret_cast<half8*>(out + 8 * g) = h;
     }
-    if (threadIdx.x == 0) a.rowscale[m] = mx ? ldexpf(1.0f, eref) : *a.xs;
+    if (threadIdx.x == 0) p.rowscale[m] = mx ? ldexpf(1.0f, eref) : *p.xs;
 }
 
 // ------------------------------------------------------------------------------------
-// main kernel
+// pre-pass 2: weight records, one per (k-step, channel, half k-step): the half's codes
+// (16 bytes at 4 bits, 32 at 8 bits) followed by its 32-byte decode table
 // ------------------------------------------------------------------------------------
-struct GemmArgs {
-    const _Float16* Xh;      // [M][K] (column order as above)
-    const float* rowscale;   // [M]
-    const ColPrep* cols;     // [N]
-    const uint8_t* wc;       // codes
-    const float* wnf4;       // [N][K/64]
-    const uint8_t* we8;      // [N][K/32]
-    float* Y;
-    int M, N, K;
-};
-
-struct ColInfo {
-    int n;           // channel index (-1: padding / invalid)
-    int fmt;
-    int eref;
-    float zero;
-    float colscale;
-};
-
-CHAM_DEV bool is_mx(int f) { return f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4; }
-CHAM_DEV bool is_8bit(int f) { return f == CHAM_W_INT8_SYM || f == CHAM_W_INT8_ASYM || f == CHAM_W_MXINT8; }
 
 // 16-entry half-precision table as byte planes: lo[j] holds the low bytes of entries
-// 4j..4j+3, hi[j] the high bytes.
+// 4j..4j+3, hi[j] the high bytes.  8-bit integer formats use the same 32 bytes for
+// {xor mask, -(1024 + zero offset) and the block factor as half pairs}.
 struct Table {
     uint32_t lo[4], hi[4];
 };
 
-CHAM_DEV void table_from_values(Table& t, const float (&v)[16]) {
-    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        h2 a01, a23;
-        a01.x = (_Float16)v[4 * j + 0]; a01.y = (_Float16)v[4 * j + 1];
-        a23.x = (_Float16)v[4 * j + 2]; a23.y = (_Float16)v[4 * j + 3];
-        const uint32_t w01 = __builtin_bit_cast(uint32_t, a01), w23 = __builtin_bit_cast(uint32_t, a23);
-        t.lo[j] = __builtin_amdgcn_perm(w23, w01, 0x06040200u);
-        t.hi[j] = __builtin_amdgcn_perm(w23, w01, 0x07050301u);
-    }
-}
-
-// Base values of the 4-bit codes of each format (before the block factor).
 CHAM_DEV float e2m1_value(int c) {
     const float m[8] = {0.0f, 0.5f, 1.0f, 1.5f, 2.0f, 3.0f, 4.0f, 6.0f};
     return (c & 8) ? -m[c & 7] : m[c & 7];
 }
 
 template <int F>
-CHAM_DEV void table_fmt(Table& t, float zero, float factor) {
-    float v[16];
+CHAM_DEV Table table_fmt(float zero, float factor) {
+    Table t;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-        float b;
-        if (F == CHAM_W_NF4) b = nf4_level(c);
-        else if (F == CHAM_W_FP4 || F == CHAM_W_MXFP4) b = e2m1_value(c);
-        else if (F == CHAM_W_INT4_ASYM) b = (float)c - zero;
-        else b = (float)(c < 8 ? c : c - 16);  // INT4-sym, MXINT4
-        v[c] = b * factor;
+    for (int j = 0; j < 4; ++j) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int c = 4 * j + e;
+            float b;
+            if (F == CHAM_W_NF4) b = nf4_level(c);
+            else if (F == CHAM_W_FP4 || F == CHAM_W_MXFP4) b = e2m1_value(c);
+            else if (F == CHAM_W_INT4_ASYM) b = (float)c - zero;
+            else b = (float)(c < 8 ? c : c - 16);  // INT4-sym, MXINT4
+            v[e] = b * factor;
+        }
+        half2v a01, a23;
+        a01.x = (_Float16)v[0]; a01.y = (_Float16)v[1];
+        a23.x = (_Float16)v[2]; a23.y = (_Float16)v[3];
+        const uint32_t w01 = __builtin_bit_cast(uint32_t, a01), w23 = __builtin_bit_cast(uint32_t, a23);
+        t.lo[j] = __builtin_amdgcn_perm(w23, w01, 0x06040200u);
+        t.hi[j] = __builtin_amdgcn_perm(w23, w01, 0x07050301u);
     }
-    table_from_values(t, v);
+    return t;
 }
 
-// Table of channel format f (4-bit) with block factor `factor` (branches are wave-uniform
-// whenever the 32 channels of an MFMA column block share a format).
-CHAM_DEV void build_table(Table& t, int f, float zero, float factor) {
-    switch (f) {
-    case CHAM_W_NF4: table_fmt<CHAM_W_NF4>(t, zero, factor); break;
-    case CHAM_W_FP4: table_fmt<CHAM_W_FP4>(t, zero, factor); break;
-    case CHAM_W_MXFP4: table_fmt<CHAM_W_MXFP4>(t, zero, factor); break;
-    case CHAM_W_INT4_ASYM: table_fmt<CHAM_W_INT4_ASYM>(t, zero, factor); break;
-    default: table_fmt<CHAM_W_INT4_SYM>(t, zero, factor); break;
-    }
+CHAM_DEV uint32_t half_pair(float v) {
+    half2v p;
+    p.x = (_Float16)v;
+    p.y = p.x;
+    return __builtin_bit_cast(uint32_t, p);
 }
+
+CHAM_DEV Table int8_record(uint32_t xmask, float zoff, float factor) {
+    return Table{{xmask, half_pair(-(1024.0f + zoff)), half_pair(factor), 0u}, {0u, 0u, 0u, 0u}};
+}
+
+struct RecArgs {
+    const ColPrep* cols;
+    const float* wnf4;
+    const uint8_t* we8;
+    const uint8_t* wc;
+    int N, K, code_bits;
+    uint4* rec;  // [K/64][N][2][pieces]
+};
+
+// One thread per (k-step, channel, half).
+__global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
+    const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = (int64_t)(a.K / BK) * a.N * 2;
+    if (id >= total) return;
+    const int h = (int)(id & 1);
+    const int n = (int)((id >> 1) % a.N);
+    const int k = (int)((id >> 1) / a.N);
+    const ColPrep c = a.cols[n];
+    Table t;
+    switch (c.fmt) {
+    case CHAM_W_NF4:
+        t = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(a.wnf4[(int64_t)n * (a.K / 64) + k], -c.eref));
+        break;
+    case CHAM_W_MXFP4:
+    case CHAM_W_MXINT4:
+    case CHAM_W_MXINT8: {
+        const int e = a.we8[(int64_t)n * (a.K / 32) + 2 * k + h];
+        const float factor = ldexpf(1.0f, e - 127 - mx_F(c.fmt) - c.eref);
+        if (c.fmt == CHAM_W_MXFP4) t = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
+        else if (c.fmt == CHAM_W_MXINT4) t = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
+        else t = int8_record(0x80808080u, 128.0f, factor);
+        break;
+    }
+    case CHAM_W_FP4: t = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
+    case CHAM_W_INT4_ASYM: t = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
+    case CHAM_W_INT4_SYM: t = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
+    case CHAM_W_INT8_SYM: t = int8_record(0x80808080u, 128.0f, 1.0f); break;
+    case CHAM_W_INT8_ASYM: t = int8_record(0u, c.zero, 1.0f); break;
+    default: t = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
+    }
+    const int cw = a.code_bits / 4;  // 16-byte code pieces per half k-step
+    const int64_t cstride = (int64_t)a.K * a.code_bits / 8;
+    const uint4* src = reinterpret_cast<const uint4*>(a.wc + n * cstride + (int64_t)k * (16 * a.code_bits / 2) +
+                                                      (int64_t)h * 16 * cw);
+    uint4* dst = a.rec + id * (cw + 2);
+    for (int q = 0; q < cw; ++q) dst[q] = src[q];
+    dst[cw] = make_uint4(t.lo[0], t.lo[1], t.lo[2], t.lo[3]);
+    dst[cw + 1] = make_uint4(t.hi[0], t.hi[1], t.hi[2], t.hi[3]);
+}
+
+// ------------------------------------------------------------------------------------
+// weight decode in the main kernel
+// ------------------------------------------------------------------------------------
 
 // Look up 4 codes (one per byte, values 0..15); returns the low and high bytes.
 CHAM_DEV void lookup4(const Table& t, uint32_t codes, uint32_t& lo, uint32_t& hi) {
@@ -252,16 +295,16 @@ union H8 {
     uint32_t u[4];
 };
 
-// 8 codes of one k-step from a word of 8 nibbles -> order (0,2,4,6,1,3,5,7)
+// 8 codes of one sub-step from a word of 8 nibbles -> order (0,4,1,5,2,6,3,7)
 CHAM_DEV half8 decode_nibbles(const Table& t, uint32_t w) {
     uint32_t lo_e, hi_e, lo_o, hi_o;
-    lookup4(t, w & 0x0F0F0F0Fu, lo_e, hi_e);
-    lookup4(t, (w >> 4) & 0x0F0F0F0Fu, lo_o, hi_o);
+    lookup4(t, w & 0x0F0F0F0Fu, lo_e, hi_e);         // k = 0, 2, 4, 6
+    lookup4(t, (w >> 4) & 0x0F0F0F0Fu, lo_o, hi_o);  // k = 1, 3, 5, 7
     H8 r;
-    r.u[0] = __builtin_amdgcn_perm(hi_e, lo_e, 0x05010400u);
-    r.u[1] = __builtin_amdgcn_perm(hi_e, lo_e, 0x07030602u);
-    r.u[2] = __builtin_amdgcn_perm(hi_o, lo_o, 0x05010400u);
-    r.u[3] = __builtin_amdgcn_perm(hi_o, lo_o, 0x07030602u);
+    r.u[0] = __builtin_amdgcn_perm(hi_e, lo_e, 0x06020400u);  // k0, k4
+    r.u[1] = __builtin_amdgcn_perm(hi_o, lo_o, 0x06020400u);  // k1, k5
+    r.u[2] = __builtin_amdgcn_perm(hi_e, lo_e, 0x07030501u);  // k2, k6
+    r.u[3] = __builtin_amdgcn_perm(hi_o, lo_o, 0x07030501u);  // k3, k7
     return r.h;
 }
 
@@ -278,76 +321,141 @@ CHAM_DEV half8 decode_bytes_table(const Table& t, uint32_t w0, uint32_t w1) {
     return r.h;
 }
 
-// 8-bit integer codes: value = ((c ^ x) - zoff) * factor, through 1024 + c in half precision
-CHAM_DEV half8 decode_bytes_int(uint32_t w0, uint32_t w1, uint32_t xmask, _Float16 negoff, _Float16 factor) {
-    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-    w0 ^= xmask;
-    w1 ^= xmask;
+// 8-bit integer codes: value = ((c ^ x) - zoff) * factor, through 1024 + c in half
+// precision; x, -(1024 + zoff) and the factor come from the table slot.
+CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
+    w0 ^= t.lo[0];
+    w1 ^= t.lo[0];
     H8 r;
     r.u[0] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04010400u);
     r.u[1] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04030402u);
     r.u[2] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04010400u);
     r.u[3] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04030402u);
-    h2 off = {negoff, negoff}, fac = {factor, factor};
+    const half2v off = __builtin_bit_cast(half2v, t.lo[1]), fac = __builtin_bit_cast(half2v, t.lo[2]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        h2 v = __builtin_bit_cast(h2, r.u[i]);
+        half2v v = __builtin_bit_cast(half2v, r.u[i]);
         v = (v + off) * fac;
         r.u[i] = __builtin_bit_cast(uint32_t, v);
     }
     return r.h;
 }
 
-CHAM_DEV int mx_F(int f) { return f == CHAM_W_MXINT8 ? 6 : (f == CHAM_W_MXINT4 ? 2 : 0); }
+// Workgroup barrier that orders LDS accesses only: outstanding global loads (the
+// prefetch) stay in flight.
+CHAM_DEV void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int CODE_BITS>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_kernel(GemmArgs a) {
-    constexpr int kThreads = 64 * WAVES_M * WAVES_N;
-    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;  // wavefront tile
-    constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int A_CHUNKS = BM * BK * 2 / 16 / kThreads;  // 16-byte chunks per thread
-    static_assert(A_CHUNKS >= 1 && BN <= kThreads, "tile / workgroup mismatch");
-    __shared__ _Float16 As[2][BM][LDA];
-    __shared__ ColInfo cinfo[BN];
-    __shared__ uint64_t ballots[CHAM_W_NFMT + 1][kThreads / kWave];
+// ------------------------------------------------------------------------------------
+// main kernel
+// ------------------------------------------------------------------------------------
+struct GemmArgs {
+    const _Float16* Xh;      // [M][K] (column order as above)
+    const float* rowscale;   // [M]
+    const ColPrep* cols;     // [N]
+    const uint4* rec;        // [K/64][N][2][pieces]
+    float* Y;
+    int M, N, K;
+    int row0, row1;  // rows [row0, row1) of this launch
+    int tn;      // tile columns
+};
+
+template <int CODE_BITS, int TM>
+__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
+    constexpr int BM = 32 * TM;
+    constexpr int CW = CODE_BITS / 4;           // 16-byte code pieces per record
+    constexpr int P = CW + 2;                   // 16-byte pieces per record
+    constexpr int AQ = TM;                      // activation loads per thread per k-step
+    constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
+    __shared__ uint4 lds[2][A_CH];
+    __shared__ float Rs[BM];
 
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-    const int K = a.K;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int K = a.K, N = a.N;
+    const int nsteps = K / BK;
+    const int m0 = a.row0 + ((int)blockIdx.x / a.tn) * BM, n0 = ((int)blockIdx.x % a.tn) * BN;
+    const int rows = a.row1 - m0 < BM ? a.row1 - m0 : BM;
 
-    // ---- prologue: sort this tile's channels by format (ballot ranks, deterministic)
-    ColPrep cp{CHAM_W_NFMT, 0, 0.0f, 0.0f};
-    if (t < BN && n0 + t < a.N) cp = a.cols[n0 + t];
-    const int myf = t < BN ? cp.fmt : CHAM_W_NFMT + 1;
-    for (int f = 0; f <= CHAM_W_NFMT; ++f) {
-        const uint64_t b = __ballot(myf == f);
-        if (lane == 0) ballots[f][wave] = b;
-    }
-    __syncthreads();
-    if (t < BN) {
-        int pos = __popcll(ballots[myf][wave] & ((1ull << lane) - 1ull));
-        for (int w = 0; w < wave; ++w) pos += __popcll(ballots[myf][w]);
-        for (int f = 0; f < myf; ++f)
-            for (int w = 0; w < kThreads / kWave; ++w) pos += __popcll(ballots[f][w]);
-        ColInfo ci{-1, CHAM_W_INT4_SYM, 0, 0.0f, 0.0f};
-        if (myf < CHAM_W_NFMT) ci = ColInfo{n0 + t, myf, cp.eref, cp.zero, cp.colscale};
-        cinfo[pos] = ci;
-    }
-    __syncthreads();
+    if (t < BM) Rs[t] = a.rowscale[t < rows ? m0 + t : m0];
 
-    const int wm = (wave / WAVES_N) * WM, wn = (wave % WAVES_N) * WN;
-    const int g = lane >> 5;  // k-half of the lane within a k-step
-    ColInfo my[TN];
+    // ---- activation tile: global -> registers two k-steps ahead -> LDS, 16-byte loads
+    // through a buffer resource whose range check returns zeros past the last row.  Chunk
+    // slot q = 256 i + t holds tile row 32 i + (t >> 3), logical chunk
+    // (t & 7) ^ ((row >> 1) & 7).
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.Xh + (int64_t)m0 * K), (short)0, rows * K * 2, kBufferFlags);
+    const uint32_t aoff0 = (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4));
+    struct AStage {
+        uint4 v[AQ];
+    };
+    auto load_a = [&](AStage& S, int k) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) my[j] = cinfo[wn + j * 32 + (lane & 31)];
-
-    // channels whose table does not depend on the k-block: build once
-    Table tab[TN];
+        for (int i = 0; i < AQ; ++i)
+            S.v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                         ra, (int)(aoff0 + (uint32_t)(i * 64 * K + k * BK * 2)), 0, 0));
+    };
+    auto store_a = [&](const AStage& S, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-        if (!is_mx(my[j].fmt) && my[j].fmt != CHAM_W_NF4 && !is_8bit(my[j].fmt))
-            build_table(tab[j], my[j].fmt, my[j].zero, 1.0f);
+        for (int i = 0; i < AQ; ++i) lds[buf][i * 256 + t] = S.v[i];
+    };
+
+    // ---- weight records of the lane's channels (column l32 of the wave's two 32-channel
+    // blocks, half h): global -> registers one k-step ahead; past the last channel the
+    // range check returns zeros (zero codes, zero table)
+    const int nl = 64 * wave + l32;
+    const int chans = N - n0 < BN ? N - n0 : BN;
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(a.rec + (int64_t)n0 * 2 * P), (short)0, (int)(((int64_t)nsteps * N - n0) * 2 * P * 16), kBufferFlags);
+    const uint32_t rstep = (uint32_t)N * 2u * P * 16u;  // record bytes per k-step
+    struct Rec {
+        uint4 c[CW];
+        Table tb;
+    };
+    struct WStage {
+        Rec r[TN];
+    };
+    auto load_w = [&](WStage& W, int k) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = nl + 32 * j;
+            const uint32_t off = col < chans ? (uint32_t)k * rstep + (uint32_t)((col * 2 + h) * P) * 16u : 0x7FFFFF00u;
+            uint4 v[P];
+#pragma unroll
+            for (int q = 0; q < P; ++q)
+                v[q] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rr, (int)(off + 16u * q), 0, 0));
+#pragma unroll
+            for (int q = 0; q < CW; ++q) W.r[j].c[q] = v[q];
+            W.r[j].tb = Table{{v[CW].x, v[CW].y, v[CW].z, v[CW].w}, {v[CW + 1].x, v[CW + 1].y, v[CW + 1].z, v[CW + 1].w}};
+        }
+    };
+
+    bool int8[TN];  // 8-bit code layout: the channel decodes arithmetically
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int n = n0 + nl + 32 * j;
+        int8[j] = CODE_BITS == 8 && n < N && is_8bit(a.cols[n].fmt);
+    }
+    auto decode = [&](const Rec& r, int j, int s) __attribute__((always_inline)) -> half8 {
+        if (CODE_BITS == 4) {
+            const uint32_t w = s == 0 ? r.c[0].x : s == 1 ? r.c[0].y : s == 2 ? r.c[0].z : r.c[0].w;
+            return decode_nibbles(r.tb, w);
+        } else {
+            const uint4& cc = r.c[(s >> 1) & (CW - 1)];
+            const uint32_t w0 = (s & 1) ? cc.z : cc.x, w1 = (s & 1) ? cc.w : cc.y;
+            return int8[j] ? decode_bytes_int(r.tb, w0, w1) : decode_bytes_table(r.tb, w0, w1);
+        }
+    };
+
+    // LDS chunk offset of the lane's activation operand in sub-step s (row l32 of block i
+    // at + 256 i chunks)
+    int aoff[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) aoff[s] = l32 * 8 + ((4 * h + s) ^ ((l32 >> 1) & 7));
 
     float16v acc[TM][TN];
 #pragma unroll
@@ -357,150 +465,164 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, 1) void gemm_kernel(GemmArg
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    // activation tile loads: chunk c -> row c / 8, 16-byte column c % 8
-    uint4 areg[A_CHUNKS];
-    auto load_a = [&](int k0) {
+    auto compute = [&](int buf, const WStage& W) __attribute__((always_inline)) {
+        const uint4* L = lds[buf];
+        half8 af[TM], bf[TN], bn[TN];
 #pragma unroll
-        for (int i = 0; i < A_CHUNKS; ++i) {
-            const int c = i * kThreads + t;
-            const int r = c >> 3, col = (c & 7) * 8;
-            const int m = m0 + r;
-            areg[i] = m < a.M ? *reinterpret_cast<const uint4*>(a.Xh + (int64_t)m * K + k0 + col)
-                              : make_uint4(0u, 0u, 0u, 0u);
-        }
-    };
-    auto store_a = [&](int buf) {
+        for (int i = 0; i < TM; ++i) af[i] = __builtin_bit_cast(half8, L[i * 256 + aoff[0]]);
 #pragma unroll
-        for (int i = 0; i < A_CHUNKS; ++i) {
-            const int c = i * kThreads + t;
-            const int r = c >> 3, col = (c & 7) * 8;
-            *reinterpret_cast<uint4*>(&As[buf][r][col]) = areg[i];
-        }
-    };
-    // weight codes of a k-step (32 consecutive k of each of the lane's TN channels) and the
-    // block metadata of those k (NF4 absmax bits, or the E8M0 byte)
-    constexpr int CW = CODE_BITS == 4 ? 4 : 8;  // 32-bit words per channel per k-step
-    uint32_t wreg[TN][CW];
-    uint32_t mreg[TN];
-    auto load_w = [&](int k0) {
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int n = my[j].n;
-            if (n < 0) {
-#pragma unroll
-                for (int q = 0; q < CW; ++q) wreg[j][q] = 0u;
-                mreg[j] = 0u;
-                continue;
-            }
-            if (CODE_BITS == 4) {
-                const uint4 v = *reinterpret_cast<const uint4*>(a.wc + (int64_t)n * (K / 2) + (k0 + 32 * g) / 2);
-                wreg[j][0] = v.x; wreg[j][1] = v.y; wreg[j][2] = v.z; wreg[j][3] = v.w;
-            } else {
-                const uint4* p = reinterpret_cast<const uint4*>(a.wc + (int64_t)n * K + k0 + 32 * g);
-                const uint4 v0 = p[0], v1 = p[1];
-                wreg[j][0] = v0.x; wreg[j][1] = v0.y; wreg[j][2] = v0.z; wreg[j][3] = v0.w;
-                wreg[j][4] = v1.x; wreg[j][5] = v1.y; wreg[j][6] = v1.z; wreg[j][7] = v1.w;
-            }
-            if (my[j].fmt == CHAM_W_NF4) mreg[j] = __float_as_uint(a.wnf4[(int64_t)n * (K / 64) + (k0 >> 6)]);
-            else if (is_mx(my[j].fmt)) mreg[j] = a.we8[(int64_t)n * (K / 32) + ((k0 + 32 * g) >> 5)];
-            else mreg[j] = 0u;
-        }
-    };
-
-    const int nsteps = K / BK;
-    load_a(0);
-    load_w(0);
-    store_a(0);
-    __syncthreads();
-
-    for (int step = 0; step < nsteps; ++step) {
-        const int k0 = step * BK;
-        const int buf = step & 1;
-        uint32_t wcur[TN][CW];
-        _Float16 bfac[TN];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-#pragma unroll
-            for (int q = 0; q < CW; ++q) wcur[j][q] = wreg[j][q];
-            const ColInfo& ci = my[j];
-            bfac[j] = (_Float16)1.0f;
-            if (ci.fmt == CHAM_W_NF4) {
-                build_table(tab[j], CHAM_W_NF4, 0.0f, ldexpf(__uint_as_float(mreg[j]), -ci.eref));
-            } else if (is_mx(ci.fmt)) {
-                const float factor = ldexpf(1.0f, (int)mreg[j] - 127 - mx_F(ci.fmt) - ci.eref);
-                if (ci.fmt == CHAM_W_MXINT8) bfac[j] = (_Float16)factor;
-                else build_table(tab[j], ci.fmt, 0.0f, factor);
-            }
-        }
-        // prefetch the next k-step
-        if (step + 1 < nsteps) {
-            load_a(k0 + BK);
-            load_w(k0 + BK);
-        }
-        // 4 sub-steps of 16 k: lane group g covers k = 32g + 8s .. +7
+        for (int j = 0; j < TN; ++j) bf[j] = decode(W.r[j], j, 0);
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            half8 af[TM];
+            if (s < 3) {
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                af[i] = *reinterpret_cast<const half8*>(&As[buf][wm + i * 32 + (lane & 31)][32 * g + 8 * s]);
-            half8 bf[TN];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                if (CODE_BITS == 4) {
-                    bf[j] = decode_nibbles(tab[j], wcur[j][s]);
-                } else {
-                    const ColInfo& ci = my[j];
-                    if (is_8bit(ci.fmt)) {
-                        const bool sgn = ci.fmt != CHAM_W_INT8_ASYM;
-                        bf[j] = decode_bytes_int(wcur[j][2 * s], wcur[j][2 * s + 1], sgn ? 0x80808080u : 0u,
-                                                 (_Float16)(-(1024.0f + (sgn ? 128.0f : ci.zero))), bfac[j]);
-                    } else {
-                        bf[j] = decode_bytes_table(tab[j], wcur[j][2 * s], wcur[j][2 * s + 1]);
-                    }
-                }
+                for (int j = 0; j < TN; ++j) bn[j] = decode(W.r[j], j, s + 1);
             }
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i) {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+                if (s < 3) af[i] = __builtin_bit_cast(half8, L[i * 256 + aoff[s + 1]]);
+            }
+            if (s < 3) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bf[j] = bn[j];
+            }
         }
-        if (step + 1 < nsteps) {
-            store_a(buf ^ 1);
-            __syncthreads();
-        }
-    }
+    };
 
-    // ---- epilogue: 32x32 tile, lane holds column lane%32, rows 8*(r/4) + 4*(lane/32) + r%4
+    // ---- main loop.  Activation register stages R0 / R1 alternate (a k-step is loaded two
+    // steps before it is computed); weight stages W0 / W1 alternate (loaded one step
+    // ahead).  Invariant at the top: LDS buffer 0 and W0 hold step k, R1 step k + 1.  Step
+    // indices past the end are clamped to the last step (harmless reloads), so the loop
+    // body has no data-dependent branches.
+    const int klast = nsteps - 1;
+    AStage R0, R1;
+    WStage W0, W1;
+    load_w(W0, 0);
+    load_a(R0, 0);
+    load_a(R1, klast < 1 ? klast : 1);
+    store_a(R0, 0);
+    lds_barrier();
+    int k = 0;
+    for (; k + 2 <= nsteps; k += 2) {
+        load_w(W1, k + 1);
+        load_a(R0, k + 2 < klast ? k + 2 : klast);
+        compute(0, W0);
+        store_a(R1, 1);
+        lds_barrier();
+        load_w(W0, k + 2 < klast ? k + 2 : klast);
+        load_a(R1, k + 3 < klast ? k + 3 : klast);
+        compute(1, W1);
+        store_a(R0, 0);
+        lds_barrier();
+    }
+    if (k < nsteps) compute(0, W0);
+
+    // ---- epilogue: 32x32 block, lane holds column l32, rows 8*(r/4) + 4*h + r%4; the
+    // lane's 16 row scales of block i are 4 aligned float4 in LDS
+    float cs[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int n = n0 + nl + 32 * j;
+        cs[j] = n < N ? a.cols[n].colscale : 0.0f;
+    }
+    const bool full = rows == BM && n0 + BN <= N;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         float rs[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int m = m0 + wm + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-            rs[r] = m < a.M ? a.rowscale[m] : 0.0f;
+        for (int q = 0; q < 4; ++q) {
+            const float4 v = *reinterpret_cast<const float4*>(&Rs[32 * i + 8 * q + 4 * h]);
+            rs[4 * q] = v.x; rs[4 * q + 1] = v.y; rs[4 * q + 2] = v.z; rs[4 * q + 3] = v.w;
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-            const ColInfo& ci = my[j];
-            if (ci.n < 0) continue;
+            const int n = n0 + nl + 32 * j;
+            float* base = a.Y + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
+            if (full) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm + i * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-                if (m < a.M) a.Y[(int64_t)m * a.N + ci.n] = (acc[i][j][r] * rs[r]) * ci.colscale;
+                for (int r = 0; r < 16; ++r)
+                    base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = (acc[i][j][r] * rs[r]) * cs[j];
+            } else if (n < N) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int ml = 32 * i + 8 * (r >> 2) + 4 * h + (r & 3);
+                    if (ml < rows) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = (acc[i][j][r] * rs[r]) * cs[j];
+                }
             }
         }
     }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
-void launch_gemm(const GemmArgs& a, int code_bits, hipStream_t s) {
-    dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + BM - 1) / BM));
-    dim3 block(64 * WAVES_M * WAVES_N);
-    if (code_bits == 4) hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, 4>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<BM, BN, WAVES_M, WAVES_N, 8>), grid, block, 0, s, a);
+// ---- launch plan.  A launch covers rows [row0, M) with one tile height; the plan may
+// use a second launch with a smaller tile height for the rows left after the full rounds
+// of the first, so the last round does not leave most CUs idle.
+int cu_count() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
 }
+
+// Modeled time (us) of a launch of tile height bm over `rows` rows: rounds of workgroups
+// over the CUs times the k-steps at a per-step cost that grows with the tile height, plus
+// the output write (costs measured on MI355X for these kernels).
+double launch_cost(int rows, int tn, int nsteps, int bm, int P) {
+    if (rows <= 0) return 0.0;
+    const int64_t tiles = (int64_t)((rows + bm - 1) / bm) * tn;
+    const double rounds = (double)((tiles + P - 1) / P);
+    const double step = bm == 256 ? 1.7 : (bm == 128 ? 1.1 : 0.66);
+    const double epi = bm == 256 ? 6.5 : (bm == 128 ? 3.5 : 2.0);
+    return rounds * nsteps * step + epi;
+}
+
+struct Launch {
+    int row0, row1, bm;
+};
+int plan_gemm(int M, int N, int K, Launch (&out)[2]) {
+    const int P = cu_count();
+    const int tn = (N + BN - 1) / BN, nsteps = K / BK;
+    const int bms[3] = {256, 128, 64};
+    double best = 1e300;
+    int n = 0;
+    for (int b = 0; b < 3; ++b) {
+        const double c = launch_cost(M, tn, nsteps, bms[b], P);
+        if (c < best) { best = c; n = 1; out[0] = Launch{0, M, bms[b]}; }
+    }
+    // big tiles for whole rounds of full tile rows, then smaller tiles for the rest
+    for (int b = 0; b < 2; ++b) {
+        const int bm = bms[b];
+        const int rows_per_round = (P / tn) * bm;
+        if (rows_per_round <= 0) continue;
+        const int r1 = (M / rows_per_round) * rows_per_round;
+        if (r1 <= 0 || r1 >= M) continue;
+        for (int b2 = b + 1; b2 < 3; ++b2) {
+            const double c = launch_cost(r1, tn, nsteps, bm, P) + launch_cost(M - r1, tn, nsteps, bms[b2], P);
+            if (c < best) { best = c; n = 2; out[0] = Launch{0, r1, bm}; out[1] = Launch{r1, M, bms[b2]}; }
+        }
+    }
+    return n;
+}
+
+template <int CODE_BITS>
+void launch_gemm(GemmArgs a, const Launch& l, hipStream_t s) {
+    a.row0 = l.row0;
+    a.row1 = l.row1;
+    const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn);
+    if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8>), dim3(grid), dim3(kThreads), 0, s, a);
+    else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4>), dim3(grid), dim3(kThreads), 0, s, a);
+    else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2>), dim3(grid), dim3(kThreads), 0, s, a);
+}
+
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+int64_t record_bytes(int64_t N, int64_t K, int code_bits) { return N * (K / BK) * 2 * (code_bits / 4 + 2) * 16; }
 
 }  // namespace
 }  // namespace cham
@@ -508,9 +630,8 @@ void launch_gemm(const GemmArgs& a, int code_bits, hipStream_t s) {
 using namespace cham;
 
 size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    const size_t xh = (((size_t)M * (size_t)K * 2) + 255) & ~(size_t)255;
-    const size_t rs = (((size_t)M * 4) + 255) & ~(size_t)255;
-    return xh + rs + (size_t)N * sizeof(ColPrep);
+    return align256((size_t)M * (size_t)K * 2) + align256((size_t)M * 4) + align256((size_t)N * sizeof(ColPrep)) +
+           (size_t)record_bytes(N, K, 8);
 }
 
 extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
@@ -518,13 +639,17 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     if (!xq || !wq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
     if (!wq->fmt || !wq->codes || !wq->scale || !wq->zero) return CHAM_EINVAL;
     if (xq->M < 1 || wq->N < 1 || xq->K < 1 || xq->K != wq->K) return CHAM_EINVAL;
-    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || xq->K > INT32_MAX / 2) return CHAM_EINVAL;
     if (xq->fmt < 0 || xq->fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
     const uint32_t mask = wq->palette_mask;
     if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
     const int code_bits = (mask & 0x7u) ? 8 : 4;
     if (wq->code_bits != code_bits) return CHAM_EFORMAT;
     if (xq->K % 64 != 0) return CHAM_ESHAPE;
+    // 32-bit buffer offsets: a 256-row activation tile and the weight records stay below
+    // 2^31 bytes
+    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || xq->K > (1 << 20) ||
+        record_bytes(wq->N, xq->K, code_bits) > (int64_t)INT32_MAX)
+        return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
     if ((nf4 && !wq->nf4_absmax) || (wmx && !wq->e8m0)) return CHAM_EINVAL;
@@ -534,54 +659,63 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     const size_t need = cham_linear_workspace_bytes(xq->M, wq->N, xq->K);
     if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return CHAM_EWORKSPACE;
     hipStream_t s = (hipStream_t)stream;
+    const int M = (int)xq->M, N = (int)wq->N, K = (int)xq->K;
 
     char* w = (char*)ws;
     _Float16* Xh = (_Float16*)w;
-    w += (((size_t)xq->M * (size_t)xq->K * 2) + 255) & ~(size_t)255;
+    w += align256((size_t)M * (size_t)K * 2);
     float* rowscale = (float*)w;
-    w += (((size_t)xq->M * 4) + 255) & ~(size_t)255;
+    w += align256((size_t)M * 4);
     ColPrep* cols = (ColPrep*)w;
+    w += align256((size_t)N * sizeof(ColPrep));
+    uint4* rec = (uint4*)w;
 
     PrepArgs p;
-    p.d.xc = xq->codes;
-    p.d.xe8 = xq->e8m0;
-    p.d.xs = xq->scale;
-    p.d.xz = xq->zero;
-    p.d.afmt = xq->fmt;
-    p.d.M = (int)xq->M;
-    p.d.K = (int)xq->K;
-    p.d.perm4 = code_bits == 4;
-    p.d.Xh = Xh;
-    p.d.rowscale = rowscale;
+    p.xc = xq->codes;
+    p.xe8 = xq->e8m0;
+    p.xs = xq->scale;
+    p.xz = xq->zero;
+    p.afmt = xq->fmt;
+    p.M = M;
+    p.K = K;
+    p.perm4 = code_bits == 4;
+    p.Xh = Xh;
+    p.rowscale = rowscale;
     p.wfmt = wq->fmt;
     p.wscale = wq->scale;
     p.wzero = wq->zero;
     p.wnf4 = wq->nf4_absmax;
     p.we8 = wq->e8m0;
-    p.N = (int)wq->N;
+    p.N = N;
     p.mask = mask;
     p.cols = cols;
-    const unsigned nprep = (unsigned)(p.d.M + (p.N + 255) / 256);
+    const unsigned nprep = (unsigned)(M + (N + kColsPerBlock - 1) / kColsPerBlock);
     hipLaunchKernelGGL(prep_kernel, dim3(nprep), dim3(256), 0, s, p);
+    CHAM_CHECK_LAUNCH();
+
+    RecArgs ra{cols, wq->nf4_absmax, wq->e8m0, wq->codes, N, K, code_bits, rec};
+    const int64_t nrec = (int64_t)N * (K / BK) * 2;
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)((nrec + 255) / 256)), dim3(256), 0, s, ra);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;
     a.Xh = Xh;
     a.rowscale = rowscale;
     a.cols = cols;
-    a.wc = wq->codes;
-    a.wnf4 = wq->nf4_absmax;
-    a.we8 = wq->e8m0;
+    a.rec = rec;
     a.Y = Y;
-    a.M = (int)xq->M;
-    a.N = (int)wq->N;
-    a.K = (int)xq->K;
-    // tile choice: the largest tile that still gives about one wave of workgroups on 256 CUs
-    const int64_t t256 = ((a.M + 255) / 256) * (int64_t)((a.N + 255) / 256);
-    const int64_t t128x256 = ((a.M + 127) / 128) * (int64_t)((a.N + 255) / 256);
-    if (t256 >= 240) launch_gemm<256, 256, 2, 4>(a, code_bits, s);
-    else if (t128x256 >= 200) launch_gemm<128, 256, 2, 4>(a, code_bits, s);
-    else launch_gemm<128, 128, 2, 4>(a, code_bits, s);
-    CHAM_CHECK_LAUNCH();
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.row0 = 0;
+    a.row1 = M;
+    a.tn = (N + BN - 1) / BN;
+    Launch plan[2];
+    const int nl = plan_gemm(M, N, K, plan);
+    for (int i = 0; i < nl; ++i) {
+        if (code_bits == 4) launch_gemm<4>(a, plan[i], s);
+        else launch_gemm<8>(a, plan[i], s);
+        CHAM_CHECK_LAUNCH();
+    }
     return CHAM_OK;
 }

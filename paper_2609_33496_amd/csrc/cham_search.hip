@@ -477,56 +477,62 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     }
 }
 
-// Stable counting sort of channels by format, in one workgroup: thread t owns rows
-// [t*R, (t+1)*R); per-format counts are prefix-summed across threads in LDS.
+// Stable counting sort of channels by format, in one workgroup of 1024 threads: format
+// totals first, then chunks of 1024 consecutive rows in order, each row placed at its
+// group's running offset plus its rank among equal formats earlier in the chunk (wave
+// ballots and per-wave counts).
 __global__ __launch_bounds__(1024) void group_kernel(const uint8_t* fmt, int64_t N, int32_t* perm,
                                                      int32_t* group_off) {
-    __shared__ int32_t cnt[CHAM_W_NFMT][1024];
-    __shared__ int32_t tot[CHAM_W_NFMT + 1];
-    const int t = threadIdx.x;
-    const int64_t R = (N + 1023) / 1024;
-    const int64_t r0 = t * R, r1 = r0 + R < N ? r0 + R : N;
+    __shared__ int32_t wcnt[16][CHAM_W_NFMT];
+    __shared__ int32_t base[CHAM_W_NFMT + 1];
+    __shared__ int32_t tot[CHAM_W_NFMT];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    if (t < CHAM_W_NFMT) tot[t] = 0;
+    __syncthreads();
     int32_t c[CHAM_W_NFMT];
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) c[f] = 0;
-    for (int64_t r = r0; r < r1; ++r) {
-        int f = fmt[r];
+    for (int64_t r = t; r < N; r += 1024) {
+        const int f = fmt[r];
 #pragma unroll
         for (int g = 0; g < CHAM_W_NFMT; ++g) c[g] += (f == g);
     }
 #pragma unroll
-    for (int f = 0; f < CHAM_W_NFMT; ++f) cnt[f][t] = c[f];
+    for (int f = 0; f < CHAM_W_NFMT; ++f)
+        if (c[f]) atomicAdd(&tot[f], c[f]);
     __syncthreads();
-    // inclusive scan over threads for each format (Hillis-Steele)
-    for (int o = 1; o < 1024; o <<= 1) {
-        int32_t add[CHAM_W_NFMT];
-#pragma unroll
-        for (int f = 0; f < CHAM_W_NFMT; ++f) add[f] = t >= o ? cnt[f][t - o] : 0;
-        __syncthreads();
-#pragma unroll
-        for (int f = 0; f < CHAM_W_NFMT; ++f) cnt[f][t] += add[f];
-        __syncthreads();
-    }
     if (t == 0) {
         int32_t acc = 0;
-        for (int f = 0; f < CHAM_W_NFMT; ++f) { tot[f] = acc; acc += cnt[f][1023]; }
-        tot[CHAM_W_NFMT] = acc;
+        for (int f = 0; f < CHAM_W_NFMT; ++f) { base[f] = acc; acc += tot[f]; }
+        base[CHAM_W_NFMT] = acc;
     }
     __syncthreads();
-    if (group_off && t <= CHAM_W_NFMT) group_off[t] = tot[t];
-    if (perm) {
-        int32_t pos[CHAM_W_NFMT];
+    if (group_off && t <= CHAM_W_NFMT) group_off[t] = base[t];
+    if (!perm) return;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    for (int64_t chunk = 0; chunk < N; chunk += 1024) {
+        const int64_t r = chunk + t;
+        const int f = r < N ? (int)fmt[r] : CHAM_W_NFMT;
+        int rank = 0;
 #pragma unroll
-        for (int f = 0; f < CHAM_W_NFMT; ++f) pos[f] = tot[f] + cnt[f][t] - c[f];
-        for (int64_t r = r0; r < r1; ++r) {
-            int f = fmt[r];
-            int32_t p = 0;
-#pragma unroll
-            for (int g = 0; g < CHAM_W_NFMT; ++g) {
-                if (f == g) { p = pos[g]; pos[g]++; }
-            }
-            perm[p] = (int32_t)r;
+        for (int g = 0; g < CHAM_W_NFMT; ++g) {
+            const uint64_t m = __ballot(f == g);
+            if (lane == 0) wcnt[wave][g] = __popcll(m);
+            if (f == g) rank = __popcll(m & lt);
         }
+        __syncthreads();
+        if (f < CHAM_W_NFMT) {
+            int32_t pos = base[f] + rank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][f];
+            perm[pos] = (int32_t)r;
+        }
+        __syncthreads();
+        if (t < CHAM_W_NFMT) {
+            int32_t sum = 0;
+            for (int w = 0; w < 16; ++w) sum += wcnt[w][t];
+            base[t] += sum;
+        }
+        __syncthreads();
     }
 }
 

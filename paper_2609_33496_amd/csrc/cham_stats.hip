@@ -5,7 +5,7 @@
 // binary32 min/max per thread, a workgroup reduction, and per-workgroup partials in the
 // workspace.  A one-workgroup finalize kernel adds the partials in a fixed order into the
 // (layer, bucket) accumulator, so the result is bitwise reproducible run to run (no
-// floating atomics).
+// floating atomics).  The LUT build runs in one workgroup (B <= 1024 buckets).
 #include <math.h>
 
 #include "cham_device.h"
@@ -67,25 +67,33 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
     }
 }
 
-__global__ __launch_bounds__(kWave) void stats_finalize_kernel(const Partial* part, int nparts,
-                                                               int64_t numel, double* nS, float* lohi) {
+__global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Partial* part, int nparts,
+                                                                        int64_t numel, double* nS, float* lohi) {
     double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
     float lo = INFINITY, hi = -INFINITY;
-    for (int i = threadIdx.x; i < nparts; i += kWave) {
+    for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {
         Partial p = part[i];
         s1 += p.s1; s2 += p.s2; s3 += p.s3; s4 += p.s4;
         lo = fminf(lo, p.lo); hi = fmaxf(hi, p.hi);
     }
     s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
     lo = wave_min(lo); hi = wave_max(hi);
+    __shared__ Partial wp[kStatsThreads / kWave];
+    if ((threadIdx.x & 63) == 0) wp[threadIdx.x >> 6] = Partial{s1, s2, s3, s4, lo, hi, 0.f, 0.f};
+    __syncthreads();
     if (threadIdx.x == 0) {
+        Partial r = wp[0];
+        for (int i = 1; i < kStatsThreads / kWave; ++i) {
+            r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
+            r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
+        }
         nS[0] += (double)numel;
-        nS[1] += s1;
-        nS[2] += s2;
-        nS[3] += s3;
-        nS[4] += s4;
-        lohi[0] = fminf(lohi[0], lo);
-        lohi[1] = fmaxf(lohi[1], hi);
+        nS[1] += r.s1;
+        nS[2] += r.s2;
+        nS[3] += r.s3;
+        nS[4] += r.s4;
+        lohi[0] = fminf(lohi[0], r.lo);
+        lohi[1] = fmaxf(lohi[1], r.hi);
     }
 }
 
@@ -112,61 +120,81 @@ struct LutArgs {
     int snr_gate_on;
 };
 
-// One thread per (layer, bucket).
-__global__ void lut_kernel(LutArgs a) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= a.L * a.B) return;
-    const int l = i / a.B, b = i % a.B;
-    // kurtosis from raw power sums (population moments)
-    const double* p = a.nS + 5 * (int64_t)i;
-    const double n = p[0];
-    const double mu = p[1] / n;
-    const double e2 = p[2] / n, e3 = p[3] / n, e4 = p[4] / n;
-    const double m2 = e2 - mu * mu;
-    const double m4 = e4 - 4.0 * mu * e3 + 6.0 * mu * mu * e2 - 3.0 * mu * mu * mu * mu;
-    const double kap = m4 / (m2 * m2);
-    // SNR at the bucket midpoint: alpha_bar_t = prod_{s=0..t} (1 - beta_s), sequential
-    const int tb = (int)(((int64_t)(2 * b + 1) * a.T) / (2LL * a.B));
-    double ab = 1.0;
-    for (int s = 0; s <= tb; ++s) {
-        double frac = a.T > 1 ? (double)s / (double)(a.T - 1) : 0.0;
-        double beta;
-        if (a.kind == CHAM_SCHED_SCALED_LINEAR) {
-            double r = a.r0 + (a.r1 - a.r0) * frac;
-            beta = r * r;
-        } else {
-            beta = a.b0 + (a.b1 - a.b0) * frac;
+constexpr int kLutThreads = 256;
+
+// One workgroup.  First the SNR at every bucket midpoint: alpha_bar_t = prod_{s<=t}
+// (1 - beta_s) as a tree product over the workgroup (binary64; its rounding differs from a
+// sequential product only in the last bits, so only an SNR within ~1e-15 of a gate could
+// route differently).  Then one thread per (layer, bucket): kurtosis, route, ScaleZP.
+constexpr int kLutMaxBuckets = 1024;
+
+__global__ __launch_bounds__(kLutThreads) void lut_kernel(LutArgs a) {
+    __shared__ double red[kLutThreads];
+    __shared__ double snr_ws[kLutMaxBuckets];
+    for (int b = 0; b < a.B; ++b) {
+        const int tb = (int)(((int64_t)(2 * b + 1) * a.T) / (2LL * a.B));
+        double prod = 1.0;
+        for (int s = threadIdx.x; s <= tb; s += kLutThreads) {
+            const double frac = a.T > 1 ? (double)s / (double)(a.T - 1) : 0.0;
+            double beta;
+            if (a.kind == CHAM_SCHED_SCALED_LINEAR) {
+                const double r = a.r0 + (a.r1 - a.r0) * frac;
+                beta = r * r;
+            } else {
+                beta = a.b0 + (a.b1 - a.b0) * frac;
+            }
+            prod *= (1.0 - beta);
         }
-        ab *= (1.0 - beta);
-    }
-    const double snr = ab / (1.0 - ab);
-    // route
-    int f;
-    const int sc = a.is_shortcut ? a.is_shortcut[l] : 0;
-    const bool snr_low = a.snr_gate_on ? (snr < a.s_lo) : false;
-    const bool snr_high = a.snr_gate_on ? (snr > a.s_hi) : true;
-    if (sc) f = CHAM_A_MXFP8_E4M3;
-    else if (kap > a.k_hi || snr_low) f = CHAM_A_FP8_E5M2;
-    else if (kap <= a.k_lo && snr_high) f = CHAM_A_INT8_ASYM;
-    else f = CHAM_A_FP8_E4M3;
-    // ScaleZP on the bucket range
-    float s = 1.0f, z = 0.0f;
-    if (n != 0.0) {
-        const float lo = a.lohi[2 * i], hi = a.lohi[2 * i + 1];
-        if (f == CHAM_A_INT8_ASYM) {
-            float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
-            s = floor_scale((h0 - l0) / 255.0f);
-            z = clampf(rne(-l0 / s), 0.0f, 255.0f);
-        } else if (f == CHAM_A_FP8_E4M3) {
-            s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
-        } else if (f == CHAM_A_FP8_E5M2) {
-            s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 57344.0f);
+        red[threadIdx.x] = prod;
+        __syncthreads();
+        for (int o = kLutThreads / 2; o > 0; o >>= 1) {
+            if ((int)threadIdx.x < o) red[threadIdx.x] *= red[threadIdx.x + o];
+            __syncthreads();
         }
+        if (threadIdx.x == 0) {
+            const double ab = red[0];
+            snr_ws[b] = ab / (1.0 - ab);
+        }
+        __syncthreads();
     }
-    a.F[i] = (uint8_t)f;
-    a.S[i] = s;
-    a.Z[i] = z;
-    if (a.kappa) a.kappa[i] = kap;
+    for (int i = threadIdx.x; i < a.L * a.B; i += kLutThreads) {
+        const int l = i / a.B, b = i % a.B;
+        // kurtosis from raw power sums (population moments)
+        const double* p = a.nS + 5 * (int64_t)i;
+        const double n = p[0];
+        const double mu = p[1] / n;
+        const double e2 = p[2] / n, e3 = p[3] / n, e4 = p[4] / n;
+        const double m2 = e2 - mu * mu;
+        const double m4 = e4 - 4.0 * mu * e3 + 6.0 * mu * mu * e2 - 3.0 * mu * mu * mu * mu;
+        const double kap = m4 / (m2 * m2);
+        const double snr = snr_ws[b];
+        int f;
+        const int sc = a.is_shortcut ? a.is_shortcut[l] : 0;
+        const bool snr_low = a.snr_gate_on ? (snr < a.s_lo) : false;
+        const bool snr_high = a.snr_gate_on ? (snr > a.s_hi) : true;
+        if (sc) f = CHAM_A_MXFP8_E4M3;
+        else if (kap > a.k_hi || snr_low) f = CHAM_A_FP8_E5M2;
+        else if (kap <= a.k_lo && snr_high) f = CHAM_A_INT8_ASYM;
+        else f = CHAM_A_FP8_E4M3;
+        // ScaleZP on the bucket range
+        float s = 1.0f, z = 0.0f;
+        if (n != 0.0) {
+            const float lo = a.lohi[2 * i], hi = a.lohi[2 * i + 1];
+            if (f == CHAM_A_INT8_ASYM) {
+                float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
+                s = floor_scale((h0 - l0) / 255.0f);
+                z = clampf(rne(-l0 / s), 0.0f, 255.0f);
+            } else if (f == CHAM_A_FP8_E4M3) {
+                s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
+            } else if (f == CHAM_A_FP8_E5M2) {
+                s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 57344.0f);
+            }
+        }
+        a.F[i] = (uint8_t)f;
+        a.S[i] = s;
+        a.Z[i] = z;
+        if (a.kappa) a.kappa[i] = kap;
+    }
 }
 
 }  // namespace
@@ -205,7 +233,7 @@ extern "C" int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t 
     hipLaunchKernelGGL(stats_partial_kernel, dim3(nb), dim3(kStatsThreads), 0, s, X, numel, part);
     CHAM_CHECK_LAUNCH();
     const int64_t i = (int64_t)layer * st->B + bucket;
-    hipLaunchKernelGGL(stats_finalize_kernel, dim3(1), dim3(kWave), 0, s, part, nb, numel, st->nS + 5 * i,
+    hipLaunchKernelGGL(stats_finalize_kernel, dim3(1), dim3(kStatsThreads), 0, s, part, nb, numel, st->nS + 5 * i,
                        st->lohi + 2 * i);
     CHAM_CHECK_LAUNCH();
     return CHAM_OK;
@@ -234,7 +262,7 @@ extern "C" int cham_build_act_lut(const cham_act_stats* st, const cham_schedule*
                                   cham_lut* lut, double* kappa, void* stream) {
     if (!st || !sch || !lut || !st->nS || !st->lohi || !lut->F || !lut->S || !lut->Z) return CHAM_EINVAL;
     if (st->L < 1 || st->B < 1 || lut->L != st->L || lut->B != st->B) return CHAM_EINVAL;
-    if (sch->T < 1 || sch->T > (1 << 20) || st->B > sch->T) return CHAM_EINVAL;
+    if (sch->T < 1 || sch->T > (1 << 20) || st->B > sch->T || st->B > kLutMaxBuckets) return CHAM_EINVAL;
     if (!(sch->beta0 >= 0.0 && sch->beta0 < 1.0 && sch->beta1 >= 0.0 && sch->beta1 < 1.0)) return CHAM_EINVAL;
     if (sch->kind != CHAM_SCHED_SCALED_LINEAR && sch->kind != CHAM_SCHED_LINEAR) return CHAM_EINVAL;
     lut->T = sch->T;
@@ -260,7 +288,8 @@ extern "C" int cham_build_act_lut(const cham_act_stats* st, const cham_schedule*
     a.s_hi = sch->snr_hi;
     a.snr_gate_on = sch->snr_gate_on;
     const int n = st->L * st->B;
-    hipLaunchKernelGGL(lut_kernel, dim3((n + 63) / 64), dim3(64), 0, (hipStream_t)stream, a);
+    (void)n;
+    hipLaunchKernelGGL(lut_kernel, dim3(1), dim3(kLutThreads), 0, (hipStream_t)stream, a);
     CHAM_CHECK_LAUNCH();
     return CHAM_OK;
 }
