@@ -57,102 +57,43 @@ struct ColPrep {
 };
 
 // ------------------------------------------------------------------------------------
-// pre-pass 1: activations -> half precision; channel parameters
+// pre-pass for MX activation formats: codes -> half precision relative to the row's
+// largest block exponent (exact), the row scale 2^eref separately
 // ------------------------------------------------------------------------------------
 struct PrepArgs {
-    // activations
     const uint8_t* xc;
     const uint8_t* xe8;
-    const float* xs;
-    const float* xz;
     int afmt;
     int M, K;
     int perm4;  // 1: store each group of 8 columns in the order 0,4,1,5,2,6,3,7
     _Float16* Xh;
     float* rowscale;
-    // channels
-    const uint8_t* wfmt;
-    const float* wscale;
-    const int32_t* wzero;
-    const float* wnf4;
-    const uint8_t* we8;
-    int N;
-    uint32_t mask;
-    ColPrep* cols;
 };
 
-CHAM_DEV float adecode(int afmt, uint32_t c, float z, int kblk_e, int eref) {
-    switch (afmt) {
-    case CHAM_A_INT8_ASYM: return (float)c - z;
-    case CHAM_A_FP8_E4M3: return e4m3_decode(c);
-    case CHAM_A_FP8_E5M2: return e5m2_decode(c);
-    case CHAM_A_MXFP8_E4M3: return ldexpf(e4m3_decode(c), kblk_e - eref);
-    default: return ldexpf((float)(int8_t)c, kblk_e - 6 - eref);  // MXINT8
-    }
-}
-
-constexpr int kColsPerBlock = 4;  // one wavefront per channel
-
-// Workgroups [0, M): activation row m.  Next ceil(N/4): one wavefront per channel reduces
-// its block metadata to the channel's reference exponent.
+// One workgroup per activation row.
 __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
     const int K = p.K;
-    const int bid = (int)blockIdx.x;
-    if (bid >= p.M) {
-        const int lane = threadIdx.x & 63;
-        const int n = (bid - p.M) * kColsPerBlock + (int)(threadIdx.x >> 6);
-        if (n >= p.N) return;
-        ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
-        const int f = p.wfmt[n];
-        if (f < CHAM_W_NFMT && ((p.mask >> f) & 1u)) {
-            c.fmt = f;
-            c.zero = (float)p.wzero[n];
-            if (f == CHAM_W_NF4) {
-                const float* r = p.wnf4 + (int64_t)n * (K / 64);
-                float mx = 0.0f;
-                for (int b = lane; b < K / 64; b += 64) mx = fmaxf(mx, r[b]);
-                mx = wave_max(mx);
-                c.eref = floor_log2(floor_scale(mx));
-                c.colscale = ldexpf(1.0f, c.eref);
-            } else if (is_mx(f)) {
-                const uint8_t* r = p.we8 + (int64_t)n * (K / 32);
-                int mx = 0;
-                for (int b = lane; b < K / 32; b += 64) mx = max(mx, (int)r[b]);
-                for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o, kWave));
-                c.eref = mx - 127 - mx_F(f);
-                c.colscale = ldexpf(1.0f, c.eref);
-            } else {
-                c.colscale = p.wscale[n];
-            }
-        }
-        if (lane == 0) p.cols[n] = c;
-        return;
-    }
-    const int m = bid;
-    const bool mx = p.afmt == CHAM_A_MXFP8_E4M3 || p.afmt == CHAM_A_MXINT8;
+    const int m = blockIdx.x;
     __shared__ int sh_e;
-    int eref = 0;
-    if (mx) {
-        int mx_e = 0;
-        for (int b = threadIdx.x; b < K / 32; b += blockDim.x) mx_e = max(mx_e, (int)p.xe8[(int64_t)m * (K / 32) + b]);
-        for (int o = 32; o > 0; o >>= 1) mx_e = max(mx_e, __shfl_xor(mx_e, o, kWave));
-        if (threadIdx.x == 0) sh_e = 0;
-        __syncthreads();
-        if ((threadIdx.x & 63) == 0) atomicMax(&sh_e, mx_e);
-        __syncthreads();
-        eref = sh_e - 127;
-    }
-    const float z = *p.xz;
+    int mx_e = 0;
+    for (int b = threadIdx.x; b < K / 32; b += blockDim.x) mx_e = max(mx_e, (int)p.xe8[(int64_t)m * (K / 32) + b]);
+    for (int o = 32; o > 0; o >>= 1) mx_e = max(mx_e, __shfl_xor(mx_e, o, kWave));
+    if (threadIdx.x == 0) sh_e = 0;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) atomicMax(&sh_e, mx_e);
+    __syncthreads();
+    const int eref = sh_e - 127;
     const uint8_t* row = p.xc + (int64_t)m * K;
     _Float16* out = p.Xh + (int64_t)m * K;
     for (int g = threadIdx.x; g < K / 8; g += blockDim.x) {
         const uint2 c2 = *reinterpret_cast<const uint2*>(row + 8 * g);
-        const int kb = mx ? (int)p.xe8[(int64_t)m * (K / 32) + (g >> 2)] - 127 : 0;
+        const int kb = (int)p.xe8[(int64_t)m * (K / 32) + (g >> 2)] - 127;
         float v[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            uint32_t c = ((j < 4 ? c2.x : c2.y) >> (8 * (j & 3))) & 0xFFu;
-            v[j] = adecode(p.afmt, c, z, kb, eref);
+            const uint32_t c = ((j < 4 ? c2.x : c2.y) >> (8 * (j & 3))) & 0xFFu;
+            v[j] = p.afmt == CHAM_A_MXFP8_E4M3 ? ldexpf(e4m3_decode(c), kb - eref)
+                                               : ldexpf((float)(int8_t)c, kb - 6 - eref);
         }
         half8 h;
         if (p.perm4) {
@@ -167,7 +108,7 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
         }
         *reinterpret_cast<half8*>(out + 8 * g) = h;
     }
-    if (threadIdx.x == 0) p.rowscale[m] = mx ? ldexpf(1.0f, eref) : *p.xs;
+    if (threadIdx.x == 0) p.rowscale[m] = ldexpf(1.0f, eref);
 }
 
 // ------------------------------------------------------------------------------------
@@ -225,53 +166,87 @@ CHAM_DEV Table int8_record(uint32_t xmask, float zoff, float factor) {
 }
 
 struct RecArgs {
-    const ColPrep* cols;
+    const uint8_t* wfmt;
+    const float* wscale;
+    const int32_t* wzero;
     const float* wnf4;
     const uint8_t* we8;
     const uint8_t* wc;
+    uint32_t mask;
     int N, K, code_bits;
+    ColPrep* cols;
     uint4* rec;  // [K/64][N][2][pieces]
 };
 
-// One thread per (k-step, channel, half).
+// Wavefront w of the launch handles channel w / per and the (k-step, half) pairs
+// 64 (w % per) .. + 63 of it, per = ceil(2 K / 64 / 64): each computes the channel's
+// reference exponent (largest NF4 block absmax or MX block exponent, wavefront max) and
+// one record per lane; the first wavefront of a channel also stores its ColPrep.
 __global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
-    const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t total = (int64_t)(a.K / BK) * a.N * 2;
-    if (id >= total) return;
-    const int h = (int)(id & 1);
-    const int n = (int)((id >> 1) % a.N);
-    const int k = (int)((id >> 1) / a.N);
-    const ColPrep c = a.cols[n];
-    Table t;
-    switch (c.fmt) {
-    case CHAM_W_NF4:
-        t = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(a.wnf4[(int64_t)n * (a.K / 64) + k], -c.eref));
-        break;
-    case CHAM_W_MXFP4:
-    case CHAM_W_MXINT4:
-    case CHAM_W_MXINT8: {
-        const int e = a.we8[(int64_t)n * (a.K / 32) + 2 * k + h];
-        const float factor = ldexpf(1.0f, e - 127 - mx_F(c.fmt) - c.eref);
-        if (c.fmt == CHAM_W_MXFP4) t = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
-        else if (c.fmt == CHAM_W_MXINT4) t = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
-        else t = int8_record(0x80808080u, 128.0f, factor);
-        break;
+    const int lane = threadIdx.x & 63;
+    const int per = (2 * (a.K / BK) + 63) / 64;
+    const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int n = (int)(wid / per), part = (int)(wid % per);
+    if (n >= a.N) return;
+    const int K = a.K, nst = K / BK;
+    ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
+    const int f = a.wfmt[n];
+    if (f < CHAM_W_NFMT && ((a.mask >> f) & 1u)) {
+        c.fmt = f;
+        c.zero = (float)a.wzero[n];
+        if (f == CHAM_W_NF4) {
+            const float* r = a.wnf4 + (int64_t)n * (K / 64);
+            float mx = 0.0f;
+            for (int b = lane; b < K / 64; b += 64) mx = fmaxf(mx, r[b]);
+            mx = wave_max(mx);
+            c.eref = floor_log2(floor_scale(mx));
+            c.colscale = ldexpf(1.0f, c.eref);
+        } else if (is_mx(f)) {
+            const uint8_t* r = a.we8 + (int64_t)n * (K / 32);
+            int mx = 0;
+            for (int b = lane; b < K / 32; b += 64) mx = max(mx, (int)r[b]);
+            for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o, kWave));
+            c.eref = mx - 127 - mx_F(f);
+            c.colscale = ldexpf(1.0f, c.eref);
+        } else {
+            c.colscale = a.wscale[n];
+        }
     }
-    case CHAM_W_FP4: t = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
-    case CHAM_W_INT4_ASYM: t = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
-    case CHAM_W_INT4_SYM: t = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
-    case CHAM_W_INT8_SYM: t = int8_record(0x80808080u, 128.0f, 1.0f); break;
-    case CHAM_W_INT8_ASYM: t = int8_record(0u, c.zero, 1.0f); break;
-    default: t = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
-    }
+    if (lane == 0 && part == 0) a.cols[n] = c;
     const int cw = a.code_bits / 4;  // 16-byte code pieces per half k-step
-    const int64_t cstride = (int64_t)a.K * a.code_bits / 8;
-    const uint4* src = reinterpret_cast<const uint4*>(a.wc + n * cstride + (int64_t)k * (16 * a.code_bits / 2) +
-                                                      (int64_t)h * 16 * cw);
-    uint4* dst = a.rec + id * (cw + 2);
-    for (int q = 0; q < cw; ++q) dst[q] = src[q];
-    dst[cw] = make_uint4(t.lo[0], t.lo[1], t.lo[2], t.lo[3]);
-    dst[cw + 1] = make_uint4(t.hi[0], t.hi[1], t.hi[2], t.hi[3]);
+    const int64_t cstride = (int64_t)K * a.code_bits / 8;
+    const int idx = 64 * part + lane;
+    if (idx < 2 * nst) {
+        const int k = idx >> 1, h = idx & 1;
+        Table t;
+        switch (c.fmt) {
+        case CHAM_W_NF4:
+            t = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(a.wnf4[(int64_t)n * (K / 64) + k], -c.eref));
+            break;
+        case CHAM_W_MXFP4:
+        case CHAM_W_MXINT4:
+        case CHAM_W_MXINT8: {
+            const int e = a.we8[(int64_t)n * (K / 32) + 2 * k + h];
+            const float factor = ldexpf(1.0f, e - 127 - mx_F(c.fmt) - c.eref);
+            if (c.fmt == CHAM_W_MXFP4) t = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
+            else if (c.fmt == CHAM_W_MXINT4) t = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
+            else t = int8_record(0x80808080u, 128.0f, factor);
+            break;
+        }
+        case CHAM_W_FP4: t = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
+        case CHAM_W_INT4_ASYM: t = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
+        case CHAM_W_INT4_SYM: t = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
+        case CHAM_W_INT8_SYM: t = int8_record(0x80808080u, 128.0f, 1.0f); break;
+        case CHAM_W_INT8_ASYM: t = int8_record(0u, c.zero, 1.0f); break;
+        default: t = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
+        }
+        const uint4* src = reinterpret_cast<const uint4*>(a.wc + n * cstride + (int64_t)k * (16 * a.code_bits / 2) +
+                                                          (int64_t)h * 16 * cw);
+        uint4* dst = a.rec + (((int64_t)k * a.N + n) * 2 + h) * (cw + 2);
+        for (int q = 0; q < cw; ++q) dst[q] = src[q];
+        dst[cw] = make_uint4(t.lo[0], t.lo[1], t.lo[2], t.lo[3]);
+        dst[cw + 1] = make_uint4(t.hi[0], t.hi[1], t.hi[2], t.hi[3]);
+    }
 }
 
 // ------------------------------------------------------------------------------------
@@ -353,8 +328,11 @@ CHAM_DEV void lds_barrier() {
 // main kernel
 // ------------------------------------------------------------------------------------
 struct GemmArgs {
-    const _Float16* Xh;      // [M][K] (column order as above)
-    const float* rowscale;   // [M]
+    const _Float16* Xh;      // [M][K] (column order as above), MX activation formats
+    const float* rowscale;   // [M], MX activation formats
+    const uint8_t* xc;       // [M][K] activation codes, per-tensor formats
+    const float* xs;         // per-tensor activation scale (device scalar)
+    const float* xz;         // per-tensor activation zero point (device scalar)
     const ColPrep* cols;     // [N]
     const uint4* rec;        // [K/64][N][2][pieces]
     float* Y;
@@ -363,12 +341,46 @@ struct GemmArgs {
     int tn;      // tile columns
 };
 
-template <int CODE_BITS, int TM>
+// Activation operand source: the half-precision copy of the pre-pass (MX formats), or the
+// per-tensor codes, decoded while they are staged into LDS.
+constexpr int kAF16 = 0, kAInt8 = 1, kAE4M3 = 2, kAE5M2 = 3;
+
+// 8 activation codes (k0..k3 in w0, k4..k7 in w1) -> 8 halves, in the order
+// (0,4,1,5,2,6,3,7) when perm4, else natural; exact for all three per-tensor formats.
+template <int AF>
+CHAM_DEV uint4 decode_act8(uint32_t w0, uint32_t w1, bool perm4, half2v negz) {
+    // byte selectors of v_perm_b32(w1, w0, sel): 0..3 -> k0..k3, 4..7 -> k4..k7, 12 -> 0
+    uint32_t d[4];
+    if (AF == kAE5M2) {  // E5M2 is the top byte of binary16
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t a = perm4 ? j : 2 * j, b = perm4 ? j + 4 : 2 * j + 1;
+            d[j] = __builtin_amdgcn_perm(w1, w0, 0x0Cu | (a << 8) | (0x0Cu << 16) | (b << 24));
+        }
+    } else if (AF == kAE4M3) {  // hardware E4M3 -> binary16 conversion, unit scale
+        const uint32_t p0 = perm4 ? __builtin_amdgcn_perm(w1, w0, 0x05010400u) : w0;
+        const uint32_t p1 = perm4 ? __builtin_amdgcn_perm(w1, w0, 0x07030602u) : w1;
+        d[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p0, 1.0f, false));
+        d[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p0, 1.0f, true));
+        d[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p1, 1.0f, false));
+        d[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(p1, 1.0f, true));
+    } else {  // INT8-asym: (1024 + c) - (1024 + z) in binary16
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t a = perm4 ? j : 2 * j, b = perm4 ? j + 4 : 2 * j + 1;
+            const uint32_t v = __builtin_amdgcn_perm(w1, w0, a | (0x0Cu << 8) | (b << 16) | (0x0Cu << 24)) | 0x64006400u;
+            d[j] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, v) + negz);
+        }
+    }
+    return make_uint4(d[0], d[1], d[2], d[3]);
+}
+
+template <int CODE_BITS, int TM, int AF>
 __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     constexpr int BM = 32 * TM;
     constexpr int CW = CODE_BITS / 4;           // 16-byte code pieces per record
     constexpr int P = CW + 2;                   // 16-byte pieces per record
-    constexpr int AQ = TM;                      // activation loads per thread per k-step
+    constexpr int AQ = AF == kAF16 ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
     constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
     __shared__ uint4 lds[2][A_CH];
     __shared__ float Rs[BM];
@@ -381,27 +393,54 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     const int m0 = a.row0 + ((int)blockIdx.x / a.tn) * BM, n0 = ((int)blockIdx.x % a.tn) * BN;
     const int rows = a.row1 - m0 < BM ? a.row1 - m0 : BM;
 
-    if (t < BM) Rs[t] = a.rowscale[t < rows ? m0 + t : m0];
+    if (t < BM) Rs[t] = AF == kAF16 ? a.rowscale[t < rows ? m0 + t : m0] : *a.xs;
+    half2v negz = {(_Float16)0.0f, (_Float16)0.0f};
+    if (AF == kAInt8) {
+        const _Float16 nz = (_Float16)(-(1024.0f + *a.xz));
+        negz = half2v{nz, nz};
+    }
 
     // ---- activation tile: global -> registers two k-steps ahead -> LDS, 16-byte loads
-    // through a buffer resource whose range check returns zeros past the last row.  Chunk
-    // slot q = 256 i + t holds tile row 32 i + (t >> 3), logical chunk
-    // (t & 7) ^ ((row >> 1) & 7).
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.Xh + (int64_t)m0 * K), (short)0, rows * K * 2, kBufferFlags);
-    const uint32_t aoff0 = (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4));
+    // through a buffer resource whose range check returns zeros past the last row.  The
+    // tile is stored as rows of 8 logical 16-byte chunks (8 k each), chunk c of row r at
+    // slot c ^ ((r >> 1) & 7).
+    //  half-precision copy: load q = 256 i + t is row q >> 3, chunk q & 7;
+    //  codes: load q is row q >> 2, codes 16 (q & 3) .. + 15 = chunks 2 (q & 3), + 1.
+    const bool perm4 = CODE_BITS == 4;
+    const __amdgpu_buffer_rsrc_t ra =
+        AF == kAF16 ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.Xh + (int64_t)m0 * K), (short)0, rows * K * 2,
+                                                        kBufferFlags)
+                    : __builtin_amdgcn_make_buffer_rsrc((void*)(a.xc + (int64_t)m0 * K), (short)0, rows * K,
+                                                        kBufferFlags);
+    const uint32_t aoff0 = AF == kAF16 ? (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4))
+                                       : (uint32_t)((t >> 2) * K + ((t & 3) << 4));
     struct AStage {
         uint4 v[AQ];
     };
     auto load_a = [&](AStage& S, int k) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < AQ; ++i)
-            S.v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                         ra, (int)(aoff0 + (uint32_t)(i * 64 * K + k * BK * 2)), 0, 0));
+        for (int i = 0; i < AQ; ++i) {
+            const uint32_t off = AF == kAF16 ? aoff0 + (uint32_t)(i * 64 * K + k * BK * 2)
+                                             : aoff0 + (uint32_t)(i * 64 * K + k * BK);
+            S.v[i] = (AF != kAF16 && i * 256 + t >= BM * 4)
+                         ? make_uint4(0u, 0u, 0u, 0u)
+                         : __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)off, 0, 0));
+        }
     };
     auto store_a = [&](const AStage& S, int buf) __attribute__((always_inline)) {
 #pragma unroll
-        for (int i = 0; i < AQ; ++i) lds[buf][i * 256 + t] = S.v[i];
+        for (int i = 0; i < AQ; ++i) {
+            if (AF == kAF16) {
+                lds[buf][i * 256 + t] = S.v[i];
+            } else {
+                const int q = i * 256 + t;
+                if (q < BM * 4) {
+                    const int r = q >> 2, c = 2 * (q & 3), sw = (r >> 1) & 7;
+                    lds[buf][r * 8 + (c ^ sw)] = decode_act8<AF>(S.v[i].x, S.v[i].y, perm4, negz);
+                    lds[buf][r * 8 + ((c + 1) ^ sw)] = decode_act8<AF>(S.v[i].z, S.v[i].w, perm4, negz);
+                }
+            }
+        }
     };
 
     // ---- weight records of the lane's channels (column l32 of the wave's two 32-channel
@@ -611,14 +650,24 @@ int plan_gemm(int M, int N, int K, Launch (&out)[2]) {
     return n;
 }
 
+template <int CODE_BITS, int AF>
+void launch_gemm_af(const GemmArgs& a, const Launch& l, hipStream_t s) {
+    const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn);
+    if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8, AF>), dim3(grid), dim3(kThreads), 0, s, a);
+    else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4, AF>), dim3(grid), dim3(kThreads), 0, s, a);
+    else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2, AF>), dim3(grid), dim3(kThreads), 0, s, a);
+}
+
 template <int CODE_BITS>
-void launch_gemm(GemmArgs a, const Launch& l, hipStream_t s) {
+void launch_gemm(GemmArgs a, const Launch& l, int af, hipStream_t s) {
     a.row0 = l.row0;
     a.row1 = l.row1;
-    const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn);
-    if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8>), dim3(grid), dim3(kThreads), 0, s, a);
-    else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4>), dim3(grid), dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2>), dim3(grid), dim3(kThreads), 0, s, a);
+    switch (af) {
+    case kAInt8: launch_gemm_af<CODE_BITS, kAInt8>(a, l, s); break;
+    case kAE4M3: launch_gemm_af<CODE_BITS, kAE4M3>(a, l, s); break;
+    case kAE5M2: launch_gemm_af<CODE_BITS, kAE5M2>(a, l, s); break;
+    default: launch_gemm_af<CODE_BITS, kAF16>(a, l, s); break;
+    }
 }
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
@@ -670,37 +719,23 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     w += align256((size_t)N * sizeof(ColPrep));
     uint4* rec = (uint4*)w;
 
-    PrepArgs p;
-    p.xc = xq->codes;
-    p.xe8 = xq->e8m0;
-    p.xs = xq->scale;
-    p.xz = xq->zero;
-    p.afmt = xq->fmt;
-    p.M = M;
-    p.K = K;
-    p.perm4 = code_bits == 4;
-    p.Xh = Xh;
-    p.rowscale = rowscale;
-    p.wfmt = wq->fmt;
-    p.wscale = wq->scale;
-    p.wzero = wq->zero;
-    p.wnf4 = wq->nf4_absmax;
-    p.we8 = wq->e8m0;
-    p.N = N;
-    p.mask = mask;
-    p.cols = cols;
-    const unsigned nprep = (unsigned)(M + (N + kColsPerBlock - 1) / kColsPerBlock);
-    hipLaunchKernelGGL(prep_kernel, dim3(nprep), dim3(256), 0, s, p);
-    CHAM_CHECK_LAUNCH();
+    if (amx) {
+        PrepArgs p{xq->codes, xq->e8m0, xq->fmt, M, K, code_bits == 4, Xh, rowscale};
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)M), dim3(256), 0, s, p);
+        CHAM_CHECK_LAUNCH();
+    }
 
-    RecArgs ra{cols, wq->nf4_absmax, wq->e8m0, wq->codes, N, K, code_bits, rec};
-    const int64_t nrec = (int64_t)N * (K / BK) * 2;
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)((nrec + 255) / 256)), dim3(256), 0, s, ra);
+    RecArgs ra{wq->fmt, wq->scale, wq->zero, wq->nf4_absmax, wq->e8m0, wq->codes, mask, N, K, code_bits, cols, rec};
+    const int64_t nwaves = (int64_t)N * ((2 * (K / BK) + 63) / 64);
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)((nwaves + 3) / 4)), dim3(256), 0, s, ra);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;
     a.Xh = Xh;
     a.rowscale = rowscale;
+    a.xc = xq->codes;
+    a.xs = xq->scale;
+    a.xz = xq->zero;
     a.cols = cols;
     a.rec = rec;
     a.Y = Y;
@@ -710,11 +745,13 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     a.row0 = 0;
     a.row1 = M;
     a.tn = (N + BN - 1) / BN;
+    const int af = amx ? kAF16
+                       : (xq->fmt == CHAM_A_INT8_ASYM ? kAInt8 : (xq->fmt == CHAM_A_FP8_E4M3 ? kAE4M3 : kAE5M2));
     Launch plan[2];
     const int nl = plan_gemm(M, N, K, plan);
     for (int i = 0; i < nl; ++i) {
-        if (code_bits == 4) launch_gemm<4>(a, plan[i], s);
-        else launch_gemm<8>(a, plan[i], s);
+        if (code_bits == 4) launch_gemm<4>(a, plan[i], af, s);
+        else launch_gemm<8>(a, plan[i], af, s);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;

@@ -477,61 +477,127 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     }
 }
 
-// Stable counting sort of channels by format, in one workgroup of 1024 threads: format
-// totals first, then chunks of 1024 consecutive rows in order, each row placed at its
-// group's running offset plus its rank among equal formats earlier in the chunk (wave
-// ballots and per-wave counts).
-__global__ __launch_bounds__(1024) void group_kernel(const uint8_t* fmt, int64_t N, int32_t* perm,
-                                                     int32_t* group_off) {
-    __shared__ int32_t wcnt[16][CHAM_W_NFMT];
-    __shared__ int32_t base[CHAM_W_NFMT + 1];
-    __shared__ int32_t tot[CHAM_W_NFMT];
+// Stable counting sort of channels by format.  Workgroup b owns a run of consecutive
+// channels; it counts every format over all channels (those before its run and the
+// total; the format bytes are small and cached), which gives the group offsets and its
+// starting position inside every group.  It then walks its run 256 channels at a time:
+// a channel's position adds the count of equal formats in earlier waves (wave totals in
+// LDS) and in earlier lanes (ballot prefix).
+constexpr int kGroupThreads = 256;
+constexpr int kGroupMaxBlocks = 256;
+
+CHAM_DEV int group_run(int64_t N) {
+    int64_t run = (N + kGroupMaxBlocks - 1) / kGroupMaxBlocks;
+    run = (run + 1023) / 1024 * 1024;
+    return (int)run;
+}
+
+__global__ __launch_bounds__(kGroupThreads) void group_kernel(const uint8_t* fmt, int64_t N, int32_t* perm,
+                                                                int32_t* group_off) {
+    __shared__ int32_t cnt[2][CHAM_W_NFMT];  // [0] before the run, [1] all channels
+    __shared__ int32_t wc[kGroupThreads / kWave][CHAM_W_NFMT];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    if (t < CHAM_W_NFMT) tot[t] = 0;
-    __syncthreads();
-    int32_t c[CHAM_W_NFMT];
+    const int64_t run = group_run(N);
+    const int64_t r0 = (int64_t)blockIdx.x * run, r1 = r0 + run < N ? r0 + run : N;
+    if (t < 2 * CHAM_W_NFMT) cnt[t / CHAM_W_NFMT][t % CHAM_W_NFMT] = 0;
+    // the formats of this thread's channels in the first four chunks of the run, loaded
+    // now so their latency overlaps the counting pass
+    int pre[4];
 #pragma unroll
-    for (int f = 0; f < CHAM_W_NFMT; ++f) c[f] = 0;
-    for (int64_t r = t; r < N; r += 1024) {
-        const int f = fmt[r];
-#pragma unroll
-        for (int g = 0; g < CHAM_W_NFMT; ++g) c[g] += (f == g);
+    for (int c = 0; c < 4; ++c) {
+        const int64_t r = r0 + (int64_t)c * kGroupThreads + t;
+        pre[c] = perm && r < r1 ? (int)fmt[r] : CHAM_W_NFMT;
     }
-#pragma unroll
-    for (int f = 0; f < CHAM_W_NFMT; ++f)
-        if (c[f]) atomicAdd(&tot[f], c[f]);
     __syncthreads();
-    if (t == 0) {
+    {
+        int32_t before[CHAM_W_NFMT], all[CHAM_W_NFMT];
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) before[f] = all[f] = 0;
+        auto count = [&](uint32_t w, int64_t r) {  // 4 format bytes of channels r .. r + 3
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int f = (w >> (8 * e)) & 255u;
+                const int b = r + e < r0;
+#pragma unroll
+                for (int g = 0; g < CHAM_W_NFMT; ++g) {
+                    all[g] += f == g;
+                    before[g] += (f == g) & b;
+                }
+            }
+        };
+        int64_t done = 0;
+        if (((uintptr_t)fmt & 15u) == 0) {  // 16 channels per load
+            const uint4* f4 = reinterpret_cast<const uint4*>(fmt);
+            const int64_t nq = N >> 4;
+#pragma unroll 2
+            for (int64_t q = t; q < nq; q += kGroupThreads) {
+                const uint4 v = f4[q];
+                count(v.x, 16 * q); count(v.y, 16 * q + 4); count(v.z, 16 * q + 8); count(v.w, 16 * q + 12);
+            }
+            done = nq << 4;
+        }
+        // remaining channels one at a time (the other three bytes 0xFF match no format)
+        for (int64_t r = done + t; r < N; r += kGroupThreads) count(0xFFFFFF00u | fmt[r], r);
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            int32_t u = before[f], v = all[f];
+            for (int o = 32; o > 0; o >>= 1) {
+                u += __shfl_xor(u, o, kWave);
+                v += __shfl_xor(v, o, kWave);
+            }
+            if (lane == 0) {
+                if (u) atomicAdd(&cnt[0][f], u);
+                if (v) atomicAdd(&cnt[1][f], v);
+            }
+        }
+    }
+    __syncthreads();
+    int32_t base[CHAM_W_NFMT];
+    {
         int32_t acc = 0;
-        for (int f = 0; f < CHAM_W_NFMT; ++f) { base[f] = acc; acc += tot[f]; }
-        base[CHAM_W_NFMT] = acc;
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            base[f] = acc + cnt[0][f];
+            acc += cnt[1][f];
+        }
+        if (group_off && blockIdx.x == 0 && t == 0) {
+            int32_t o = 0;
+#pragma unroll
+            for (int f = 0; f < CHAM_W_NFMT; ++f) {
+                group_off[f] = o;
+                o += cnt[1][f];
+            }
+            group_off[CHAM_W_NFMT] = o;
+        }
     }
-    __syncthreads();
-    if (group_off && t <= CHAM_W_NFMT) group_off[t] = base[t];
     if (!perm) return;
     const uint64_t lt = (1ull << lane) - 1ull;
-    for (int64_t chunk = 0; chunk < N; chunk += 1024) {
-        const int64_t r = chunk + t;
-        const int f = r < N ? (int)fmt[r] : CHAM_W_NFMT;
+    for (int64_t c0 = r0, ci = 0; c0 < r1; c0 += kGroupThreads, ++ci) {
+        const int64_t r = c0 + t;
+        const int f = ci < 4 ? (ci == 0 ? pre[0] : ci == 1 ? pre[1] : ci == 2 ? pre[2] : pre[3])
+                             : (r < r1 ? (int)fmt[r] : CHAM_W_NFMT);
         int rank = 0;
 #pragma unroll
         for (int g = 0; g < CHAM_W_NFMT; ++g) {
             const uint64_t m = __ballot(f == g);
-            if (lane == 0) wcnt[wave][g] = __popcll(m);
+            if (lane == 0) wc[wave][g] = __popcll(m);
             if (f == g) rank = __popcll(m & lt);
         }
         __syncthreads();
-        if (f < CHAM_W_NFMT) {
-            int32_t pos = base[f] + rank;
-            for (int w = 0; w < wave; ++w) pos += wcnt[w][f];
-            perm[pos] = (int32_t)r;
+        int32_t pos = 0;
+#pragma unroll
+        for (int g = 0; g < CHAM_W_NFMT; ++g) {
+            int32_t earlier = 0, chunk = 0;
+#pragma unroll
+            for (int w = 0; w < kGroupThreads / kWave; ++w) {
+                const int32_t v = wc[w][g];
+                earlier += w < wave ? v : 0;
+                chunk += v;
+            }
+            if (f == g) pos = base[g] + earlier + rank;
+            base[g] += chunk;
         }
-        __syncthreads();
-        if (t < CHAM_W_NFMT) {
-            int32_t sum = 0;
-            for (int w = 0; w < 16; ++w) sum += wcnt[w][t];
-            base[t] += sum;
-        }
+        if (f < CHAM_W_NFMT) perm[pos] = (int32_t)r;
         __syncthreads();
     }
 }
@@ -591,7 +657,9 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     else launch_search<32>(a, s);
     CHAM_CHECK_LAUNCH();
     if (wq->perm || wq->group_off) {
-        hipLaunchKernelGGL(group_kernel, dim3(1), dim3(1024), 0, s, wq->fmt, wq->N, wq->perm, wq->group_off);
+        const int64_t run = (((wq->N + kGroupMaxBlocks - 1) / kGroupMaxBlocks) + 1023) / 1024 * 1024;
+        hipLaunchKernelGGL(group_kernel, dim3((unsigned)((wq->N + run - 1) / run)), dim3(kGroupThreads), 0, s, wq->fmt,
+                           wq->N, wq->perm, wq->group_off);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;

@@ -14,7 +14,7 @@ namespace cham {
 namespace {
 
 constexpr int kStatsThreads = 256;
-constexpr int kStatsMaxBlocks = 1024;
+constexpr int kStatsMaxBlocks = 2048;
 
 struct Partial {
     double s1, s2, s3, s4;
@@ -29,9 +29,8 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
     const int64_t nq = numel >> 2;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const float4* X4 = reinterpret_cast<const float4*>(X);
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
-        float4 t = X4[i];
-        float e[4] = {t.x, t.y, t.z, t.w};
+    auto add = [&](const float4& t) {
+        const float e[4] = {t.x, t.y, t.z, t.w};
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             double d = (double)e[j];
@@ -43,7 +42,14 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
             lo = fminf(lo, e[j]);
             hi = fmaxf(hi, e[j]);
         }
+    };
+    // four loads in flight per thread, then their sums in index order
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < nq; i += 4 * stride) {
+        const float4 t0 = X4[i], t1 = X4[i + stride], t2 = X4[i + 2 * stride], t3 = X4[i + 3 * stride];
+        add(t0); add(t1); add(t2); add(t3);
     }
+    for (; i < nq; i += stride) add(X4[i]);
     // scalar tail (numel % 4), handled by the first threads of workgroup 0
     if (blockIdx.x == 0 && threadIdx.x < (numel & 3)) {
         float x = X[(nq << 2) + threadIdx.x];
@@ -69,6 +75,15 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
 
 __global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Partial* part, int nparts,
                                                                         int64_t numel, double* nS, float* lohi) {
+    // the accumulator is read at the start so its latency overlaps the partial loads
+    double acc[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
+    float alo = 0.0f, ahi = 0.0f;
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k) acc[k] = nS[k];
+        alo = lohi[0];
+        ahi = lohi[1];
+    }
     double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
     float lo = INFINITY, hi = -INFINITY;
     for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {
@@ -87,13 +102,13 @@ __global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Par
             r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
             r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
         }
-        nS[0] += (double)numel;
-        nS[1] += r.s1;
-        nS[2] += r.s2;
-        nS[3] += r.s3;
-        nS[4] += r.s4;
-        lohi[0] = fminf(lohi[0], r.lo);
-        lohi[1] = fmaxf(lohi[1], r.hi);
+        nS[0] = acc[0] + (double)numel;
+        nS[1] = acc[1] + r.s1;
+        nS[2] = acc[2] + r.s2;
+        nS[3] = acc[3] + r.s3;
+        nS[4] = acc[4] + r.s4;
+        lohi[0] = fminf(alo, r.lo);
+        lohi[1] = fmaxf(ahi, r.hi);
     }
 }
 
@@ -213,7 +228,7 @@ extern "C" int cham_act_stats_reset(cham_act_stats* st, void* stream) {
 
 static int stats_blocks(int64_t numel) {
     int64_t nq = numel >> 2;
-    int64_t b = (nq + kStatsThreads * 8 - 1) / (kStatsThreads * 8);  // >= 8 float4 per thread
+    int64_t b = (nq + kStatsThreads * 2 - 1) / (kStatsThreads * 2);  // >= 2 float4 per thread
     if (b < 1) b = 1;
     if (b > kStatsMaxBlocks) b = kStatsMaxBlocks;
     return (int)b;

@@ -123,8 +123,10 @@ def test_search_full_size_sampled():
         assert np.array_equal(_np(wq.scale)[rows], ref["scale"])
         assert np.array_equal(_np(wq.nf4_absmax)[rows], ref["nf4_absmax"])
         assert np.array_equal(_np(wq.e8m0)[rows], ref["e8m0"])
-        # perm is a stable sort of the GPU's own format vector
+        # perm is a stable sort of the GPU's own format vector, group_off its group starts
         assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable"))
+        counts = np.bincount(f, minlength=9)
+        assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(counts)]))
 
 
 # ---------------------------------------------------------------------------------------
