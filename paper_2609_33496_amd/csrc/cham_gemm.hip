@@ -13,23 +13,27 @@
 // rounding (relative error <= 2^-11).  8-bit integer formats are decoded arithmetically
 // (1024 + c trick, exact) with parameters from the same table slot.
 //
-// The same pre-pass decodes the activations once per call into a half-precision copy in
-// the workspace (exact for every activation format) with a per-row scale.
+// Activations in a per-tensor format (INT8, E4M3, E5M2) are decoded to half precision
+// while they are staged into LDS (exact); MX activations are decoded by a pre-pass into a
+// half-precision copy relative to the row's largest block exponent, with a row scale.
 //
 // Main kernel: BM x 256 output tiles (BM = 256, 128 or 64), k-steps of 64, four
 // wavefronts that each own BM rows x 64 channels (BM/32 x 2 blocks of
 // v_mfma_f32_32x32x16_f16, binary32 accumulation), so a decoded weight feeds BM/16 MFMAs.
-// The activation tile and the weight records of step k + 2 go global -> registers with
-// coalesced 16-byte loads while step k computes, and into one of two LDS buffers at the
-// end of step k + 1; the activation tile is stored with its 16-byte chunks XOR-swizzled
-// per row pair and the records piece-major, so all LDS reads are free of bank conflicts.
-// Barriers fence LDS only, so the prefetch stays in flight across them.  Each output
-// element is written once (no atomics), so results do not depend on scheduling.
+// Activation tiles and weight records go global -> registers with coalesced 16-byte
+// buffer loads one or more k-steps ahead (deeper register rings for the short steps of
+// small tiles); the activation tile is stored into one of two LDS buffers with its
+// 16-byte chunks XOR-swizzled per row pair, so all LDS accesses are free of bank
+// conflicts, and the weight records stay in registers.  Barriers fence LDS only, so the
+// prefetch stays in flight across them.  Layers with too few output tiles to fill the
+// CUs split k over several workgroups that write partial outputs, summed in split order
+// by a second kernel; every output element is produced by plain stores (no atomics), so
+// results do not depend on scheduling.
 //
 // The MFMA contracts over k in any order as long as both operands agree: lane half h of a
 // k-step takes k = 32h .. 32h+31, sub-step s the 8 k at 32h + 8s, and with two codes per
-// byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation copy stores its
-// columns in that same order.
+// byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation operand is
+// staged with its columns in that same order.
 #include "cham_device.h"
 
 namespace cham {
@@ -165,6 +169,73 @@ CHAM_DEV Table int8_record(uint32_t xmask, float zoff, float factor) {
     return Table{{xmask, half_pair(-(1024.0f + zoff)), half_pair(factor), 0u}, {0u, 0u, 0u, 0u}};
 }
 
+// ------------------------------------------------------------------------------------
+// weight decode in the main kernel
+// ------------------------------------------------------------------------------------
+
+// Look up 4 codes (one per byte, values 0..15); returns the low and high bytes.
+CHAM_DEV void lookup4(const Table& t, uint32_t codes, uint32_t& lo, uint32_t& hi) {
+    const uint32_t sel = codes & 0x07070707u;
+    const uint32_t sel2 = 0x03020100u | ((codes >> 1) & 0x04040404u);
+    const uint32_t l0 = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
+    const uint32_t l1 = __builtin_amdgcn_perm(t.lo[3], t.lo[2], sel);
+    const uint32_t h0 = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
+    const uint32_t h1 = __builtin_amdgcn_perm(t.hi[3], t.hi[2], sel);
+    lo = __builtin_amdgcn_perm(l1, l0, sel2);
+    hi = __builtin_amdgcn_perm(h1, h0, sel2);
+}
+
+union H8 {
+    half8 h;
+    uint32_t u[4];
+};
+
+// 8 codes of one sub-step from a word of 8 nibbles -> order (0,4,1,5,2,6,3,7)
+CHAM_DEV half8 decode_nibbles(const Table& t, uint32_t w) {
+    uint32_t lo_e, hi_e, lo_o, hi_o;
+    lookup4(t, w & 0x0F0F0F0Fu, lo_e, hi_e);         // k = 0, 2, 4, 6
+    lookup4(t, (w >> 4) & 0x0F0F0F0Fu, lo_o, hi_o);  // k = 1, 3, 5, 7
+    H8 r;
+    r.u[0] = __builtin_amdgcn_perm(hi_e, lo_e, 0x06020400u);  // k0, k4
+    r.u[1] = __builtin_amdgcn_perm(hi_o, lo_o, 0x06020400u);  // k1, k5
+    r.u[2] = __builtin_amdgcn_perm(hi_e, lo_e, 0x07030501u);  // k2, k6
+    r.u[3] = __builtin_amdgcn_perm(hi_o, lo_o, 0x07030501u);  // k3, k7
+    return r.h;
+}
+
+// 8 codes in natural order from two words of 4 byte-codes (4-bit formats in 8-bit layout)
+CHAM_DEV half8 decode_bytes_table(const Table& t, uint32_t w0, uint32_t w1) {
+    uint32_t lo0, hi0, lo1, hi1;
+    lookup4(t, w0, lo0, hi0);
+    lookup4(t, w1, lo1, hi1);
+    H8 r;
+    r.u[0] = __builtin_amdgcn_perm(hi0, lo0, 0x05010400u);
+    r.u[1] = __builtin_amdgcn_perm(hi0, lo0, 0x07030602u);
+    r.u[2] = __builtin_amdgcn_perm(hi1, lo1, 0x05010400u);
+    r.u[3] = __builtin_amdgcn_perm(hi1, lo1, 0x07030602u);
+    return r.h;
+}
+
+// 8-bit integer codes: value = ((c ^ x) - zoff) * factor, through 1024 + c in half
+// precision; x, -(1024 + zoff) and the factor come from the table slot.
+CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
+    w0 ^= t.lo[0];
+    w1 ^= t.lo[0];
+    H8 r;
+    r.u[0] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04010400u);
+    r.u[1] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04030402u);
+    r.u[2] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04010400u);
+    r.u[3] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04030402u);
+    const half2v off = __builtin_bit_cast(half2v, t.lo[1]), fac = __builtin_bit_cast(half2v, t.lo[2]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        half2v v = __builtin_bit_cast(half2v, r.u[i]);
+        v = (v + off) * fac;
+        r.u[i] = __builtin_bit_cast(uint32_t, v);
+    }
+    return r.h;
+}
+
 struct RecArgs {
     const uint8_t* wfmt;
     const float* wscale;
@@ -249,73 +320,6 @@ __global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
     }
 }
 
-// ------------------------------------------------------------------------------------
-// weight decode in the main kernel
-// ------------------------------------------------------------------------------------
-
-// Look up 4 codes (one per byte, values 0..15); returns the low and high bytes.
-CHAM_DEV void lookup4(const Table& t, uint32_t codes, uint32_t& lo, uint32_t& hi) {
-    const uint32_t sel = codes & 0x07070707u;
-    const uint32_t sel2 = 0x03020100u | ((codes >> 1) & 0x04040404u);
-    const uint32_t l0 = __builtin_amdgcn_perm(t.lo[1], t.lo[0], sel);
-    const uint32_t l1 = __builtin_amdgcn_perm(t.lo[3], t.lo[2], sel);
-    const uint32_t h0 = __builtin_amdgcn_perm(t.hi[1], t.hi[0], sel);
-    const uint32_t h1 = __builtin_amdgcn_perm(t.hi[3], t.hi[2], sel);
-    lo = __builtin_amdgcn_perm(l1, l0, sel2);
-    hi = __builtin_amdgcn_perm(h1, h0, sel2);
-}
-
-union H8 {
-    half8 h;
-    uint32_t u[4];
-};
-
-// 8 codes of one sub-step from a word of 8 nibbles -> order (0,4,1,5,2,6,3,7)
-CHAM_DEV half8 decode_nibbles(const Table& t, uint32_t w) {
-    uint32_t lo_e, hi_e, lo_o, hi_o;
-    lookup4(t, w & 0x0F0F0F0Fu, lo_e, hi_e);         // k = 0, 2, 4, 6
-    lookup4(t, (w >> 4) & 0x0F0F0F0Fu, lo_o, hi_o);  // k = 1, 3, 5, 7
-    H8 r;
-    r.u[0] = __builtin_amdgcn_perm(hi_e, lo_e, 0x06020400u);  // k0, k4
-    r.u[1] = __builtin_amdgcn_perm(hi_o, lo_o, 0x06020400u);  // k1, k5
-    r.u[2] = __builtin_amdgcn_perm(hi_e, lo_e, 0x07030501u);  // k2, k6
-    r.u[3] = __builtin_amdgcn_perm(hi_o, lo_o, 0x07030501u);  // k3, k7
-    return r.h;
-}
-
-// 8 codes in natural order from two words of 4 byte-codes (4-bit formats in 8-bit layout)
-CHAM_DEV half8 decode_bytes_table(const Table& t, uint32_t w0, uint32_t w1) {
-    uint32_t lo0, hi0, lo1, hi1;
-    lookup4(t, w0, lo0, hi0);
-    lookup4(t, w1, lo1, hi1);
-    H8 r;
-    r.u[0] = __builtin_amdgcn_perm(hi0, lo0, 0x05010400u);
-    r.u[1] = __builtin_amdgcn_perm(hi0, lo0, 0x07030602u);
-    r.u[2] = __builtin_amdgcn_perm(hi1, lo1, 0x05010400u);
-    r.u[3] = __builtin_amdgcn_perm(hi1, lo1, 0x07030602u);
-    return r.h;
-}
-
-// 8-bit integer codes: value = ((c ^ x) - zoff) * factor, through 1024 + c in half
-// precision; x, -(1024 + zoff) and the factor come from the table slot.
-CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
-    w0 ^= t.lo[0];
-    w1 ^= t.lo[0];
-    H8 r;
-    r.u[0] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04010400u);
-    r.u[1] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04030402u);
-    r.u[2] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04010400u);
-    r.u[3] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04030402u);
-    const half2v off = __builtin_bit_cast(half2v, t.lo[1]), fac = __builtin_bit_cast(half2v, t.lo[2]);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        half2v v = __builtin_bit_cast(half2v, r.u[i]);
-        v = (v + off) * fac;
-        r.u[i] = __builtin_bit_cast(uint32_t, v);
-    }
-    return r.h;
-}
-
 // Workgroup barrier that orders LDS accesses only: outstanding global loads (the
 // prefetch) stay in flight.
 CHAM_DEV void lds_barrier() {
@@ -338,7 +342,10 @@ struct GemmArgs {
     float* Y;
     int M, N, K;
     int row0, row1;  // rows [row0, row1) of this launch
-    int tn;      // tile columns
+    int tn;          // tile columns
+    int splits;      // k-splits: workgroup b takes tile b % tiles and k-steps of split b / tiles
+    int kchunk;      // k-steps per split
+    float* part;     // splits > 1: [splits][M][N] partial outputs, summed by reduce_kernel
 };
 
 // Activation operand source: the half-precision copy of the pre-pass (MX formats), or the
@@ -376,10 +383,10 @@ CHAM_DEV uint4 decode_act8(uint32_t w0, uint32_t w1, bool perm4, half2v negz) {
 }
 
 template <int CODE_BITS, int TM, int AF>
-__global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void gemm_kernel(GemmArgs a) {
     constexpr int BM = 32 * TM;
-    constexpr int CW = CODE_BITS / 4;           // 16-byte code pieces per record
-    constexpr int P = CW + 2;                   // 16-byte pieces per record
+    constexpr int CW = CODE_BITS / 4;  // 16-byte code pieces per record
+    constexpr int P = CW + 2;          // 16-byte pieces per record (codes + two table planes)
     constexpr int AQ = AF == kAF16 ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
     constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
     __shared__ uint4 lds[2][A_CH];
@@ -389,9 +396,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     const int lane = t & 63, wave = t >> 6;
     const int l32 = lane & 31, h = lane >> 5;
     const int K = a.K, N = a.N;
-    const int nsteps = K / BK;
-    const int m0 = a.row0 + ((int)blockIdx.x / a.tn) * BM, n0 = ((int)blockIdx.x % a.tn) * BN;
+    const int tiles = ((a.row1 - a.row0 + BM - 1) / BM) * a.tn;
+    const int tile = (int)blockIdx.x % tiles, split = (int)blockIdx.x / tiles;
+    const int m0 = a.row0 + (tile / a.tn) * BM, n0 = (tile % a.tn) * BN;
     const int rows = a.row1 - m0 < BM ? a.row1 - m0 : BM;
+    // k-steps [kb, kb + nsteps) of this workgroup; the operand bases below start at kb
+    const int kb = split * a.kchunk;
+    const int nsteps = K / BK - kb < a.kchunk ? K / BK - kb : a.kchunk;
 
     if (t < BM) Rs[t] = AF == kAF16 ? a.rowscale[t < rows ? m0 + t : m0] : *a.xs;
     half2v negz = {(_Float16)0.0f, (_Float16)0.0f};
@@ -408,10 +419,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     //  codes: load q is row q >> 2, codes 16 (q & 3) .. + 15 = chunks 2 (q & 3), + 1.
     const bool perm4 = CODE_BITS == 4;
     const __amdgpu_buffer_rsrc_t ra =
-        AF == kAF16 ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.Xh + (int64_t)m0 * K), (short)0, rows * K * 2,
-                                                        kBufferFlags)
-                    : __builtin_amdgcn_make_buffer_rsrc((void*)(a.xc + (int64_t)m0 * K), (short)0, rows * K,
-                                                        kBufferFlags);
+        AF == kAF16 ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.Xh + (int64_t)m0 * K + kb * BK), (short)0,
+                                                        (rows * K - kb * BK) * 2, kBufferFlags)
+                    : __builtin_amdgcn_make_buffer_rsrc((void*)(a.xc + (int64_t)m0 * K + kb * BK), (short)0,
+                                                        rows * K - kb * BK, kBufferFlags);
     const uint32_t aoff0 = AF == kAF16 ? (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4))
                                        : (uint32_t)((t >> 2) * K + ((t & 3) << 4));
     struct AStage {
@@ -449,7 +460,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     const int nl = 64 * wave + l32;
     const int chans = N - n0 < BN ? N - n0 : BN;
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(a.rec + (int64_t)n0 * 2 * P), (short)0, (int)(((int64_t)nsteps * N - n0) * 2 * P * 16), kBufferFlags);
+        (void*)(a.rec + ((int64_t)kb * N + n0) * 2 * P), (short)0, (int)(((int64_t)(K / BK - kb) * N - n0) * 2 * P * 16),
+        kBufferFlags);
     const uint32_t rstep = (uint32_t)N * 2u * P * 16u;  // record bytes per k-step
     struct Rec {
         uint4 c[CW];
@@ -473,11 +485,16 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
         }
     };
 
-    bool int8[TN];  // 8-bit code layout: the channel decodes arithmetically
+    // per-channel parameters of the lane's two channels: 8-bit code layout decoded
+    // arithmetically, epilogue factor (loaded here, off the tail of the kernel)
+    bool int8[TN];
+    float cs[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int n = n0 + nl + 32 * j;
-        int8[j] = CODE_BITS == 8 && n < N && is_8bit(a.cols[n].fmt);
+        const ColPrep cp = n < N ? a.cols[n] : ColPrep{CHAM_W_NFMT, 0, 0.0f, 0.0f};
+        int8[j] = CODE_BITS == 8 && is_8bit(cp.fmt);
+        cs[j] = cp.colscale;
     }
     auto decode = [&](const Rec& r, int j, int s) __attribute__((always_inline)) -> half8 {
         if (CODE_BITS == 4) {
@@ -504,70 +521,92 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    auto compute = [&](int buf, const WStage& W) __attribute__((always_inline)) {
-        const uint4* L = lds[buf];
-        half8 af[TM], bf[TN], bn[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) af[i] = __builtin_bit_cast(half8, L[i * 256 + aoff[0]]);
-#pragma unroll
-        for (int j = 0; j < TN; ++j) bf[j] = decode(W.r[j], j, 0);
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if (s < 3) {
-#pragma unroll
-                for (int j = 0; j < TN; ++j) bn[j] = decode(W.r[j], j, s + 1);
-            }
-#pragma unroll
-            for (int i = 0; i < TM; ++i) {
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
-                if (s < 3) af[i] = __builtin_bit_cast(half8, L[i * 256 + aoff[s + 1]]);
-            }
-            if (s < 3) {
-#pragma unroll
-                for (int j = 0; j < TN; ++j) bf[j] = bn[j];
-            }
-        }
-    };
-
-    // ---- main loop.  Activation register stages R0 / R1 alternate (a k-step is loaded two
-    // steps before it is computed); weight stages W0 / W1 alternate (loaded one step
-    // ahead).  Invariant at the top: LDS buffer 0 and W0 hold step k, R1 step k + 1.  Step
-    // indices past the end are clamped to the last step (harmless reloads), so the loop
-    // body has no data-dependent branches.
+    // ---- main loop.  Step k computes from LDS buffer k & 1.  At its start it stores the
+    // activation tile of step k + 1 (loaded DA steps earlier) into the other buffer and
+    // issues the loads of step k + 1 + DA (activations) and k + DW (weights) into register
+    // rings of DA and DW + 1 stages; short steps (small tiles) take deeper rings so the
+    // loads have more than one memory latency to arrive.  Sub-steps 0-2 run with the
+    // operand reads and weight decode one sub-step ahead; then one barrier makes the new
+    // tile visible (and retires every read of this step's buffer), and the first operands
+    // of step k + 1 are read and decoded behind the MFMAs of sub-step 3.  Step indices past
+    // the end are clamped (harmless reloads); scheduling barriers keep the compiler from
+    // sinking the reads next to their uses.  The loop is unrolled by a multiple of both
+    // ring lengths so every ring index is a constant.
+    constexpr int DW = TM == 2 ? 3 : 1;
+    constexpr int DA = TM == 2 ? 2 : 1;
+    constexpr int U = (DW + 1) > 2 ? (DW + 1) : 2;  // DA divides it
     const int klast = nsteps - 1;
-    AStage R0, R1;
-    WStage W0, W1;
-    load_w(W0, 0);
-    load_a(R0, 0);
-    load_a(R1, klast < 1 ? klast : 1);
-    store_a(R0, 0);
+    AStage R[DA];
+    WStage W[DW + 1];
+    half8 af[TM], an[TM], bf[TN], bn[TN];
+#pragma unroll
+    for (int d = 0; d < DW; ++d) load_w(W[d], d < klast ? d : klast);
+    load_a(R[0], 0);
+    store_a(R[0], 0);
+#pragma unroll
+    for (int d = 1; d <= DA; ++d) load_a(R[d % DA], d < klast ? d : klast);
     lds_barrier();
+#pragma unroll
+    for (int i = 0; i < TM; ++i) af[i] = __builtin_bit_cast(half8, lds[0][i * 256 + aoff[0]]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bf[j] = decode(W[0].r[j], j, 0);
+
+    auto mfmas = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    };
+    auto step = [&](int k, int buf, const WStage& Wc, const WStage& Wn, WStage& Wl, AStage& Ra)
+                    __attribute__((always_inline)) {
+        if (k + 1 < nsteps) store_a(Ra, buf ^ 1);
+        load_a(Ra, k + 1 + DA < klast ? k + 1 + DA : klast);
+        load_w(Wl, k + DW < klast ? k + DW : klast);
+        const uint4* L = lds[buf];
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) an[i] = __builtin_bit_cast(half8, L[i * 256 + aoff[s + 1]]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bn[j] = decode(Wc.r[j], j, s + 1);
+            mfmas();
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) af[i] = an[i];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bf[j] = bn[j];
+        }
+        lds_barrier();
+        const uint4* Ln = lds[buf ^ 1];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) an[i] = __builtin_bit_cast(half8, Ln[i * 256 + aoff[0]]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bn[j] = decode(Wn.r[j], j, 0);
+        mfmas();
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[i] = an[i];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) bf[j] = bn[j];
+    };
     int k = 0;
-    for (; k + 2 <= nsteps; k += 2) {
-        load_w(W1, k + 1);
-        load_a(R0, k + 2 < klast ? k + 2 : klast);
-        compute(0, W0);
-        store_a(R1, 1);
-        lds_barrier();
-        load_w(W0, k + 2 < klast ? k + 2 : klast);
-        load_a(R1, k + 3 < klast ? k + 3 : klast);
-        compute(1, W1);
-        store_a(R0, 0);
-        lds_barrier();
+    for (; k + U <= nsteps; k += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            step(k + u, u & 1, W[u % (DW + 1)], W[(u + 1) % (DW + 1)], W[(u + DW) % (DW + 1)], R[(u + 1) % DA]);
     }
-    if (k < nsteps) compute(0, W0);
+#pragma unroll
+    for (int u = 0; u + 1 < U; ++u)
+        if (k + u < nsteps)
+            step(k + u, u & 1, W[u % (DW + 1)], W[(u + 1) % (DW + 1)], W[(u + DW) % (DW + 1)], R[(u + 1) % DA]);
 
     // ---- epilogue: 32x32 block, lane holds column l32, rows 8*(r/4) + 4*h + r%4; the
     // lane's 16 row scales of block i are 4 aligned float4 in LDS
-    float cs[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int n = n0 + nl + 32 * j;
-        cs[j] = n < N ? a.cols[n].colscale : 0.0f;
-    }
     const bool full = rows == BM && n0 + BN <= N;
+    float* const out = a.splits > 1 ? a.part + (int64_t)split * a.M * N : a.Y;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         float rs[16];
@@ -579,7 +618,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const int n = n0 + nl + 32 * j;
-            float* base = a.Y + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
+            float* base = out + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
             if (full) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
@@ -595,9 +634,37 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_kernel(GemmArgs a) {
     }
 }
 
-// ---- launch plan.  A launch covers rows [row0, M) with one tile height; the plan may
-// use a second launch with a smaller tile height for the rows left after the full rounds
-// of the first, so the last round does not leave most CUs idle.
+// Sum of the k-split partial outputs in split order (the result does not depend on the
+// order in which workgroups ran); 4 outputs per thread when M N is a multiple of 4.
+__global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ part, float* __restrict__ Y,
+                                                     int64_t MN, int splits) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if ((MN & 3) == 0) {
+        const float4* p4 = reinterpret_cast<const float4*>(part);
+        float4* y4 = reinterpret_cast<float4*>(Y);
+        const int64_t n4 = MN >> 2;
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+            float4 acc = p4[i];
+            for (int sp = 1; sp < splits; ++sp) {
+                const float4 v = p4[(int64_t)sp * n4 + i];
+                acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+            }
+            y4[i] = acc;
+        }
+    } else {
+        for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < MN; i += stride) {
+            float acc = part[i];
+            for (int sp = 1; sp < splits; ++sp) acc += part[(int64_t)sp * MN + i];
+            Y[i] = acc;
+        }
+    }
+}
+
+// ---- launch plan.  A launch covers rows [row0, row1) with one tile height.  The plan is
+// either one launch, optionally split along k into partial outputs that reduce_kernel
+// sums (for layers with too few output tiles to fill the CUs), or two launches of
+// different tile heights: the larger for whole rounds of workgroups, the smaller for the
+// rows left, so the last round does not leave most CUs idle.
 int cu_count() {
     static int cached[64] = {0};
     int dev = 0;
@@ -610,49 +677,83 @@ int cu_count() {
     return cached[dev];
 }
 
-// Modeled time (us) of a launch of tile height bm over `rows` rows: rounds of workgroups
-// over the CUs times the k-steps at a per-step cost that grows with the tile height, plus
-// the output write (costs measured on MI355X for these kernels).
-double launch_cost(int rows, int tn, int nsteps, int bm, int P) {
-    if (rows <= 0) return 0.0;
-    const int64_t tiles = (int64_t)((rows + bm - 1) / bm) * tn;
-    const double rounds = (double)((tiles + P - 1) / P);
-    const double step = bm == 256 ? 1.7 : (bm == 128 ? 1.1 : 0.66);
-    const double epi = bm == 256 ? 6.5 : (bm == 128 ? 3.5 : 2.0);
-    return rounds * nsteps * step + epi;
+// Modeled time (us) of a launch of one tile height: per-step and fixed (prologue, output
+// write) cost of a workgroup, measured on MI355X for these kernels.  Tile height 128 with
+// 4-bit codes fits two workgroups on a CU; each then runs at the slower shared-CU step cost.
+struct TileCost {
+    int bm, occ;
+    double step1, step2, fixed;  // us: step alone on the CU, step sharing it, fixed
+};
+constexpr TileCost kTileCosts[3] = {{256, 1, 1.75, 1.75, 14.0}, {128, 2, 1.12, 1.35, 9.0}, {64, 1, 0.78, 0.78, 6.0}};
+
+double launch_cost(int64_t wgs, int nsteps, const TileCost& c, int P) {
+    if (wgs <= 0) return 0.0;
+    const int64_t slots = (int64_t)c.occ * P;
+    const int64_t full = wgs / slots, rem = wgs % slots;
+    const double t_alone = nsteps * c.step1 + c.fixed, t_shared = nsteps * c.step2 + c.fixed;
+    return full * t_shared + (rem == 0 ? 0.0 : (rem <= P ? t_alone : t_shared));
 }
 
 struct Launch {
     int row0, row1, bm;
 };
-int plan_gemm(int M, int N, int K, Launch (&out)[2]) {
+struct Plan {
+    int n;       // launches
+    int splits;  // k-splits of a single launch (1: none)
+    Launch l[2];
+};
+// k-split reduction: one extra launch reading the partials and writing the output
+// (modeled at 5 TB/s)
+double reduce_cost(int64_t M, int64_t N, int splits) {
+    return splits > 1 ? 3.0 + (double)(splits + 1) * (double)(M * N * 4) / 5.0e6 : 0.0;
+}
+constexpr int kMaxSplits = 8;
+
+Plan plan_gemm(int M, int N, int K, int code_bits) {
     const int P = cu_count();
     const int tn = (N + BN - 1) / BN, nsteps = K / BK;
-    const int bms[3] = {256, 128, 64};
+    TileCost costs[3] = {kTileCosts[0], kTileCosts[1], kTileCosts[2]};
+    if (code_bits != 4) costs[1].occ = 1;
     double best = 1e300;
-    int n = 0;
+    Plan plan{1, 1, {Launch{0, M, 64}, Launch{0, 0, 0}}};
     for (int b = 0; b < 3; ++b) {
-        const double c = launch_cost(M, tn, nsteps, bms[b], P);
-        if (c < best) { best = c; n = 1; out[0] = Launch{0, M, bms[b]}; }
+        for (int sp = 1; sp <= kMaxSplits && sp <= nsteps; ++sp) {
+            const int kchunk = (nsteps + sp - 1) / sp;
+            if (sp > 1 && (sp - 1) * kchunk >= nsteps) continue;  // an empty split
+            const int64_t tiles = (int64_t)((M + costs[b].bm - 1) / costs[b].bm) * tn;
+            const double c = launch_cost(tiles * sp, kchunk, costs[b], P) + reduce_cost(M, N, sp);
+            if (c < best) { best = c; plan = Plan{1, sp, {Launch{0, M, costs[b].bm}, Launch{0, 0, 0}}}; }
+        }
     }
-    // big tiles for whole rounds of full tile rows, then smaller tiles for the rest
+    // larger tiles for whole rounds of full tile rows, then smaller tiles for the rest
     for (int b = 0; b < 2; ++b) {
-        const int bm = bms[b];
-        const int rows_per_round = (P / tn) * bm;
+        const TileCost& c1 = costs[b];
+        const int rows_per_round = (c1.occ * P / tn) * c1.bm;
         if (rows_per_round <= 0) continue;
         const int r1 = (M / rows_per_round) * rows_per_round;
         if (r1 <= 0 || r1 >= M) continue;
         for (int b2 = b + 1; b2 < 3; ++b2) {
-            const double c = launch_cost(r1, tn, nsteps, bm, P) + launch_cost(M - r1, tn, nsteps, bms[b2], P);
-            if (c < best) { best = c; n = 2; out[0] = Launch{0, r1, bm}; out[1] = Launch{r1, M, bms[b2]}; }
+            const double c = launch_cost((int64_t)(r1 / c1.bm) * tn, nsteps, c1, P) +
+                             launch_cost((int64_t)((M - r1 + costs[b2].bm - 1) / costs[b2].bm) * tn, nsteps, costs[b2], P);
+            if (c < best) { best = c; plan = Plan{2, 1, {Launch{0, r1, c1.bm}, Launch{r1, M, costs[b2].bm}}}; }
         }
     }
-    return n;
+    return plan;
+}
+
+// partial-output bytes of the plan for these sizes (the larger of the two code widths)
+size_t split_bytes(int64_t M, int64_t N, int64_t K) {
+    size_t b = 0;
+    for (int bits = 4; bits <= 8; bits += 4) {
+        const Plan p = plan_gemm((int)M, (int)N, (int)K, bits);
+        if (p.splits > 1) b = std::max(b, (size_t)p.splits * (size_t)M * (size_t)N * 4);
+    }
+    return b;
 }
 
 template <int CODE_BITS, int AF>
 void launch_gemm_af(const GemmArgs& a, const Launch& l, hipStream_t s) {
-    const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn);
+    const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn * a.splits);
     if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8, AF>), dim3(grid), dim3(kThreads), 0, s, a);
     else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4, AF>), dim3(grid), dim3(kThreads), 0, s, a);
     else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2, AF>), dim3(grid), dim3(kThreads), 0, s, a);
@@ -671,7 +772,8 @@ void launch_gemm(GemmArgs a, const Launch& l, int af, hipStream_t s) {
 }
 
 size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
-int64_t record_bytes(int64_t N, int64_t K, int code_bits) { return N * (K / BK) * 2 * (code_bits / 4 + 2) * 16; }
+// weight record slots (48 or 64 bytes used) per (k-step, channel, half)
+int64_t record_bytes(int64_t N, int64_t K) { return N * (K / BK) * 2 * 64; }
 
 }  // namespace
 }  // namespace cham
@@ -680,7 +782,7 @@ using namespace cham;
 
 size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
     return align256((size_t)M * (size_t)K * 2) + align256((size_t)M * 4) + align256((size_t)N * sizeof(ColPrep)) +
-           (size_t)record_bytes(N, K, 8);
+           align256((size_t)record_bytes(N, K)) + split_bytes(M, N, K);
 }
 
 extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
@@ -697,7 +799,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     // 32-bit buffer offsets: a 256-row activation tile and the weight records stay below
     // 2^31 bytes
     if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || xq->K > (1 << 20) ||
-        record_bytes(wq->N, xq->K, code_bits) > (int64_t)INT32_MAX)
+        record_bytes(wq->N, xq->K) > (int64_t)INT32_MAX)
         return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
@@ -709,6 +811,10 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return CHAM_EWORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     const int M = (int)xq->M, N = (int)wq->N, K = (int)xq->K;
+    const Plan plan = plan_gemm(M, N, K, code_bits);
+    const int kchunk = (K / BK + plan.splits - 1) / plan.splits;
+    // every split holds at least one k-step (the operand ranges of the kernel rely on it)
+    if (plan.splits < 1 || (plan.splits - 1) * kchunk >= K / BK) return CHAM_ESHAPE;
 
     char* w = (char*)ws;
     _Float16* Xh = (_Float16*)w;
@@ -718,6 +824,8 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     ColPrep* cols = (ColPrep*)w;
     w += align256((size_t)N * sizeof(ColPrep));
     uint4* rec = (uint4*)w;
+    w += align256((size_t)record_bytes(N, K));
+    float* part = (float*)w;
 
     if (amx) {
         PrepArgs p{xq->codes, xq->e8m0, xq->fmt, M, K, code_bits == 4, Xh, rowscale};
@@ -725,7 +833,8 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
 
-    RecArgs ra{wq->fmt, wq->scale, wq->zero, wq->nf4_absmax, wq->e8m0, wq->codes, mask, N, K, code_bits, cols, rec};
+    RecArgs ra{wq->fmt, wq->scale, wq->zero, wq->nf4_absmax, wq->e8m0, wq->codes, mask, N, K, code_bits,
+               cols, rec};
     const int64_t nwaves = (int64_t)N * ((2 * (K / BK) + 63) / 64);
     hipLaunchKernelGGL(record_kernel, dim3((unsigned)((nwaves + 3) / 4)), dim3(256), 0, s, ra);
     CHAM_CHECK_LAUNCH();
@@ -745,13 +854,21 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     a.row0 = 0;
     a.row1 = M;
     a.tn = (N + BN - 1) / BN;
+    a.part = part;
     const int af = amx ? kAF16
                        : (xq->fmt == CHAM_A_INT8_ASYM ? kAInt8 : (xq->fmt == CHAM_A_FP8_E4M3 ? kAE4M3 : kAE5M2));
-    Launch plan[2];
-    const int nl = plan_gemm(M, N, K, plan);
-    for (int i = 0; i < nl; ++i) {
-        if (code_bits == 4) launch_gemm<4>(a, plan[i], af, s);
-        else launch_gemm<8>(a, plan[i], af, s);
+    a.splits = plan.splits;
+    a.kchunk = kchunk;
+    for (int i = 0; i < plan.n; ++i) {
+        if (code_bits == 4) launch_gemm<4>(a, plan.l[i], af, s);
+        else launch_gemm<8>(a, plan.l[i], af, s);
+        CHAM_CHECK_LAUNCH();
+    }
+    if (plan.splits > 1) {
+        const int64_t MN = (int64_t)M * N;
+        const int64_t per = (MN & 3) == 0 ? MN / 4 : MN;
+        const unsigned grid = (unsigned)std::min<int64_t>((per + 255) / 256, 4096);
+        hipLaunchKernelGGL(reduce_kernel, dim3(grid), dim3(256), 0, s, part, Y, MN, plan.splits);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;
