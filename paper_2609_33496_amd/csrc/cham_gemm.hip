@@ -245,78 +245,130 @@ struct RecArgs {
     const uint8_t* wc;
     uint32_t mask;
     int N, K, code_bits;
+    int kchunk;  // k-steps per workgroup
     ColPrep* cols;
     uint4* rec;  // [K/64][N][2][pieces]
 };
 
-// Wavefront w of the launch handles channel w / per and the (k-step, half) pairs
-// 64 (w % per) .. + 63 of it, per = ceil(2 K / 64 / 64): each computes the channel's
-// reference exponent (largest NF4 block absmax or MX block exponent, wavefront max) and
-// one record per lane; the first wavefront of a channel also stores its ColPrep.
-__global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
-    const int lane = threadIdx.x & 63;
-    const int per = (2 * (a.K / BK) + 63) / 64;
-    const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int n = (int)(wid / per), part = (int)(wid % per);
-    if (n >= a.N) return;
-    const int K = a.K, nst = K / BK;
-    ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
-    const int f = a.wfmt[n];
-    if (f < CHAM_W_NFMT && ((a.mask >> f) & 1u)) {
-        c.fmt = f;
-        c.zero = (float)a.wzero[n];
-        if (f == CHAM_W_NF4) {
-            const float* r = a.wnf4 + (int64_t)n * (K / 64);
-            float mx = 0.0f;
-            for (int b = lane; b < K / 64; b += 64) mx = fmaxf(mx, r[b]);
-            mx = wave_max(mx);
-            c.eref = floor_log2(floor_scale(mx));
-            c.colscale = ldexpf(1.0f, c.eref);
-        } else if (is_mx(f)) {
-            const uint8_t* r = a.we8 + (int64_t)n * (K / 32);
-            int mx = 0;
-            for (int b = lane; b < K / 32; b += 64) mx = max(mx, (int)r[b]);
-            for (int o = 32; o > 0; o >>= 1) mx = max(mx, __shfl_xor(mx, o, kWave));
-            c.eref = mx - 127 - mx_F(f);
-            c.colscale = ldexpf(1.0f, c.eref);
-        } else {
-            c.colscale = a.wscale[n];
-        }
+// Workgroup b handles 32 channels (block b % nblk) and the k-steps of chunk b / nblk.
+// 8 threads per channel compute its ColPrep (the reference exponent is the largest NF4
+// block absmax or MX block exponent of the whole channel); thread t builds the records of
+// channel t/2 % 32, half t % 2, at k-steps congruent to t/64 mod 4, so each wavefront
+// stores 64 consecutive records (coalesced).  The codes and block metadata of the
+// thread's first kRecPrefetch records are loaded before the ColPrep pass, so both
+// passes' loads are in flight together.
+constexpr int kRecChannels = 32;
+constexpr int kRecPrefetch = 4;
+
+CHAM_DEV Table record_table(const ColPrep& c, float nf4a, int e8) {
+    Table tb;
+    switch (c.fmt) {
+    case CHAM_W_NF4: tb = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(nf4a, -c.eref)); break;
+    case CHAM_W_MXFP4:
+    case CHAM_W_MXINT4:
+    case CHAM_W_MXINT8: {
+        const float factor = ldexpf(1.0f, e8 - 127 - mx_F(c.fmt) - c.eref);
+        if (c.fmt == CHAM_W_MXFP4) tb = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
+        else if (c.fmt == CHAM_W_MXINT4) tb = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
+        else tb = int8_record(0x80808080u, 128.0f, factor);
+        break;
     }
-    if (lane == 0 && part == 0) a.cols[n] = c;
+    case CHAM_W_FP4: tb = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
+    case CHAM_W_INT4_ASYM: tb = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
+    case CHAM_W_INT4_SYM: tb = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
+    case CHAM_W_INT8_SYM: tb = int8_record(0x80808080u, 128.0f, 1.0f); break;
+    case CHAM_W_INT8_ASYM: tb = int8_record(0u, c.zero, 1.0f); break;
+    default: tb = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
+    }
+    return tb;
+}
+
+__global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
+    __shared__ ColPrep cp[kRecChannels];
+    const int t = threadIdx.x;
+    const int K = a.K, nst = K / BK;
+    const int nblk = (a.N + kRecChannels - 1) / kRecChannels;
+    const int cb = (int)blockIdx.x % nblk, kc = (int)blockIdx.x / nblk;
+    const int n0 = cb * kRecChannels;
     const int cw = a.code_bits / 4;  // 16-byte code pieces per half k-step
     const int64_t cstride = (int64_t)K * a.code_bits / 8;
-    const int idx = 64 * part + lane;
-    if (idx < 2 * nst) {
-        const int k = idx >> 1, h = idx & 1;
-        Table t;
-        switch (c.fmt) {
-        case CHAM_W_NF4:
-            t = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(a.wnf4[(int64_t)n * (K / 64) + k], -c.eref));
-            break;
-        case CHAM_W_MXFP4:
-        case CHAM_W_MXINT4:
-        case CHAM_W_MXINT8: {
-            const int e = a.we8[(int64_t)n * (K / 32) + 2 * k + h];
-            const float factor = ldexpf(1.0f, e - 127 - mx_F(c.fmt) - c.eref);
-            if (c.fmt == CHAM_W_MXFP4) t = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
-            else if (c.fmt == CHAM_W_MXINT4) t = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
-            else t = int8_record(0x80808080u, 128.0f, factor);
-            break;
-        }
-        case CHAM_W_FP4: t = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
-        case CHAM_W_INT4_ASYM: t = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
-        case CHAM_W_INT4_SYM: t = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
-        case CHAM_W_INT8_SYM: t = int8_record(0x80808080u, 128.0f, 1.0f); break;
-        case CHAM_W_INT8_ASYM: t = int8_record(0u, c.zero, 1.0f); break;
-        default: t = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
-        }
+
+    // this thread's records: channel n, half h, k-steps kb, kb + 4, ... below ke
+    const int n = n0 + ((t & 63) >> 1), h = t & 1;
+    const bool live = n < a.N;
+    const int kb = kc * a.kchunk + (t >> 6), ke = min(nst, (kc + 1) * a.kchunk);
+    auto load_rec = [&](int k, uint4 (&code)[2], float& nfa, int& e8) __attribute__((always_inline)) {
         const uint4* src = reinterpret_cast<const uint4*>(a.wc + n * cstride + (int64_t)k * (16 * a.code_bits / 2) +
                                                           (int64_t)h * 16 * cw);
+        code[0] = src[0];
+        code[1] = cw > 1 ? src[1] : make_uint4(0u, 0u, 0u, 0u);
+        nfa = a.wnf4 ? a.wnf4[(int64_t)n * (K / 64) + k] : 0.0f;
+        e8 = a.we8 ? (int)a.we8[(int64_t)n * (K / 32) + 2 * k + h] : 0;
+    };
+    auto store_rec = [&](int k, const uint4 (&code)[2], const Table& tb) __attribute__((always_inline)) {
         uint4* dst = a.rec + (((int64_t)k * a.N + n) * 2 + h) * (cw + 2);
-        for (int q = 0; q < cw; ++q) dst[q] = src[q];
-        dst[cw] = make_uint4(t.lo[0], t.lo[1], t.lo[2], t.lo[3]);
-        dst[cw + 1] = make_uint4(t.hi[0], t.hi[1], t.hi[2], t.hi[3]);
+        dst[0] = code[0];
+        if (cw > 1) dst[1] = code[1];
+        dst[cw] = make_uint4(tb.lo[0], tb.lo[1], tb.lo[2], tb.lo[3]);
+        dst[cw + 1] = make_uint4(tb.hi[0], tb.hi[1], tb.hi[2], tb.hi[3]);
+    };
+    uint4 pc[kRecPrefetch][2];
+    float pn[kRecPrefetch];
+    int pe[kRecPrefetch];
+#pragma unroll
+    for (int i = 0; i < kRecPrefetch; ++i)
+        if (live && kb + 4 * i < ke) load_rec(kb + 4 * i, pc[i], pn[i], pe[i]);
+
+    {
+        const int ch = t >> 3, sub = t & 7;
+        const int nn = n0 + ch;
+        const int f = nn < a.N ? a.wfmt[nn] : CHAM_W_NFMT;
+        const bool ok = f < CHAM_W_NFMT && ((a.mask >> f) & 1u);
+        float mxf = 0.0f;
+        int mxe = 0;
+        if (ok && f == CHAM_W_NF4) {
+            const float* r = a.wnf4 + (int64_t)nn * (K / 64);
+            for (int b = sub; b < K / 64; b += 8) mxf = fmaxf(mxf, r[b]);
+        } else if (ok && is_mx(f)) {
+            const uint8_t* r = a.we8 + (int64_t)nn * (K / 32);
+            for (int b = sub; b < K / 32; b += 8) mxe = max(mxe, (int)r[b]);
+        }
+#pragma unroll
+        for (int o = 1; o < 8; o <<= 1) {
+            mxf = fmaxf(mxf, __shfl_xor(mxf, o, kWave));
+            mxe = max(mxe, __shfl_xor(mxe, o, kWave));
+        }
+        ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
+        if (ok) {
+            c.fmt = f;
+            c.zero = (float)a.wzero[nn];
+            if (f == CHAM_W_NF4) {
+                c.eref = floor_log2(floor_scale(mxf));
+                c.colscale = ldexpf(1.0f, c.eref);
+            } else if (is_mx(f)) {
+                c.eref = mxe - 127 - mx_F(f);
+                c.colscale = ldexpf(1.0f, c.eref);
+            } else {
+                c.colscale = a.wscale[nn];
+            }
+        }
+        if (sub == 0) {
+            cp[ch] = c;
+            if (kc == 0 && nn < a.N) a.cols[nn] = c;
+        }
+    }
+    __syncthreads();
+    if (!live) return;
+    const ColPrep c = cp[(t & 63) >> 1];
+#pragma unroll
+    for (int i = 0; i < kRecPrefetch; ++i)
+        if (kb + 4 * i < ke) store_rec(kb + 4 * i, pc[i], record_table(c, pn[i], pe[i]));
+    for (int k = kb + 4 * kRecPrefetch; k < ke; k += 4) {
+        uint4 code[2];
+        float nfa;
+        int e8;
+        load_rec(k, code, nfa, e8);
+        store_rec(k, code, record_table(c, nfa, e8));
     }
 }
 
@@ -833,10 +885,14 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
 
-    RecArgs ra{wq->fmt, wq->scale, wq->zero, wq->nf4_absmax, wq->e8m0, wq->codes, mask, N, K, code_bits,
-               cols, rec};
-    const int64_t nwaves = (int64_t)N * ((2 * (K / BK) + 63) / 64);
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)((nwaves + 3) / 4)), dim3(256), 0, s, ra);
+    // enough workgroups to fill the chip, at least 4 k-steps each
+    const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
+    const int nkc = std::max(1, std::min((512 + nblk - 1) / nblk, (nst + 3) / 4));
+    const int rchunk = (nst + nkc - 1) / nkc;
+    // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
+    RecArgs ra{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
+               mask, N, K, code_bits, rchunk, cols, rec};
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(nblk * ((nst + rchunk - 1) / rchunk))), dim3(256), 0, s, ra);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;

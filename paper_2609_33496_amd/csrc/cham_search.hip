@@ -313,18 +313,24 @@ CHAM_DEV double row_err64(const float (&v)[NCH][4], const bool (&valid)[NCH], co
 
 CHAM_DEV float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 
-template <uint32_t MASK, int NCH>
-__global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
-    __shared__ NF4Cell cells[33];
-    nf4_cells_init(cells);
-    __syncthreads();
+// Cross-wavefront sums when SPLIT wavefronts share a channel (SPLIT = 4: the whole
+// workgroup); partial values are combined in wavefront order, so the result is fixed.
+struct SplitLDS {
+    float lohi[4][2];
+    float e[4][CHAM_W_NFMT];
+    double ed[4][CHAM_W_NFMT];
+};
 
+// Search of channel n by SPLIT wavefronts; this wavefront holds part `part` of the row
+// (K / SPLIT consecutive elements, a multiple of 64).
+template <uint32_t MASK, int NCH, int SPLIT>
+CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, int part, SplitLDS* sl) {
     const int lane = threadIdx.x & 63;
-    const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (n >= a.N) return;  // wave-uniform
+    const int wv = threadIdx.x >> 6;
     const int K = a.K;
-    const int nq = K >> 2;  // float4 per row
-    const float* row = a.W + n * (int64_t)K;
+    const int KP = K / SPLIT;  // elements of this wavefront
+    const int nq = KP >> 2;    // float4 of this wavefront
+    const float* row = a.W + n * (int64_t)K + (int64_t)part * KP;
     const uint32_t mask = MASK ? MASK : a.mask;
 
     float v[NCH][4];
@@ -352,6 +358,12 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     }
     lo = wave_min_dpp(lo);
     hi = wave_max_dpp(hi);
+    if (SPLIT > 1) {
+        if (lane == 0) { sl->lohi[wv][0] = lo; sl->lohi[wv][1] = hi; }
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < SPLIT; ++w) { lo = fminf(lo, sl->lohi[w][0]); hi = fmaxf(hi, sl->lohi[w][1]); }
+    }
     const float amax = fmaxf(fabsf(lo), fabsf(hi));
 
     RowParams p;
@@ -383,12 +395,28 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
         if (mask & (1u << 7)) e[7] += chunk_err<7>(v[c], p, b32[c], b64[c], cells);
         if (mask & (1u << 8)) e[8] += chunk_err<8>(v[c], p, b32[c], b64[c], cells);
     }
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) {
+        if (!(mask & (1u << f))) continue;
+        e[f] = wave_sum_dpp(e[f]);
+        if (SPLIT > 1 && lane == 0) sl->e[wv][f] = e[f];
+    }
+    if (SPLIT > 1) {
+        __syncthreads();
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            if (!(mask & (1u << f))) continue;
+            float t = sl->e[0][f];
+#pragma unroll
+            for (int w = 1; w < SPLIT; ++w) t += sl->e[w][f];
+            e[f] = t;
+        }
+    }
     int best = -1, second = -1;
     float eb = 0.0f, es = 0.0f;
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) {
         if (!(mask & (1u << f))) continue;
-        e[f] = wave_sum_dpp(e[f]);
         if (best < 0 || e[f] < eb) {
             second = best; es = eb;
             best = f; eb = e[f];
@@ -416,6 +444,18 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
             case 7: ed[7] = row_err64<7, NCH>(v, valid, p, b32, b64, cells); break;
             default: ed[8] = row_err64<8, NCH>(v, valid, p, b32, b64, cells); break;
             }
+            if (SPLIT > 1 && lane == 0) sl->ed[wv][f] = ed[f];
+        }
+        if (SPLIT > 1) {  // the condition above is the same in every wavefront of the channel
+            __syncthreads();
+#pragma unroll
+            for (int f = 0; f < CHAM_W_NFMT; ++f) {
+                if (!(mask & (1u << f))) continue;
+                double t = sl->ed[0][f];
+#pragma unroll
+                for (int w = 1; w < SPLIT; ++w) t += sl->ed[w][f];
+                ed[f] = t;
+            }
         }
         best = -1;
         double bd = 0.0;
@@ -425,14 +465,14 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
             if (best < 0 || ed[f] < bd) { best = f; bd = ed[f]; }
         }
     }
-    if (a.err && lane == 0) {
+    if (a.err && lane == 0 && part == 0) {
 #pragma unroll
         for (int f = 0; f < CHAM_W_NFMT; ++f) a.err[n * CHAM_W_NFMT + f] = (mask & (1u << f)) ? ed[f] : -1.0;
     }
 
     // ---- emit the winner's codes and metadata
     const int f = best;
-    if (lane == 0) {
+    if (lane == 0 && part == 0) {
         a.fmt[n] = (uint8_t)f;
         float s = 0.0f;
         int32_t z = 0;
@@ -460,7 +500,7 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!valid[c]) continue;
-        const int q = c * 64 + lane;
+        const int q = c * 64 + lane + part * (KP >> 2);  // float4 index in the row
         const uint32_t cw = cws[c];
         if (a.code_bits == 4) {
             reinterpret_cast<uint16_t*>(a.codes + n * (int64_t)(K / 2))[q] = (uint16_t)cw;
@@ -477,138 +517,162 @@ __global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
     }
 }
 
-// Stable counting sort of channels by format.  Workgroup b owns a run of consecutive
-// channels; it counts every format over all channels (those before its run and the
-// total; the format bytes are small and cached), which gives the group offsets and its
-// starting position inside every group.  It then walks its run 256 channels at a time:
-// a channel's position adds the count of equal formats in earlier waves (wave totals in
-// LDS) and in earlier lanes (ballot prefix).
-constexpr int kGroupThreads = 256;
-constexpr int kGroupMaxBlocks = 256;
+// Stable counting sort of the channels by chosen format, in one workgroup of 1024
+// threads: thread t counts the formats of a run of consecutive channels (a multiple of 16,
+// read 16 bytes at a time), an exclusive scan over the threads (per format) gives each run
+// its start inside every group, and the thread then places its channels in order -- into
+// LDS when the permutation fits (then copied out with coalesced 16-byte stores), else
+// directly.
+constexpr int kGroupThreads = 1024;
+constexpr int kGroupRun = 16;
+constexpr int kGroupLdsChannels = 16000;  // with the static arrays, within 64 KB of LDS
 
-CHAM_DEV int group_run(int64_t N) {
-    int64_t run = (N + kGroupMaxBlocks - 1) / kGroupMaxBlocks;
-    run = (run + 1023) / 1024 * 1024;
-    return (int)run;
+// 16 format bytes from channel c on; bytes at or past N read as 0xFF (no format)
+CHAM_DEV uint4 fmt16(const uint8_t* fmt, int N, int c, bool aligned) {
+    if (aligned && c + 16 <= N) return *reinterpret_cast<const uint4*>(fmt + c);
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t v = 0u;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int r = c + 4 * i + b;
+            v |= (r < N ? (uint32_t)fmt[r] : 0xFFu) << (8 * b);
+        }
+        w[i] = v;
+    }
+    return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-__global__ __launch_bounds__(kGroupThreads) void group_kernel(const uint8_t* fmt, int64_t N, int32_t* perm,
-                                                                int32_t* group_off) {
-    __shared__ int32_t cnt[2][CHAM_W_NFMT];  // [0] before the run, [1] all channels
-    __shared__ int32_t wc[kGroupThreads / kWave][CHAM_W_NFMT];
+struct GroupArgs {
+    const uint8_t* fmt;
+    int N;
+    int32_t* perm;       // NULL = skip
+    int32_t* group_off;  // NULL = skip
+};
+
+__global__ __launch_bounds__(kGroupThreads) void group_kernel(GroupArgs a) {
+    extern __shared__ int32_t lperm[];  // [N] when N <= kGroupLdsChannels
+    constexpr int NW = kGroupThreads / kWave;
+    __shared__ int32_t wtot[NW][CHAM_W_NFMT];
+    __shared__ int32_t gbase[CHAM_W_NFMT];
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    const int64_t run = group_run(N);
-    const int64_t r0 = (int64_t)blockIdx.x * run, r1 = r0 + run < N ? r0 + run : N;
-    if (t < 2 * CHAM_W_NFMT) cnt[t / CHAM_W_NFMT][t % CHAM_W_NFMT] = 0;
-    // the formats of this thread's channels in the first four chunks of the run, loaded
-    // now so their latency overlaps the counting pass
-    int pre[4];
+    const int N = a.N;
+    const bool aligned = ((uintptr_t)a.fmt & 15u) == 0;
+    const int R = ((N + kGroupThreads - 1) / kGroupThreads + kGroupRun - 1) / kGroupRun * kGroupRun;
+    const int64_t c0l = (int64_t)t * R;
+    const int c0 = c0l < N ? (int)c0l : N, c1 = c0l + R < N ? (int)(c0l + R) : N;
+    int32_t cnt[CHAM_W_NFMT];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const int64_t r = r0 + (int64_t)c * kGroupThreads + t;
-        pre[c] = perm && r < r1 ? (int)fmt[r] : CHAM_W_NFMT;
-    }
-    __syncthreads();
-    {
-        int32_t before[CHAM_W_NFMT], all[CHAM_W_NFMT];
+    for (int f = 0; f < CHAM_W_NFMT; ++f) cnt[f] = 0;
+    // four 16-byte loads in flight, then their counts
+    for (int c = c0; c < c1; c += 64) {
+        uint4 q[4];
 #pragma unroll
-        for (int f = 0; f < CHAM_W_NFMT; ++f) before[f] = all[f] = 0;
-        auto count = [&](uint32_t w, int64_t r) {  // 4 format bytes of channels r .. r + 3
+        for (int i = 0; i < 4; ++i) q[i] = c + 16 * i < c1 ? fmt16(a.fmt, N, c + 16 * i, aligned) : make_uint4(~0u, ~0u, ~0u, ~0u);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int f = (w >> (8 * e)) & 255u;
-                const int b = r + e < r0;
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t w[4] = {q[i].x, q[i].y, q[i].z, q[i].w};
 #pragma unroll
-                for (int g = 0; g < CHAM_W_NFMT; ++g) {
-                    all[g] += f == g;
-                    before[g] += (f == g) & b;
-                }
-            }
-        };
-        int64_t done = 0;
-        if (((uintptr_t)fmt & 15u) == 0) {  // 16 channels per load
-            const uint4* f4 = reinterpret_cast<const uint4*>(fmt);
-            const int64_t nq = N >> 4;
-#pragma unroll 2
-            for (int64_t q = t; q < nq; q += kGroupThreads) {
-                const uint4 v = f4[q];
-                count(v.x, 16 * q); count(v.y, 16 * q + 4); count(v.z, 16 * q + 8); count(v.w, 16 * q + 12);
-            }
-            done = nq << 4;
-        }
-        // remaining channels one at a time (the other three bytes 0xFF match no format)
-        for (int64_t r = done + t; r < N; r += kGroupThreads) count(0xFFFFFF00u | fmt[r], r);
+            for (int j = 0; j < 16; ++j) {
+                const int f = (w[j >> 2] >> (8 * (j & 3))) & 255u;
 #pragma unroll
-        for (int f = 0; f < CHAM_W_NFMT; ++f) {
-            int32_t u = before[f], v = all[f];
-            for (int o = 32; o > 0; o >>= 1) {
-                u += __shfl_xor(u, o, kWave);
-                v += __shfl_xor(v, o, kWave);
-            }
-            if (lane == 0) {
-                if (u) atomicAdd(&cnt[0][f], u);
-                if (v) atomicAdd(&cnt[1][f], v);
+                for (int g = 0; g < CHAM_W_NFMT; ++g) cnt[g] += f == g;
             }
         }
     }
+    // exclusive scan over the threads, per format: within the wave, then across waves
+    int32_t pre[CHAM_W_NFMT];
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) {
+        int32_t v = cnt[f];
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int32_t u = __shfl_up(v, o, kWave);
+            if (lane >= o) v += u;
+        }
+        pre[f] = v - cnt[f];
+        if (lane == 63) wtot[wave][f] = v;
+    }
     __syncthreads();
-    int32_t base[CHAM_W_NFMT];
-    {
+    if (t < CHAM_W_NFMT) {  // exclusive scan of the wave totals per format, in place
         int32_t acc = 0;
+        for (int w = 0; w < NW; ++w) {
+            const int32_t v = wtot[w][t];
+            wtot[w][t] = acc;
+            acc += v;
+        }
+        gbase[t] = acc;  // format total for now
+    }
+    __syncthreads();
+    if (t == 0) {
+        int32_t o = 0;
 #pragma unroll
         for (int f = 0; f < CHAM_W_NFMT; ++f) {
-            base[f] = acc + cnt[0][f];
-            acc += cnt[1][f];
+            const int32_t tot = gbase[f];
+            gbase[f] = o;
+            if (a.group_off) a.group_off[f] = o;
+            o += tot;
         }
-        if (group_off && blockIdx.x == 0 && t == 0) {
-            int32_t o = 0;
+        if (a.group_off) a.group_off[CHAM_W_NFMT] = o;
+    }
+    __syncthreads();
+    if (!a.perm) return;
+    const bool staged = N <= kGroupLdsChannels;
+    int32_t* dst = staged ? lperm : a.perm;
 #pragma unroll
-            for (int f = 0; f < CHAM_W_NFMT; ++f) {
-                group_off[f] = o;
-                o += cnt[1][f];
+    for (int f = 0; f < CHAM_W_NFMT; ++f) pre[f] += gbase[f] + wtot[wave][f];
+    for (int c = c0; c < c1; c += 16) {
+        const uint4 q = fmt16(a.fmt, N, c, aligned);
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int f = (w[j >> 2] >> (8 * (j & 3))) & 255u;
+            int32_t pos = -1;
+#pragma unroll
+            for (int g = 0; g < CHAM_W_NFMT; ++g) {
+                if (f == g) pos = pre[g]++;
             }
-            group_off[CHAM_W_NFMT] = o;
+            if (pos >= 0) dst[pos] = c + j;
         }
     }
-    if (!perm) return;
-    const uint64_t lt = (1ull << lane) - 1ull;
-    for (int64_t c0 = r0, ci = 0; c0 < r1; c0 += kGroupThreads, ++ci) {
-        const int64_t r = c0 + t;
-        const int f = ci < 4 ? (ci == 0 ? pre[0] : ci == 1 ? pre[1] : ci == 2 ? pre[2] : pre[3])
-                             : (r < r1 ? (int)fmt[r] : CHAM_W_NFMT);
-        int rank = 0;
-#pragma unroll
-        for (int g = 0; g < CHAM_W_NFMT; ++g) {
-            const uint64_t m = __ballot(f == g);
-            if (lane == 0) wc[wave][g] = __popcll(m);
-            if (f == g) rank = __popcll(m & lt);
-        }
-        __syncthreads();
-        int32_t pos = 0;
-#pragma unroll
-        for (int g = 0; g < CHAM_W_NFMT; ++g) {
-            int32_t earlier = 0, chunk = 0;
-#pragma unroll
-            for (int w = 0; w < kGroupThreads / kWave; ++w) {
-                const int32_t v = wc[w][g];
-                earlier += w < wave ? v : 0;
-                chunk += v;
-            }
-            if (f == g) pos = base[g] + earlier + rank;
-            base[g] += chunk;
-        }
-        if (f < CHAM_W_NFMT) perm[pos] = (int32_t)r;
-        __syncthreads();
+    if (!staged) return;
+    __syncthreads();  // every channel has a format of the palette, so all N slots are set
+    if (((uintptr_t)a.perm & 15u) == 0) {
+        const int n4 = N >> 2;
+        for (int i = t; i < n4; i += kGroupThreads)
+            reinterpret_cast<int4*>(a.perm)[i] = reinterpret_cast<const int4*>(lperm)[i];
+        for (int i = (n4 << 2) + t; i < N; i += kGroupThreads) a.perm[i] = lperm[i];
+    } else {
+        for (int i = t; i < N; i += kGroupThreads) a.perm[i] = lperm[i];
     }
 }
 
-template <int NCH>
-void launch_search(const SearchArgs& a, hipStream_t s) {
-    dim3 grid((unsigned)((a.N + 3) / 4));
-    if (a.mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH>), grid, dim3(256), 0, s, a);
-    else if (a.mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((search_kernel<0u, NCH>), grid, dim3(256), 0, s, a);
+// SPLIT = 1: four channels per workgroup, one per wavefront.  SPLIT = 4: one channel per
+// workgroup, a quarter of the row per wavefront (more wavefronts in flight when the
+// layer has few channels).
+template <uint32_t MASK, int NCH, int SPLIT>
+__global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
+    __shared__ NF4Cell cells[33];
+    __shared__ SplitLDS sl;
+    nf4_cells_init(cells);
+    __syncthreads();
+    const int wv = threadIdx.x >> 6;
+    const int64_t n = SPLIT == 1 ? (int64_t)blockIdx.x * 4 + wv : (int64_t)blockIdx.x;
+    if (n < a.N) search_row<MASK, NCH, SPLIT>(a, cells, n, SPLIT == 1 ? 0 : wv, &sl);  // workgroup-uniform for SPLIT 4
 }
+
+template <int NCH, int SPLIT>
+void launch_search(const SearchArgs& a, hipStream_t s) {
+    const dim3 grid((unsigned)(SPLIT == 1 ? (a.N + 3) / 4 : a.N));
+    if (a.mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH, SPLIT>), grid, dim3(256), 0, s, a);
+    else if (a.mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH, SPLIT>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((search_kernel<0u, NCH, SPLIT>), grid, dim3(256), 0, s, a);
+}
+
+// Layers with few channels and long rows split each row over the four wavefronts of a
+// workgroup, so at least ~4 wavefronts per SIMD are in flight.
+constexpr int64_t kSplitBelowChannels = 4096;
 
 }  // namespace
 }  // namespace cham
@@ -623,7 +687,7 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     if (!W || !wq) return CHAM_EINVAL;
     const uint32_t mask = wq->palette_mask;
     if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
-    if (wq->N < 1 || wq->K < 1 || wq->N > (int64_t)INT32_MAX) return CHAM_EINVAL;
+    if (wq->N < 1 || wq->K < 1 || wq->N > (int64_t)INT32_MAX - 4096) return CHAM_EINVAL;
     const int64_t K = wq->K;
     if (K % 32 != 0) return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
@@ -649,17 +713,28 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     a.e8 = mx ? wq->e8m0 : nullptr;
     a.err = wq->err;
     hipStream_t s = (hipStream_t)stream;
-    const int nch = (int)((K + 255) / 256);
-    if (nch <= 3) launch_search<3>(a, s);
-    else if (nch <= 5) launch_search<5>(a, s);
-    else if (nch <= 10) launch_search<10>(a, s);
-    else if (nch <= 20) launch_search<20>(a, s);
-    else launch_search<32>(a, s);
+    // split when the quarter rows fill their 256-element chunks to at least 85 %
+    const int64_t qc = K / 4;  // elements per wavefront when split
+    const bool fill = K % 256 == 0 && qc * 100 >= 85 * ((qc + 255) / 256 * 256);
+    const int split = (fill && K >= 1024 && wq->N < kSplitBelowChannels) ? 4 : 1;
+    const int nch = (int)((K / split + 255) / 256);
+    if (split == 4) {
+        if (nch <= 2) launch_search<2, 4>(a, s);
+        else if (nch <= 3) launch_search<3, 4>(a, s);
+        else if (nch <= 5) launch_search<5, 4>(a, s);
+        else launch_search<8, 4>(a, s);
+    } else {
+        if (nch <= 3) launch_search<3, 1>(a, s);
+        else if (nch <= 5) launch_search<5, 1>(a, s);
+        else if (nch <= 10) launch_search<10, 1>(a, s);
+        else if (nch <= 20) launch_search<20, 1>(a, s);
+        else launch_search<32, 1>(a, s);
+    }
     CHAM_CHECK_LAUNCH();
     if (wq->perm || wq->group_off) {
-        const int64_t run = (((wq->N + kGroupMaxBlocks - 1) / kGroupMaxBlocks) + 1023) / 1024 * 1024;
-        hipLaunchKernelGGL(group_kernel, dim3((unsigned)((wq->N + run - 1) / run)), dim3(kGroupThreads), 0, s, wq->fmt,
-                           wq->N, wq->perm, wq->group_off);
+        const size_t lds = wq->perm && wq->N <= kGroupLdsChannels ? (size_t)wq->N * 4 : 0;
+        hipLaunchKernelGGL(group_kernel, dim3(1), dim3(kGroupThreads), lds, s,
+                           GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off});
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;

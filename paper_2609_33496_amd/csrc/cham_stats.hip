@@ -49,7 +49,15 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
         const float4 t0 = X4[i], t1 = X4[i + stride], t2 = X4[i + 2 * stride], t3 = X4[i + 3 * stride];
         add(t0); add(t1); add(t2); add(t3);
     }
-    for (; i < nq; i += stride) add(X4[i]);
+    // the last up to three: all loads issued first, then the sums in index order
+    {
+        const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+        const bool v0 = i < nq, v1 = i + stride < nq, v2 = i + 2 * stride < nq;
+        const float4 t0 = v0 ? X4[i] : z, t1 = v1 ? X4[i + stride] : z, t2 = v2 ? X4[i + 2 * stride] : z;
+        if (v0) add(t0);
+        if (v1) add(t1);
+        if (v2) add(t2);
+    }
     // scalar tail (numel % 4), handled by the first threads of workgroup 0
     if (blockIdx.x == 0 && threadIdx.x < (numel & 3)) {
         float x = X[(nq << 2) + threadIdx.x];

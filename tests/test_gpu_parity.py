@@ -76,8 +76,8 @@ def test_search_hetero_rows(mask, N, K):
     _assert_search_equal(wq, ref)
 
 
-def test_search_known_winners_and_degenerate_rows():
-    K = 256
+@pytest.mark.parametrize("K", [256, 1024])  # 1024: each row split over four wavefronts
+def test_search_known_winners_and_degenerate_rows(K):
     g = np.random.default_rng(0)
     rows = []
     v = oracle.nf4_table()
@@ -127,6 +127,32 @@ def test_search_full_size_sampled():
         assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable"))
         counts = np.bincount(f, minlength=9)
         assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(counts)]))
+
+
+def test_search_grouping_repeated_and_partial_outputs():
+    """Repeated calls on one output object, a different matrix in between, and calls that
+    request only perm or only group_off all give the stable sort of the formats."""
+    Wa, _ = synth.hetero_weights(21, 3000, 640)   # 750 workgroups, ragged last one
+    Wb, _ = synth.hetero_weights(22, 3000, 640)
+    wq = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV)
+    for it, W in enumerate((Wa, Wb, Wa)):
+        case(f"select_weight_formats grouping call {it} N=3000 K=640")
+        cham.select_weight_formats(torch.from_numpy(W).to(DEV), oracle.MASK_W4, out=wq)
+        torch.cuda.synchronize()
+        f = _np(wq.fmt)
+        assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable"))
+        assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(np.bincount(f, minlength=9))]))
+    for keep in ("perm", "group_off"):
+        case(f"select_weight_formats grouping with only {keep}")
+        w2 = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV)
+        setattr(w2, "group_off" if keep == "perm" else "perm", None)
+        cham.select_weight_formats(torch.from_numpy(Wa).to(DEV), oracle.MASK_W4, out=w2)
+        torch.cuda.synchronize()
+        f = _np(w2.fmt)
+        if keep == "perm":
+            assert np.array_equal(_np(w2.perm), np.argsort(f, kind="stable"))
+        else:
+            assert np.array_equal(_np(w2.group_off), np.concatenate([[0], np.cumsum(np.bincount(f, minlength=9))]))
 
 
 # ---------------------------------------------------------------------------------------
