@@ -7,7 +7,7 @@ activations are A8 in the format a lookup table built for B = 4 timestep buckets
 kurtosis and SNR (scaled-linear schedule 0.00085 -> 0.012, T = 1000) assigns.
 
 One step = one pass of every step of the path over one batch, all inputs resident in HBM:
-  select_weight_formats (4 layers) -> act_stats_accumulate (4 layer inputs) ->
+  select_weight_formats_batch (the 4 layers, one call) -> act_stats_accumulate (4 layer inputs) ->
   build_act_lut -> quantize_act_lut (4) -> mixed_linear (4).
 
 Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step time (GEMM
@@ -134,6 +134,7 @@ def main():
     ws_lin = [torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=dev)
               for (_, K, N) in layers]
     wq_s = [w.struct() for w in wqs]
+    sbatch = cham.SearchBatch(Ws, wqs)  # the block's four layers searched in one call
     st_s = stats.struct()
     sc_s = sched.struct()
     lut_s = lut.struct()
@@ -148,9 +149,8 @@ def main():
         if record:
             e0 = torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-        for li in range(len(layers)):
-            rc = L.cham_select_weight_formats(P(Ws[li]), ctypes.byref(wq_s[li]), S)
-            assert rc == 0, rc
+        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, len(layers), S)
+        assert rc == 0, rc
         if record:
             e1 = torch.cuda.Event(enable_timing=True)
             e1.record(stream)

@@ -129,6 +129,14 @@ typedef struct cham_wq {
  * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K), CHAM_EHIP. */
 int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream);
 
+/* The same search for nlayers independent weight matrices (Sec. 4.5 applies per layer):
+ * W is a host array of nlayers device pointers, wq a host array of nlayers descriptors,
+ * each with its own buffers.  Results are those of nlayers separate calls; layers that
+ * share a kernel variant share launches (fewer, fuller launches for a model's layers).
+ * Every layer is checked before anything is launched; the first error is returned.
+ * Errors: as cham_select_weight_formats, CHAM_EINVAL also for NULL arrays or nlayers < 1. */
+int cham_select_weight_formats_batch(const float* const* W, cham_wq* wq, int32_t nlayers, void* stream);
+
 /* ---------------------------------------------------------------------------------------
  * 2. calibration statistics (Sec. 4.4; Alg. 1) and the LUT (Sec. 4.3; Alg. 1)
  * ------------------------------------------------------------------------------------- */

@@ -79,6 +79,7 @@ def lib():
     L.cham_status_string.restype = ctypes.c_char_p
     L.cham_version.restype = ctypes.c_int
     L.cham_select_weight_formats.argtypes = [_P, ctypes.POINTER(_WQ), _P]
+    L.cham_select_weight_formats_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(_WQ), i32, _P]
     L.cham_act_stats_reset.argtypes = [ctypes.POINTER(_Stats), _P]
     L.cham_act_stats_accumulate.argtypes = [_P, i64, i32, i32, ctypes.POINTER(_Stats), _P, sz, _P]
     L.cham_schedule_default.argtypes = [ctypes.POINTER(_Sched)]
@@ -93,7 +94,7 @@ def lib():
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
     L.cham_workspace_bytes.restype = sz
-    for name in ("cham_select_weight_formats", "cham_act_stats_reset", "cham_act_stats_accumulate",
+    for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -201,6 +202,34 @@ def select_weight_formats(W: torch.Tensor, mask: int = MASK_W4, out: Optional[WQ
     _check(lib().cham_select_weight_formats(_ptr(W), ctypes.byref(st), _stream(stream)), "select_weight_formats")
     out.code_bits = st.code_bits
     return out
+
+
+class SearchBatch:
+    """Prepared C arguments of a batched search over several layers (host arrays of the
+    weight pointers and descriptors), reusable across calls."""
+
+    def __init__(self, Ws, outs):
+        assert len(Ws) == len(outs) and len(Ws) > 0
+        for W in Ws:
+            _dev_tensor(W, torch.float32, "W")
+        self.Ws, self.outs = list(Ws), list(outs)
+        self.ptrs = (_P * len(Ws))(*[W.data_ptr() for W in Ws])
+        self.structs = (_WQ * len(outs))(*[o.struct() for o in outs])
+
+    def run(self, stream=None):
+        _check(lib().cham_select_weight_formats_batch(self.ptrs, self.structs, len(self.Ws), _stream(stream)),
+               "select_weight_formats_batch")
+        for o, st in zip(self.outs, self.structs):
+            o.code_bits = st.code_bits
+
+
+def select_weight_formats_batch(Ws, mask: int = MASK_W4, outs=None, want_perm=True, want_err=False,
+                                stream=None):
+    """Format search of several layers' weights (each [N_i, K_i] fp32, device) in one call."""
+    if outs is None:
+        outs = [alloc_wq(W.shape[0], W.shape[1], mask, W.device, want_perm, want_err) for W in Ws]
+    SearchBatch(Ws, outs).run(stream)
+    return outs
 
 
 # -------------------------------------------------------------------------------------------

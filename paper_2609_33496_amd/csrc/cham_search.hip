@@ -13,6 +13,9 @@
 // summation error -- the errors of every enabled format are recomputed with binary64 sums,
 // so the choice is always the binary64 argmin.  The winner's codes and metadata are then
 // written packed.  Nothing is re-read from HBM.
+#include <algorithm>
+#include <vector>
+
 #include "cham_device.h"
 
 namespace cham {
@@ -551,7 +554,16 @@ struct GroupArgs {
     int32_t* group_off;  // NULL = skip
 };
 
-__global__ __launch_bounds__(kGroupThreads) void group_kernel(GroupArgs a) {
+// layers per launch of a batched call (the descriptors travel in the kernel arguments)
+constexpr int kBatchMax = 16;
+struct GroupBatch {
+    int nl;
+    GroupArgs g[kBatchMax];
+};
+
+// workgroup i groups layer i of the batch
+__global__ __launch_bounds__(kGroupThreads) void group_kernel(GroupBatch B) {
+    const GroupArgs& a = B.g[blockIdx.x];
     extern __shared__ int32_t lperm[];  // [N] when N <= kGroupLdsChannels
     constexpr int NW = kGroupThreads / kWave;
     __shared__ int32_t wtot[NW][CHAM_W_NFMT];
@@ -648,31 +660,82 @@ __global__ __launch_bounds__(kGroupThreads) void group_kernel(GroupArgs a) {
     }
 }
 
+struct SearchBatch {
+    int nl;
+    int64_t wg_end[kBatchMax];  // workgroups of layers 0..i
+    SearchArgs l[kBatchMax];
+};
+
 // SPLIT = 1: four channels per workgroup, one per wavefront.  SPLIT = 4: one channel per
 // workgroup, a quarter of the row per wavefront (more wavefronts in flight when the
-// layer has few channels).
+// layer has few channels).  The workgroups of the batch's layers follow each other.
 template <uint32_t MASK, int NCH, int SPLIT>
-__global__ __launch_bounds__(256) void search_kernel(SearchArgs a) {
+__global__ __launch_bounds__(256) void search_kernel(SearchBatch B) {
     __shared__ NF4Cell cells[33];
     __shared__ SplitLDS sl;
     nf4_cells_init(cells);
     __syncthreads();
+    const int64_t b = blockIdx.x;
+    int i = 0;
+    while (i + 1 < B.nl && b >= B.wg_end[i]) ++i;
+    const SearchArgs& a = B.l[i];
+    const int64_t lb = b - (i ? B.wg_end[i - 1] : 0);
     const int wv = threadIdx.x >> 6;
-    const int64_t n = SPLIT == 1 ? (int64_t)blockIdx.x * 4 + wv : (int64_t)blockIdx.x;
+    const int64_t n = SPLIT == 1 ? lb * 4 + wv : lb;
     if (n < a.N) search_row<MASK, NCH, SPLIT>(a, cells, n, SPLIT == 1 ? 0 : wv, &sl);  // workgroup-uniform for SPLIT 4
 }
 
 template <int NCH, int SPLIT>
-void launch_search(const SearchArgs& a, hipStream_t s) {
-    const dim3 grid((unsigned)(SPLIT == 1 ? (a.N + 3) / 4 : a.N));
-    if (a.mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH, SPLIT>), grid, dim3(256), 0, s, a);
-    else if (a.mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH, SPLIT>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((search_kernel<0u, NCH, SPLIT>), grid, dim3(256), 0, s, a);
+void launch_search(const SearchBatch& B, uint32_t mask, hipStream_t s) {
+    const dim3 grid((unsigned)B.wg_end[B.nl - 1]);
+    if (mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH, SPLIT>), grid, dim3(256), 0, s, B);
+    else if (mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH, SPLIT>), grid, dim3(256), 0, s, B);
+    else hipLaunchKernelGGL((search_kernel<0u, NCH, SPLIT>), grid, dim3(256), 0, s, B);
 }
 
 // Layers with few channels and long rows split each row over the four wavefronts of a
 // workgroup, so at least ~4 wavefronts per SIMD are in flight.
 constexpr int64_t kSplitBelowChannels = 4096;
+
+// Kernel variant of a layer: rows split over 4 wavefronts or not, and the register
+// chunks (256 elements) per wavefront, rounded up to an instantiated count.
+struct Variant {
+    int split, nch;
+};
+Variant variant_of(int64_t N, int64_t K) {
+    // split when the quarter rows fill their 256-element chunks to at least 85 %
+    const int64_t qc = K / 4;
+    const bool fill = K % 256 == 0 && qc * 100 >= 85 * ((qc + 255) / 256 * 256);
+    const int split = (fill && K >= 1024 && N < kSplitBelowChannels) ? 4 : 1;
+    const int nch = (int)((K / split + 255) / 256);
+    static const int c4[] = {2, 3, 5, 8}, c1[] = {3, 5, 10, 20, 32};
+    int r = 0;
+    if (split == 4) {
+        for (int c : c4) if (nch <= c) { r = c; break; }
+    } else {
+        for (int c : c1) if (nch <= c) { r = c; break; }
+    }
+    return Variant{split, r};
+}
+
+void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipStream_t s) {
+    if (v.split == 4) {
+        switch (v.nch) {
+        case 2: launch_search<2, 4>(B, mask, s); break;
+        case 3: launch_search<3, 4>(B, mask, s); break;
+        case 5: launch_search<5, 4>(B, mask, s); break;
+        default: launch_search<8, 4>(B, mask, s); break;
+        }
+    } else {
+        switch (v.nch) {
+        case 3: launch_search<3, 1>(B, mask, s); break;
+        case 5: launch_search<5, 1>(B, mask, s); break;
+        case 10: launch_search<10, 1>(B, mask, s); break;
+        case 20: launch_search<20, 1>(B, mask, s); break;
+        default: launch_search<32, 1>(B, mask, s); break;
+        }
+    }
+}
 
 }  // namespace
 }  // namespace cham
@@ -683,7 +746,8 @@ static int mask_code_bits(uint32_t mask) {
     return (mask & 0x7u) ? 8 : 4;  // formats 0..2 are the 8-bit ones
 }
 
-extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream) {
+// Checks one layer's arguments and fills its search descriptor.
+static int prepare_layer(const float* W, cham_wq* wq, SearchArgs& a) {
     if (!W || !wq) return CHAM_EINVAL;
     const uint32_t mask = wq->palette_mask;
     if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
@@ -697,14 +761,11 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     if ((nf4 && !wq->nf4_absmax) || (mx && !wq->e8m0)) return CHAM_EINVAL;
     if (((uintptr_t)W & 15u) || ((uintptr_t)wq->codes & 3u)) return CHAM_EINVAL;
     if (K > 32 * 256) return CHAM_ESHAPE;  // rows up to 8192 are held in registers
-    wq->code_bits = mask_code_bits(mask);
-
-    SearchArgs a;
     a.W = W;
     a.N = wq->N;
     a.K = (int)K;
     a.mask = mask;
-    a.code_bits = wq->code_bits;
+    a.code_bits = mask_code_bits(mask);
     a.fmt = wq->fmt;
     a.codes = wq->codes;
     a.scale = wq->scale;
@@ -712,30 +773,62 @@ extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* str
     a.nf4a = nf4 ? wq->nf4_absmax : nullptr;  // block metadata is written only when its format is enabled
     a.e8 = mx ? wq->e8m0 : nullptr;
     a.err = wq->err;
-    hipStream_t s = (hipStream_t)stream;
-    // split when the quarter rows fill their 256-element chunks to at least 85 %
-    const int64_t qc = K / 4;  // elements per wavefront when split
-    const bool fill = K % 256 == 0 && qc * 100 >= 85 * ((qc + 255) / 256 * 256);
-    const int split = (fill && K >= 1024 && wq->N < kSplitBelowChannels) ? 4 : 1;
-    const int nch = (int)((K / split + 255) / 256);
-    if (split == 4) {
-        if (nch <= 2) launch_search<2, 4>(a, s);
-        else if (nch <= 3) launch_search<3, 4>(a, s);
-        else if (nch <= 5) launch_search<5, 4>(a, s);
-        else launch_search<8, 4>(a, s);
-    } else {
-        if (nch <= 3) launch_search<3, 1>(a, s);
-        else if (nch <= 5) launch_search<5, 1>(a, s);
-        else if (nch <= 10) launch_search<10, 1>(a, s);
-        else if (nch <= 20) launch_search<20, 1>(a, s);
-        else launch_search<32, 1>(a, s);
+    return CHAM_OK;
+}
+
+extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* wq, int32_t nlayers, void* stream) {
+    if (!W || !wq || nlayers < 1) return CHAM_EINVAL;
+    std::vector<SearchArgs> args((size_t)nlayers);
+    for (int i = 0; i < nlayers; ++i) {
+        const int rc = prepare_layer(W[i], &wq[i], args[i]);
+        if (rc != CHAM_OK) return rc;
     }
-    CHAM_CHECK_LAUNCH();
-    if (wq->perm || wq->group_off) {
-        const size_t lds = wq->perm && wq->N <= kGroupLdsChannels ? (size_t)wq->N * 4 : 0;
-        hipLaunchKernelGGL(group_kernel, dim3(1), dim3(kGroupThreads), lds, s,
-                           GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off});
+    hipStream_t s = (hipStream_t)stream;
+    // one launch per kernel variant (and palette), up to kBatchMax layers each
+    std::vector<bool> done((size_t)nlayers, false);
+    for (int i = 0; i < nlayers; ++i) {
+        if (done[i]) continue;
+        const Variant v = variant_of(args[i].N, args[i].K);
+        const uint32_t key = args[i].mask == CHAM_MASK_W4 || args[i].mask == CHAM_MASK_W8 ? args[i].mask : 0u;
+        SearchBatch B;
+        B.nl = 0;
+        int64_t wgs = 0;
+        for (int j = i; j < nlayers; ++j) {
+            if (done[j]) continue;
+            const Variant vj = variant_of(args[j].N, args[j].K);
+            const uint32_t kj = args[j].mask == CHAM_MASK_W4 || args[j].mask == CHAM_MASK_W8 ? args[j].mask : 0u;
+            if (vj.split != v.split || vj.nch != v.nch || kj != key) continue;
+            wgs += v.split == 1 ? (args[j].N + 3) / 4 : args[j].N;
+            B.l[B.nl] = args[j];
+            B.wg_end[B.nl] = wgs;
+            ++B.nl;
+            done[j] = true;
+            if (B.nl == kBatchMax) break;
+        }
+        // a mixed palette (key 0) reads each layer's mask at run time
+        launch_variant(v, B, key ? key : 0u, s);
         CHAM_CHECK_LAUNCH();
     }
+    for (int i = 0; i < nlayers; ++i) wq[i].code_bits = args[i].code_bits;
+    // grouping: one workgroup per layer that asks for it
+    GroupBatch G;
+    G.nl = 0;
+    size_t lds = 0;
+    for (int i = 0; i <= nlayers; ++i) {
+        if (i < nlayers && (wq[i].perm || wq[i].group_off)) {
+            G.g[G.nl++] = GroupArgs{wq[i].fmt, (int)wq[i].N, wq[i].perm, wq[i].group_off};
+            if (wq[i].perm && wq[i].N <= kGroupLdsChannels) lds = std::max(lds, (size_t)wq[i].N * 4);
+        }
+        if (G.nl > 0 && (G.nl == kBatchMax || i == nlayers)) {
+            hipLaunchKernelGGL(group_kernel, dim3((unsigned)G.nl), dim3(kGroupThreads), lds, s, G);
+            CHAM_CHECK_LAUNCH();
+            G.nl = 0;
+            lds = 0;
+        }
+    }
     return CHAM_OK;
+}
+
+extern "C" int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream) {
+    return cham_select_weight_formats_batch(&W, wq, 1, stream);
 }

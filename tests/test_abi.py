@@ -67,6 +67,18 @@ def test_select_weight_formats_argument_errors(kw, status):
     assert rc == status
 
 
+def test_select_weight_formats_batch_argument_errors():
+    L = cham.lib()
+    good, bad = _wq(), _wq(K=48)
+    arr = (cham._WQ * 2)(good, bad)
+    ptrs = (ctypes.c_void_p * 2)(16, 16)
+    assert L.cham_select_weight_formats_batch(ptrs, arr, 2, None) == cham.ESHAPE  # checked before any launch
+    assert L.cham_select_weight_formats_batch(ptrs, arr, 0, None) == cham.EINVAL
+    assert L.cham_select_weight_formats_batch(None, arr, 1, None) == cham.EINVAL
+    nullw = (ctypes.c_void_p * 1)(None)
+    assert L.cham_select_weight_formats_batch(nullw, (cham._WQ * 1)(good), 1, None) == cham.EINVAL
+
+
 def test_other_argument_errors():
     L = cham.lib()
     st = cham._Stats(2, 3, ctypes.c_void_p(16), ctypes.c_void_p(16))

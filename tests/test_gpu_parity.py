@@ -129,6 +129,32 @@ def test_search_full_size_sampled():
         assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(counts)]))
 
 
+def test_search_batch_matches_single_calls():
+    """The batched search over 19 layers of mixed shapes, kernel variants and palettes (more
+    layers than one launch takes) equals one call per layer, bit for bit."""
+    shapes = [(37, 640), (300, 1280), (20, 1152), (24, 4608), (9, 5120), (5, 8192), (3, 64), (4100, 256),
+              (1280, 1280), (64, 5120), (7, 2048)] * 2
+    masks = [oracle.MASK_W4, oracle.MASK_W8, 0x1FF, (1 << oracle.W_INT4_SYM) | (1 << oracle.W_FP4)]
+    Ws, outs, singles = [], [], []
+    for i, (N, K) in enumerate(shapes[:19]):
+        m = masks[i % len(masks)]
+        W, _ = synth.hetero_weights(500 + i, N, K)
+        Wd = torch.from_numpy(W).to(DEV)
+        Ws.append(Wd)
+        outs.append(cham.alloc_wq(N, K, m, DEV, want_perm=(i % 3 != 2), want_err=(i % 5 == 0)))
+        singles.append(cham.select_weight_formats(Wd, m, want_perm=(i % 3 != 2), want_err=(i % 5 == 0)))
+    case("select_weight_formats_batch 19 layers")
+    cham.select_weight_formats_batch(Ws, outs=outs)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(outs, singles)):
+        assert a.code_bits == b.code_bits, i
+        for name in ("fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err"):
+            x, y = getattr(a, name), getattr(b, name)
+            assert (x is None) == (y is None), (i, name)
+            if x is not None:
+                assert torch.equal(x, y), (i, name)
+
+
 def test_search_grouping_repeated_and_partial_outputs():
     """Repeated calls on one output object, a different matrix in between, and calls that
     request only perm or only group_off all give the stable sort of the formats."""
