@@ -226,7 +226,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4),
                      "traffic": committed_traffic(),
-                     "kernel": "mixed_linear (record pre-pass + gemm_kernel); achieved = 2MNK summed over the "
+                     "kernel": "mixed_linear (record pre-pass, gemm_kernel, k-split reduce_kernel); achieved = 2MNK summed over the "
                                "4 calls / their HIP-event time; traffic = HBM bytes per call"},
     }
     if not args.no_cpu_baseline:
