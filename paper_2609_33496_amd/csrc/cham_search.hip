@@ -265,6 +265,26 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
     return e;
 }
 
+// NF4 error of one chunk, and the chunk's NF4 codes packed as the emitted layout has them
+// (4 bits per code, or one byte per code with 8-bit codes): the error pass already finds
+// each code, so a channel that chooses NF4 needs no second quantization pass.
+CHAM_DEV float chunk_err_nf4(const float (&w)[4], float blk64, const NF4Cell* cells, int code_bits, uint32_t& cw) {
+    const float a = floor_scale(blk64);
+    const float r = 1.0f / a;
+    float e = 0.0f;
+    cw = 0u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float y = w[j] * r;
+        const NF4Cell cl = nf4_cell(cells, y);
+        const bool up = y > cl.thr;
+        const float d = w[j] - (up ? cl.vhi : cl.vlo) * a;
+        e = __builtin_fmaf(d, d, e);
+        cw |= (cl.cnt + (up ? 1u : 0u)) << (code_bits == 4 ? 4 * j : 8 * j);
+    }
+    return e;
+}
+
 template <int F, int NCH>
 CHAM_DEV void row_codes(const float (&v)[NCH][4], const RowParams& p, const float (&b32)[NCH],
                         const float (&b64)[NCH], const NF4Cell* cells, int code_bits, uint32_t (&cws)[NCH]) {
@@ -383,6 +403,9 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 
     // ---- binary32 error sums of every enabled format, one fused pass
     float e[CHAM_W_NFMT];
+    uint32_t nf4cw[NCH];  // NF4 codes of each chunk, kept from the error pass
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) nf4cw[c] = 0u;
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) e[f] = 0.0f;
 #pragma unroll
@@ -393,7 +416,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
         if (mask & (1u << 2)) e[2] += chunk_err<2>(v[c], p, b32[c], b64[c], cells);
         if (mask & (1u << 3)) e[3] += chunk_err<3>(v[c], p, b32[c], b64[c], cells);
         if (mask & (1u << 4)) e[4] += chunk_err<4>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 5)) e[5] += chunk_err<5>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 5)) e[5] += chunk_err_nf4(v[c], b64[c], cells, a.code_bits, nf4cw[c]);
         if (mask & (1u << 6)) e[6] += chunk_err<6>(v[c], p, b32[c], b64[c], cells);
         if (mask & (1u << 7)) e[7] += chunk_err<7>(v[c], p, b32[c], b64[c], cells);
         if (mask & (1u << 8)) e[8] += chunk_err<8>(v[c], p, b32[c], b64[c], cells);
@@ -495,7 +518,10 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     case 2: row_codes<2, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
     case 3: row_codes<3, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
     case 4: row_codes<4, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
-    case 5: row_codes<5, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
+    case 5:
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) cws[c] = nf4cw[c];
+        break;
     case 6: row_codes<6, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
     case 7: row_codes<7, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
     default: row_codes<8, NCH>(v, p, b32, b64, cells, a.code_bits, cws); break;
