@@ -416,3 +416,37 @@ def test_linear_full_size_sampled():
             yr, bm = oracle.linear_pairs(xh, Wh, mm, nn)
             err = np.abs(Y[mm, nn] - yr)
             assert np.all(err <= 1e-3 * bm), (name, afmt, (err / bm).max())
+
+
+@pytest.mark.parametrize("M,N,K,mask,afmt", [
+    (1500, 3000, 2560, oracle.MASK_W4, cham.A_FP8_E5M2),   # 128-row tiles, 3 k-splits, ragged M
+    (1500, 3000, 2560, oracle.MASK_W8, cham.A_INT8_ASYM),  # 8-bit codes, 128-row tiles
+    (3000, 4000, 1280, oracle.MASK_W8, cham.A_MXFP8),      # 8-bit codes, 256-row tiles, MX activations
+    (3000, 4000, 1280, oracle.MASK_W4, cham.A_MXINT8),     # 128-row tiles, MX activations
+    (2048, 10240, 1280, oracle.MASK_W8, cham.A_FP8_E4M3),  # two launches: 256-row then 128-row tiles
+])
+def test_linear_plans_sampled(M, N, K, mask, afmt):
+    """Tile heights, k-splits and two-launch plans the sizes above select (each code width,
+    per-tensor and MX activations): sampled outputs against the oracle one by one."""
+    X = synth.diffusion_acts(5, 2, 600, M, K)
+    W, _ = synth.hetero_weights(31, N, K)
+    case(f"mixed_linear plan M={M} N={N} K={K} mask={mask:#x} afmt={afmt}")
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask)
+    xq = cham.quantize_act(torch.from_numpy(X).to(DEV), afmt, dynamic=True)
+    Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+    g = np.random.default_rng(M + N + K + afmt)
+    mm = np.concatenate([g.integers(0, M, 1500), [M - 1, 0]])
+    nn = np.concatenate([g.integers(0, N, 1500), [N - 1, 0]])
+    rows = np.unique(nn)
+    ref = oracle.select_weight_formats(W[rows], mask, want_err=False, want_perm=False)
+    assert np.array_equal(_np(wq.fmt)[rows], ref["fmt"])
+    Wh = np.zeros((N, K), np.float32)
+    Wh[rows] = oracle.dequant_weights(ref, K)
+    mrows = np.unique(mm)
+    lo, hi = oracle.minmax(X)  # the whole tensor's range (MX formats: s = 1, z = 0)
+    s, z = oracle.scale_zp(afmt, lo, hi)
+    xh = np.zeros_like(X)
+    xh[mrows] = oracle.quantize_act(X[mrows], afmt, s, z, want_xhat=True)[2]
+    yr, bm = oracle.linear_pairs(xh, Wh, mm, nn)
+    err = np.abs(Y[mm, nn] - yr)
+    assert np.all(err <= 1e-3 * bm), (err / bm).max()
