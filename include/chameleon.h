@@ -122,12 +122,22 @@ typedef struct cham_wq {
                                NULL = skip                                                    */
     double* err;            /* [N][9]   per-format error sums (diagnostic, relative accuracy
                                1e-5; -1 for disabled formats); NULL = skip                    */
+    void* packed;           /* cham_packed_bytes(N, K) bytes, 256-byte aligned: the weights in
+                               the layout cham_mixed_linear consumes (per channel its format
+                               parameters; per (64-wide k-step, channel, half) its codes and a
+                               16-entry decode table).  Written by the search when non-NULL
+                               (K must then be a multiple of 64); cham_mixed_linear reads it
+                               instead of deriving it from the codes on every call.  It must
+                               come from the search that wrote these codes.  NULL = skip.      */
 } cham_wq;
 
 /* Search the formats of W [N][K] (device, binary32, finite) and fill *wq's buffers.
  * Ownership: the caller owns W and every buffer in *wq.  Errors: CHAM_EINVAL (NULL W/wq/
  * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K), CHAM_EHIP. */
 int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream);
+
+/* Bytes of the packed GEMM layout of an N x K weight (see cham_wq.packed). */
+size_t cham_packed_bytes(int64_t N, int64_t K);
 
 /* The same search for nlayers independent weight matrices (Sec. 4.5 applies per layer):
  * W is a host array of nlayers device pointers, wq a host array of nlayers descriptors,
@@ -235,10 +245,12 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element (NF4 levels are carried at half
  * precision; every other operand is exact).  xq->K must equal wq->K and be a multiple of
  * 64; xq->codes, wq->codes and Y must be 16-byte aligned.  Y [M][N] is written in the
- * original channel order.  When the output has too few 256x256/128x128 tiles to fill the
- * GPU, K is split across workgroups whose partial sums are added into Y with binary32
- * atomics (Y is zeroed first), so such outputs are not bitwise reproducible run to run.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of the decoded
- * activations and per-row scales), 256-byte aligned.
+ * original channel order.  When the output has too few tiles to fill the GPU, K is split
+ * across workgroups whose partial outputs a second kernel adds in split order; no atomics
+ * are used, so Y is bitwise reproducible run to run.  If wq->packed is set it supplies the
+ * weights' decode layout; otherwise a pre-pass derives it from the codes and metadata into
+ * the workspace.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of MX activations, per-row
+ * scales, the weights' decode layout, the k-split partial outputs), 256-byte aligned.
  * Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE, CHAM_EWORKSPACE, CHAM_EHIP.
  * ------------------------------------------------------------------------------------- */
 int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,

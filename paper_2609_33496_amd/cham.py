@@ -40,7 +40,7 @@ _P = ctypes.c_void_p
 class _WQ(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("palette_mask", ctypes.c_uint32),
                 ("code_bits", ctypes.c_int32), ("fmt", _P), ("codes", _P), ("scale", _P), ("zero", _P),
-                ("nf4_absmax", _P), ("e8m0", _P), ("perm", _P), ("group_off", _P), ("err", _P)]
+                ("nf4_absmax", _P), ("e8m0", _P), ("perm", _P), ("group_off", _P), ("err", _P), ("packed", _P)]
 
 
 class _Stats(ctypes.Structure):
@@ -94,6 +94,8 @@ def lib():
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
     L.cham_workspace_bytes.restype = sz
+    L.cham_packed_bytes.argtypes = [i64, i64]
+    L.cham_packed_bytes.restype = sz
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear"):
         getattr(L, name).restype = ctypes.c_int
@@ -167,14 +169,19 @@ class WQ:
     perm: Optional[torch.Tensor]
     group_off: Optional[torch.Tensor]
     err: Optional[torch.Tensor]
+    packed: Optional[torch.Tensor] = None  # GEMM-ready layout written by the search (cham_wq.packed)
 
     def struct(self) -> _WQ:
         return _WQ(self.N, self.K, self.mask, self.code_bits, _ptr(self.fmt), _ptr(self.codes), _ptr(self.scale),
                    _ptr(self.zero), _ptr(self.nf4_absmax), _ptr(self.e8m0), _ptr(self.perm), _ptr(self.group_off),
-                   _ptr(self.err))
+                   _ptr(self.err), _ptr(self.packed))
 
 
-def alloc_wq(N: int, K: int, mask: int, device="cuda", want_perm=True, want_err=False) -> WQ:
+def packed_bytes(N: int, K: int) -> int:
+    return int(lib().cham_packed_bytes(N, K))
+
+
+def alloc_wq(N: int, K: int, mask: int, device="cuda", want_perm=True, want_err=False, want_packed=False) -> WQ:
     cb = code_bits(mask)
     u8, f32, i32 = torch.uint8, torch.float32, torch.int32
     nf4 = bool(mask >> W_NF4 & 1)
@@ -188,16 +195,18 @@ def alloc_wq(N: int, K: int, mask: int, device="cuda", want_perm=True, want_err=
               e8m0=torch.empty((N, K // 32), dtype=u8, device=device) if mx else None,
               perm=torch.empty(N, dtype=i32, device=device) if want_perm else None,
               group_off=torch.empty(10, dtype=i32, device=device) if want_perm else None,
-              err=torch.empty((N, 9), dtype=torch.float64, device=device) if want_err else None)
+              err=torch.empty((N, 9), dtype=torch.float64, device=device) if want_err else None,
+              packed=torch.empty(packed_bytes(N, K), dtype=u8, device=device) if want_packed else None)
 
 
 def select_weight_formats(W: torch.Tensor, mask: int = MASK_W4, out: Optional[WQ] = None, want_perm=True,
-                          want_err=False, stream=None) -> WQ:
-    """Per-output-channel format search of W [N, K] (fp32, device)."""
+                          want_err=False, want_packed=False, stream=None) -> WQ:
+    """Per-output-channel format search of W [N, K] (fp32, device); with want_packed the
+    search also writes the GEMM-ready layout that mixed_linear then uses."""
     _dev_tensor(W, torch.float32, "W")
     N, K = W.shape
     if out is None:
-        out = alloc_wq(N, K, mask, W.device, want_perm, want_err)
+        out = alloc_wq(N, K, mask, W.device, want_perm, want_err, want_packed)
     st = out.struct()
     _check(lib().cham_select_weight_formats(_ptr(W), ctypes.byref(st), _stream(stream)), "select_weight_formats")
     out.code_bits = st.code_bits
@@ -224,10 +233,10 @@ class SearchBatch:
 
 
 def select_weight_formats_batch(Ws, mask: int = MASK_W4, outs=None, want_perm=True, want_err=False,
-                                stream=None):
+                                want_packed=False, stream=None):
     """Format search of several layers' weights (each [N_i, K_i] fp32, device) in one call."""
     if outs is None:
-        outs = [alloc_wq(W.shape[0], W.shape[1], mask, W.device, want_perm, want_err) for W in Ws]
+        outs = [alloc_wq(W.shape[0], W.shape[1], mask, W.device, want_perm, want_err, want_packed) for W in Ws]
     SearchBatch(Ws, outs).run(stream)
     return outs
 

@@ -832,6 +832,36 @@ int64_t record_bytes(int64_t N, int64_t K) { return N * (K / BK) * 2 * 64; }
 
 using namespace cham;
 
+extern "C" size_t cham_packed_bytes(int64_t N, int64_t K) {
+    if (N < 1 || K < 1) return 0;
+    return align256((size_t)N * sizeof(ColPrep)) + (size_t)record_bytes(N, K);
+}
+
+// Launches the record pre-pass of one searched weight into cols / rec (both device).
+static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStream_t s) {
+    const uint32_t mask = wq->palette_mask;
+    const int N = (int)wq->N, K = (int)wq->K;
+    const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
+    const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
+    // enough workgroups to fill the chip, at least 4 k-steps each
+    const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
+    const int nkc = std::max(1, std::min((512 + nblk - 1) / nblk, (nst + 3) / 4));
+    const int rchunk = (nst + nkc - 1) / nkc;
+    // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
+    RecArgs ra{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
+               mask, N, K, wq->code_bits, rchunk, cols, rec};
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(nblk * ((nst + rchunk - 1) / rchunk))), dim3(256), 0, s, ra);
+}
+
+// Writes wq->packed after the search (called by the search entry points, which have
+// checked the arguments and set code_bits).
+int cham_pack_weights(const cham_wq* wq, hipStream_t s) {
+    char* p = (char*)wq->packed;
+    launch_records(wq, (ColPrep*)p, (uint4*)(p + align256((size_t)wq->N * sizeof(ColPrep))), s);
+    CHAM_CHECK_LAUNCH();
+    return CHAM_OK;
+}
+
 size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
     return align256((size_t)M * (size_t)K * 2) + align256((size_t)M * 4) + align256((size_t)N * sizeof(ColPrep)) +
            align256((size_t)record_bytes(N, K)) + split_bytes(M, N, K);
@@ -858,7 +888,8 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     if ((nf4 && !wq->nf4_absmax) || (wmx && !wq->e8m0)) return CHAM_EINVAL;
     const bool amx = xq->fmt == CHAM_A_MXFP8_E4M3 || xq->fmt == CHAM_A_MXINT8;
     if (amx && !xq->e8m0) return CHAM_EINVAL;
-    if (((uintptr_t)xq->codes & 15u) || ((uintptr_t)wq->codes & 15u)) return CHAM_EINVAL;
+    if (((uintptr_t)xq->codes & 15u) || ((uintptr_t)wq->codes & 15u) || ((uintptr_t)wq->packed & 255u))
+        return CHAM_EINVAL;
     const size_t need = cham_linear_workspace_bytes(xq->M, wq->N, xq->K);
     if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return CHAM_EWORKSPACE;
     hipStream_t s = (hipStream_t)stream;
@@ -878,6 +909,10 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     uint4* rec = (uint4*)w;
     w += align256((size_t)record_bytes(N, K));
     float* part = (float*)w;
+    if (wq->packed) {  // the search's packed layout replaces the pre-pass
+        cols = (ColPrep*)wq->packed;
+        rec = (uint4*)((char*)wq->packed + align256((size_t)N * sizeof(ColPrep)));
+    }
 
     if (amx) {
         PrepArgs p{xq->codes, xq->e8m0, xq->fmt, M, K, code_bits == 4, Xh, rowscale};
@@ -885,14 +920,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
 
-    // enough workgroups to fill the chip, at least 4 k-steps each
-    const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
-    const int nkc = std::max(1, std::min((512 + nblk - 1) / nblk, (nst + 3) / 4));
-    const int rchunk = (nst + nkc - 1) / nkc;
-    // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
-    RecArgs ra{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
-               mask, N, K, code_bits, rchunk, cols, rec};
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(nblk * ((nst + rchunk - 1) / rchunk))), dim3(256), 0, s, ra);
+    if (!wq->packed) launch_records(wq, cols, rec, s);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;

@@ -768,6 +768,8 @@ void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipSt
 
 using namespace cham;
 
+int cham_pack_weights(const cham_wq* wq, hipStream_t s);  // the GEMM's record pre-pass
+
 static int mask_code_bits(uint32_t mask) {
     return (mask & 0x7u) ? 8 : 4;  // formats 0..2 are the 8-bit ones
 }
@@ -787,6 +789,10 @@ static int prepare_layer(const float* W, cham_wq* wq, SearchArgs& a) {
     if ((nf4 && !wq->nf4_absmax) || (mx && !wq->e8m0)) return CHAM_EINVAL;
     if (((uintptr_t)W & 15u) || ((uintptr_t)wq->codes & 3u)) return CHAM_EINVAL;
     if (K > 32 * 256) return CHAM_ESHAPE;  // rows up to 8192 are held in registers
+    if (wq->packed) {  // the packed GEMM layout: 64-wide k-steps, 32-bit record offsets
+        if (K % 64 != 0) return CHAM_ESHAPE;
+        if (((uintptr_t)wq->packed & 255u) || wq->N * (K / 64) * 128 > (int64_t)INT32_MAX) return CHAM_EINVAL;
+    }
     a.W = W;
     a.N = wq->N;
     a.K = (int)K;
@@ -836,6 +842,8 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
         CHAM_CHECK_LAUNCH();
     }
     for (int i = 0; i < nlayers; ++i) wq[i].code_bits = args[i].code_bits;
+    for (int i = 0; i < nlayers; ++i)
+        if (wq[i].packed && cham_pack_weights(&wq[i], s) != CHAM_OK) return CHAM_EHIP;
     // grouping: one workgroup per layer that asks for it
     GroupBatch G;
     G.nl = 0;

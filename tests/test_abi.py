@@ -41,14 +41,16 @@ def test_host_only_helpers():
     assert cham.workspace_bytes(cham.OP_QUANT_ACT, 2048, 0, 1280) > 0
     assert cham.workspace_bytes(cham.OP_SELECT, 10, 10, 64) == 0
     assert cham.workspace_bytes(cham.OP_LINEAR, 2048, 1280, 1280) >= 2048 * 1280 * 2 + 2048 * 4
+    assert cham.packed_bytes(1280, 1280) == 1280 * 16 + 1280 * 20 * 2 * 64
+    assert cham.packed_bytes(0, 64) == 0
 
 
 def _wq(**kw):
     d = dict(N=4, K=64, palette_mask=cham.MASK_W4, code_bits=0, fmt=16, codes=16, scale=16, zero=16,
-             nf4_absmax=16, e8m0=16, perm=None, group_off=None, err=None)
+             nf4_absmax=16, e8m0=16, perm=None, group_off=None, err=None, packed=None)
     d.update(kw)
     return cham._WQ(d["N"], d["K"], d["palette_mask"], d["code_bits"], *[d[k] for k in (
-        "fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err")])
+        "fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err", "packed")])
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -60,6 +62,8 @@ def _wq(**kw):
     (dict(nf4_absmax=None), cham.EINVAL),
     (dict(e8m0=None), cham.EINVAL),
     (dict(fmt=None), cham.EINVAL),
+    (dict(K=96, palette_mask=1 << cham.W_FP4, packed=256), cham.ESHAPE),  # packed layout: K % 64
+    (dict(packed=16), cham.EINVAL),                                      # packed layout: 256-byte aligned
 ])
 def test_select_weight_formats_argument_errors(kw, status):
     w = _wq(**kw)

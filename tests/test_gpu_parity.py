@@ -141,14 +141,20 @@ def test_search_batch_matches_single_calls():
         W, _ = synth.hetero_weights(500 + i, N, K)
         Wd = torch.from_numpy(W).to(DEV)
         Ws.append(Wd)
-        outs.append(cham.alloc_wq(N, K, m, DEV, want_perm=(i % 3 != 2), want_err=(i % 5 == 0)))
-        singles.append(cham.select_weight_formats(Wd, m, want_perm=(i % 3 != 2), want_err=(i % 5 == 0)))
+        pk = K % 64 == 0 and i % 2 == 0
+        o, o1 = [cham.alloc_wq(N, K, m, DEV, want_perm=(i % 3 != 2), want_err=(i % 5 == 0), want_packed=pk)
+                 for _ in range(2)]
+        if pk:  # the layout leaves alignment padding unwritten: start both from zeros
+            o.packed.zero_()
+            o1.packed.zero_()
+        outs.append(o)
+        singles.append(cham.select_weight_formats(Wd, m, out=o1))
     case("select_weight_formats_batch 19 layers")
     cham.select_weight_formats_batch(Ws, outs=outs)
     torch.cuda.synchronize()
     for i, (a, b) in enumerate(zip(outs, singles)):
         assert a.code_bits == b.code_bits, i
-        for name in ("fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err"):
+        for name in ("fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "err", "packed"):
             x, y = getattr(a, name), getattr(b, name)
             assert (x is None) == (y is None), (i, name)
             if x is not None:
@@ -344,6 +350,9 @@ def _linear_case(X, W, mask, afmt, dynamic=True):
     err = np.abs(Y - Yr)
     bad = err > 1e-3 * Bm
     assert not bad.any(), (np.argwhere(bad)[:5], (err / np.maximum(Bm, 1e-300)).max())
+    # the search's packed layout gives the same kernels the same operands: identical Y
+    wp = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask, want_packed=True)
+    assert np.array_equal(_np(cham.mixed_linear(xq, wp)).astype(np.float64), Y)
     return (err / np.maximum(Bm, 1e-300)).max()
 
 
@@ -431,9 +440,11 @@ def test_linear_plans_sampled(M, N, K, mask, afmt):
     X = synth.diffusion_acts(5, 2, 600, M, K)
     W, _ = synth.hetero_weights(31, N, K)
     case(f"mixed_linear plan M={M} N={N} K={K} mask={mask:#x} afmt={afmt}")
-    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask)
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask, want_packed=True)
     xq = cham.quantize_act(torch.from_numpy(X).to(DEV), afmt, dynamic=True)
     Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+    wq.packed = None  # the same call deriving the layout from the codes in its pre-pass
+    assert np.array_equal(_np(cham.mixed_linear(xq, wq)).astype(np.float64), Y)
     g = np.random.default_rng(M + N + K + afmt)
     mm = np.concatenate([g.integers(0, M, 1500), [M - 1, 0]])
     nn = np.concatenate([g.integers(0, N, 1500), [N - 1, 0]])
