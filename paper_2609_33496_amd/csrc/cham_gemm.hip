@@ -283,12 +283,25 @@ CHAM_DEV Table record_table(const ColPrep& c, float nf4a, int e8) {
     return tb;
 }
 
-__global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
+// Several weights' records in one launch: the workgroups of the batch's layers follow
+// each other (descriptors in the kernel arguments).
+constexpr int kRecBatchMax = 16;
+struct RecBatch {
+    int nl;
+    int wg_end[kRecBatchMax];  // workgroups of layers 0..i
+    RecArgs r[kRecBatchMax];
+};
+
+__global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     __shared__ ColPrep cp[kRecChannels];
+    int li = 0;
+    while (li + 1 < B.nl && (int)blockIdx.x >= B.wg_end[li]) ++li;
+    const RecArgs& a = B.r[li];
+    const int bid = (int)blockIdx.x - (li ? B.wg_end[li - 1] : 0);
     const int t = threadIdx.x;
     const int K = a.K, nst = K / BK;
     const int nblk = (a.N + kRecChannels - 1) / kRecChannels;
-    const int cb = (int)blockIdx.x % nblk, kc = (int)blockIdx.x / nblk;
+    const int cb = bid % nblk, kc = bid / nblk;
     const int n0 = cb * kRecChannels;
     const int cw = a.code_bits / 4;  // 16-byte code pieces per half k-step
     const int64_t cstride = (int64_t)K * a.code_bits / 8;
@@ -324,15 +337,22 @@ __global__ __launch_bounds__(256) void record_kernel(RecArgs a) {
         const int nn = n0 + ch;
         const int f = nn < a.N ? a.wfmt[nn] : CHAM_W_NFMT;
         const bool ok = f < CHAM_W_NFMT && ((a.mask >> f) & 1u);
+        // the block metadata of every enabled kind is read without waiting for the format
+        // (it is zero for channels of other formats), so these loads overlap the format load
         float mxf = 0.0f;
         int mxe = 0;
-        if (ok && f == CHAM_W_NF4) {
+        if (nn < a.N && a.wnf4) {
             const float* r = a.wnf4 + (int64_t)nn * (K / 64);
+#pragma unroll 4
             for (int b = sub; b < K / 64; b += 8) mxf = fmaxf(mxf, r[b]);
-        } else if (ok && is_mx(f)) {
+        }
+        if (nn < a.N && a.we8) {
             const uint8_t* r = a.we8 + (int64_t)nn * (K / 32);
+#pragma unroll 4
             for (int b = sub; b < K / 32; b += 8) mxe = max(mxe, (int)r[b]);
         }
+        if (!(ok && f == CHAM_W_NF4)) mxf = 0.0f;
+        if (!(ok && is_mx(f))) mxe = 0;
 #pragma unroll
         for (int o = 1; o < 8; o <<= 1) {
             mxf = fmaxf(mxf, __shfl_xor(mxf, o, kWave));
@@ -837,8 +857,9 @@ extern "C" size_t cham_packed_bytes(int64_t N, int64_t K) {
     return align256((size_t)N * sizeof(ColPrep)) + (size_t)record_bytes(N, K);
 }
 
-// Launches the record pre-pass of one searched weight into cols / rec (both device).
-static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStream_t s) {
+// Record pre-pass arguments of one searched weight writing into cols / rec (device), and
+// the workgroups it takes.
+static RecArgs record_args(const cham_wq* wq, ColPrep* cols, uint4* rec, int* wgs) {
     const uint32_t mask = wq->palette_mask;
     const int N = (int)wq->N, K = (int)wq->K;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
@@ -847,18 +868,39 @@ static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStre
     const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
     const int nkc = std::max(1, std::min((512 + nblk - 1) / nblk, (nst + 3) / 4));
     const int rchunk = (nst + nkc - 1) / nkc;
+    *wgs = nblk * ((nst + rchunk - 1) / rchunk);
     // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
-    RecArgs ra{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
-               mask, N, K, wq->code_bits, rchunk, cols, rec};
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(nblk * ((nst + rchunk - 1) / rchunk))), dim3(256), 0, s, ra);
+    return RecArgs{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
+                   mask, N, K, wq->code_bits, rchunk, cols, rec};
 }
 
-// Writes wq->packed after the search (called by the search entry points, which have
-// checked the arguments and set code_bits).
-int cham_pack_weights(const cham_wq* wq, hipStream_t s) {
-    char* p = (char*)wq->packed;
-    launch_records(wq, (ColPrep*)p, (uint4*)(p + align256((size_t)wq->N * sizeof(ColPrep))), s);
-    CHAM_CHECK_LAUNCH();
+static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStream_t s) {
+    RecBatch B;
+    B.nl = 1;
+    int wgs = 0;
+    B.r[0] = record_args(wq, cols, rec, &wgs);
+    B.wg_end[0] = wgs;
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)wgs), dim3(256), 0, s, B);
+}
+
+// Writes the packed layout of n searched weights (called by the search entry points, which
+// have checked the arguments and set code_bits); one launch per kRecBatchMax weights.
+int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
+    for (int i0 = 0; i0 < n; i0 += kRecBatchMax) {
+        RecBatch B;
+        B.nl = std::min(kRecBatchMax, n - i0);
+        int total = 0;
+        for (int j = 0; j < B.nl; ++j) {
+            const cham_wq* wq = wqs[i0 + j];
+            char* p = (char*)wq->packed;
+            int wgs = 0;
+            B.r[j] = record_args(wq, (ColPrep*)p, (uint4*)(p + align256((size_t)wq->N * sizeof(ColPrep))), &wgs);
+            total += wgs;
+            B.wg_end[j] = total;
+        }
+        hipLaunchKernelGGL(record_kernel, dim3((unsigned)total), dim3(256), 0, s, B);
+        CHAM_CHECK_LAUNCH();
+    }
     return CHAM_OK;
 }
 

@@ -34,6 +34,7 @@ struct SearchArgs {
     float* nf4a;
     uint8_t* e8;
     double* err;
+    int split;  // wavefronts per channel: 1, or 4 (a quarter of the row each)
 };
 
 // per-channel parameters of the per-channel formats
@@ -336,7 +337,7 @@ CHAM_DEV double row_err64(const float (&v)[NCH][4], const bool (&valid)[NCH], co
 
 CHAM_DEV float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 
-// Cross-wavefront sums when SPLIT wavefronts share a channel (SPLIT = 4: the whole
+// Cross-wavefront sums when `split` wavefronts share a channel (split = 4: the whole
 // workgroup); partial values are combined in wavefront order, so the result is fixed.
 struct SplitLDS {
     float lohi[4][2];
@@ -344,13 +345,15 @@ struct SplitLDS {
     double ed[4][CHAM_W_NFMT];
 };
 
-// Search of channel n by SPLIT wavefronts; this wavefront holds part `part` of the row
-// (K / SPLIT consecutive elements, a multiple of 64).
-template <uint32_t MASK, int NCH, int SPLIT>
+// Search of channel n by `split` wavefronts; this wavefront holds part `part` of the row
+// (K / split consecutive elements, a multiple of 64).  split is the same for the whole
+// workgroup, so the barriers below are reached by all of its wavefronts.
+template <uint32_t MASK, int NCH>
 CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, int part, SplitLDS* sl) {
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const int K = a.K;
+    const int SPLIT = a.split;
     const int KP = K / SPLIT;  // elements of this wavefront
     const int nq = KP >> 2;    // float4 of this wavefront
     const float* row = a.W + n * (int64_t)K + (int64_t)part * KP;
@@ -385,7 +388,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
         if (lane == 0) { sl->lohi[wv][0] = lo; sl->lohi[wv][1] = hi; }
         __syncthreads();
 #pragma unroll
-        for (int w = 0; w < SPLIT; ++w) { lo = fminf(lo, sl->lohi[w][0]); hi = fmaxf(hi, sl->lohi[w][1]); }
+        for (int w = 0; w < 4; ++w) { lo = fminf(lo, sl->lohi[w][0]); hi = fmaxf(hi, sl->lohi[w][1]); }
     }
     const float amax = fmaxf(fabsf(lo), fabsf(hi));
 
@@ -434,7 +437,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
             if (!(mask & (1u << f))) continue;
             float t = sl->e[0][f];
 #pragma unroll
-            for (int w = 1; w < SPLIT; ++w) t += sl->e[w][f];
+            for (int w = 1; w < 4; ++w) t += sl->e[w][f];
             e[f] = t;
         }
     }
@@ -479,7 +482,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
                 if (!(mask & (1u << f))) continue;
                 double t = sl->ed[0][f];
 #pragma unroll
-                for (int w = 1; w < SPLIT; ++w) t += sl->ed[w][f];
+                for (int w = 1; w < 4; ++w) t += sl->ed[w][f];
                 ed[f] = t;
             }
         }
@@ -692,10 +695,10 @@ struct SearchBatch {
     SearchArgs l[kBatchMax];
 };
 
-// SPLIT = 1: four channels per workgroup, one per wavefront.  SPLIT = 4: one channel per
+// split = 1: four channels per workgroup, one per wavefront.  split = 4: one channel per
 // workgroup, a quarter of the row per wavefront (more wavefronts in flight when the
 // layer has few channels).  The workgroups of the batch's layers follow each other.
-template <uint32_t MASK, int NCH, int SPLIT>
+template <uint32_t MASK, int NCH>
 __global__ __launch_bounds__(256) void search_kernel(SearchBatch B) {
     __shared__ NF4Cell cells[33];
     __shared__ SplitLDS sl;
@@ -707,16 +710,16 @@ __global__ __launch_bounds__(256) void search_kernel(SearchBatch B) {
     const SearchArgs& a = B.l[i];
     const int64_t lb = b - (i ? B.wg_end[i - 1] : 0);
     const int wv = threadIdx.x >> 6;
-    const int64_t n = SPLIT == 1 ? lb * 4 + wv : lb;
-    if (n < a.N) search_row<MASK, NCH, SPLIT>(a, cells, n, SPLIT == 1 ? 0 : wv, &sl);  // workgroup-uniform for SPLIT 4
+    const int64_t n = a.split == 1 ? lb * 4 + wv : lb;
+    if (n < a.N) search_row<MASK, NCH>(a, cells, n, a.split == 1 ? 0 : wv, &sl);  // workgroup-uniform for split 4
 }
 
-template <int NCH, int SPLIT>
+template <int NCH>
 void launch_search(const SearchBatch& B, uint32_t mask, hipStream_t s) {
     const dim3 grid((unsigned)B.wg_end[B.nl - 1]);
-    if (mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH, SPLIT>), grid, dim3(256), 0, s, B);
-    else if (mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH, SPLIT>), grid, dim3(256), 0, s, B);
-    else hipLaunchKernelGGL((search_kernel<0u, NCH, SPLIT>), grid, dim3(256), 0, s, B);
+    if (mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W4, NCH>), grid, dim3(256), 0, s, B);
+    else if (mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_kernel<CHAM_MASK_W8, NCH>), grid, dim3(256), 0, s, B);
+    else hipLaunchKernelGGL((search_kernel<0u, NCH>), grid, dim3(256), 0, s, B);
 }
 
 // Layers with few channels and long rows split each row over the four wavefronts of a
@@ -734,32 +737,22 @@ Variant variant_of(int64_t N, int64_t K) {
     const bool fill = K % 256 == 0 && qc * 100 >= 85 * ((qc + 255) / 256 * 256);
     const int split = (fill && K >= 1024 && N < kSplitBelowChannels) ? 4 : 1;
     const int nch = (int)((K / split + 255) / 256);
-    static const int c4[] = {2, 3, 5, 8}, c1[] = {3, 5, 10, 20, 32};
-    int r = 0;
-    if (split == 4) {
-        for (int c : c4) if (nch <= c) { r = c; break; }
-    } else {
-        for (int c : c1) if (nch <= c) { r = c; break; }
-    }
+    static const int counts[] = {2, 3, 5, 8, 10, 20, 32};
+    int r = 32;
+    for (int c : counts)
+        if (nch <= c) { r = c; break; }
     return Variant{split, r};
 }
 
-void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipStream_t s) {
-    if (v.split == 4) {
-        switch (v.nch) {
-        case 2: launch_search<2, 4>(B, mask, s); break;
-        case 3: launch_search<3, 4>(B, mask, s); break;
-        case 5: launch_search<5, 4>(B, mask, s); break;
-        default: launch_search<8, 4>(B, mask, s); break;
-        }
-    } else {
-        switch (v.nch) {
-        case 3: launch_search<3, 1>(B, mask, s); break;
-        case 5: launch_search<5, 1>(B, mask, s); break;
-        case 10: launch_search<10, 1>(B, mask, s); break;
-        case 20: launch_search<20, 1>(B, mask, s); break;
-        default: launch_search<32, 1>(B, mask, s); break;
-        }
+void launch_variant(int nch, const SearchBatch& B, uint32_t mask, hipStream_t s) {
+    switch (nch) {
+    case 2: launch_search<2>(B, mask, s); break;
+    case 3: launch_search<3>(B, mask, s); break;
+    case 5: launch_search<5>(B, mask, s); break;
+    case 8: launch_search<8>(B, mask, s); break;
+    case 10: launch_search<10>(B, mask, s); break;
+    case 20: launch_search<20>(B, mask, s); break;
+    default: launch_search<32>(B, mask, s); break;
     }
 }
 
@@ -768,7 +761,7 @@ void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipSt
 
 using namespace cham;
 
-int cham_pack_weights(const cham_wq* wq, hipStream_t s);  // the GEMM's record pre-pass
+int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s);  // the GEMM's record pre-pass
 
 static int mask_code_bits(uint32_t mask) {
     return (mask & 0x7u) ? 8 : 4;  // formats 0..2 are the 8-bit ones
@@ -816,11 +809,12 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
         if (rc != CHAM_OK) return rc;
     }
     hipStream_t s = (hipStream_t)stream;
-    // one launch per kernel variant (and palette), up to kBatchMax layers each
+    // one launch per register-chunk count (and palette), up to kBatchMax layers each
     std::vector<bool> done((size_t)nlayers, false);
     for (int i = 0; i < nlayers; ++i) {
         if (done[i]) continue;
         const Variant v = variant_of(args[i].N, args[i].K);
+        args[i].split = v.split;
         const uint32_t key = args[i].mask == CHAM_MASK_W4 || args[i].mask == CHAM_MASK_W8 ? args[i].mask : 0u;
         SearchBatch B;
         B.nl = 0;
@@ -829,8 +823,9 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
             if (done[j]) continue;
             const Variant vj = variant_of(args[j].N, args[j].K);
             const uint32_t kj = args[j].mask == CHAM_MASK_W4 || args[j].mask == CHAM_MASK_W8 ? args[j].mask : 0u;
-            if (vj.split != v.split || vj.nch != v.nch || kj != key) continue;
-            wgs += v.split == 1 ? (args[j].N + 3) / 4 : args[j].N;
+            if (vj.nch != v.nch || kj != key) continue;
+            args[j].split = vj.split;
+            wgs += vj.split == 1 ? (args[j].N + 3) / 4 : args[j].N;
             B.l[B.nl] = args[j];
             B.wg_end[B.nl] = wgs;
             ++B.nl;
@@ -838,12 +833,14 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
             if (B.nl == kBatchMax) break;
         }
         // a mixed palette (key 0) reads each layer's mask at run time
-        launch_variant(v, B, key ? key : 0u, s);
+        launch_variant(v.nch, B, key ? key : 0u, s);
         CHAM_CHECK_LAUNCH();
     }
     for (int i = 0; i < nlayers; ++i) wq[i].code_bits = args[i].code_bits;
+    std::vector<const cham_wq*> pk;
     for (int i = 0; i < nlayers; ++i)
-        if (wq[i].packed && cham_pack_weights(&wq[i], s) != CHAM_OK) return CHAM_EHIP;
+        if (wq[i].packed) pk.push_back(&wq[i]);
+    if (!pk.empty() && cham_pack_weights(pk.data(), (int)pk.size(), s) != CHAM_OK) return CHAM_EHIP;
     // grouping: one workgroup per layer that asks for it
     GroupBatch G;
     G.nl = 0;

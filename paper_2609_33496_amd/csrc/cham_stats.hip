@@ -94,7 +94,8 @@ __global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Par
     }
     double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
     float lo = INFINITY, hi = -INFINITY;
-    for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {
+#pragma unroll 4
+    for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {  // loads of 4 partials in flight
         Partial p = part[i];
         s1 += p.s1; s2 += p.s2; s3 += p.s3; s4 += p.s4;
         lo = fminf(lo, p.lo); hi = fmaxf(hi, p.hi);
