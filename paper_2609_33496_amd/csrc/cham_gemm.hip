@@ -35,6 +35,7 @@
 // byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation operand is
 // staged with its columns in that same order.
 #include "cham_device.h"
+#include "cham_group.h"
 
 namespace cham {
 namespace {
@@ -284,20 +285,29 @@ CHAM_DEV Table record_table(const ColPrep& c, float nf4a, int e8) {
 }
 
 // Several weights' records in one launch: the workgroups of the batch's layers follow
-// each other (descriptors in the kernel arguments).
+// each other (descriptors in the kernel arguments); before them, one workgroup per entry
+// of g groups a searched weight's channels by format (the search's grouping, run here when
+// the search also packs the weights, to save a launch; first, so its longer serial work
+// overlaps the records instead of trailing them).
 constexpr int kRecBatchMax = 16;
 struct RecBatch {
-    int nl;
+    int nl, ng;
     int wg_end[kRecBatchMax];  // workgroups of layers 0..i
     RecArgs r[kRecBatchMax];
+    GroupArgs g[kRecBatchMax];
 };
 
 __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     __shared__ ColPrep cp[kRecChannels];
+    if ((int)blockIdx.x < B.ng) {  // workgroup-uniform
+        group_channels<256>(B.g[blockIdx.x], nullptr);
+        return;
+    }
+    const int rb = (int)blockIdx.x - B.ng;  // record workgroup index
     int li = 0;
-    while (li + 1 < B.nl && (int)blockIdx.x >= B.wg_end[li]) ++li;
+    while (li + 1 < B.nl && rb >= B.wg_end[li]) ++li;
     const RecArgs& a = B.r[li];
-    const int bid = (int)blockIdx.x - (li ? B.wg_end[li - 1] : 0);
+    const int bid = rb - (li ? B.wg_end[li - 1] : 0);
     const int t = threadIdx.x;
     const int K = a.K, nst = K / BK;
     const int nblk = (a.N + kRecChannels - 1) / kRecChannels;
@@ -877,6 +887,7 @@ static RecArgs record_args(const cham_wq* wq, ColPrep* cols, uint4* rec, int* wg
 static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStream_t s) {
     RecBatch B;
     B.nl = 1;
+    B.ng = 0;
     int wgs = 0;
     B.r[0] = record_args(wq, cols, rec, &wgs);
     B.wg_end[0] = wgs;
@@ -884,11 +895,13 @@ static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStre
 }
 
 // Writes the packed layout of n searched weights (called by the search entry points, which
-// have checked the arguments and set code_bits); one launch per kRecBatchMax weights.
+// have checked the arguments and set code_bits), and groups the channels of those that ask
+// for perm / group_off; one launch per kRecBatchMax weights.
 int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
     for (int i0 = 0; i0 < n; i0 += kRecBatchMax) {
         RecBatch B;
         B.nl = std::min(kRecBatchMax, n - i0);
+        B.ng = 0;
         int total = 0;
         for (int j = 0; j < B.nl; ++j) {
             const cham_wq* wq = wqs[i0 + j];
@@ -897,8 +910,9 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
             B.r[j] = record_args(wq, (ColPrep*)p, (uint4*)(p + align256((size_t)wq->N * sizeof(ColPrep))), &wgs);
             total += wgs;
             B.wg_end[j] = total;
+            if (wq->perm || wq->group_off) B.g[B.ng++] = GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off};
         }
-        hipLaunchKernelGGL(record_kernel, dim3((unsigned)total), dim3(256), 0, s, B);
+        hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + B.ng)), dim3(256), 0, s, B);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;

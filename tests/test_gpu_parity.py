@@ -167,16 +167,18 @@ def test_search_grouping_repeated_and_partial_outputs():
     Wa, _ = synth.hetero_weights(21, 3000, 640)   # 750 workgroups, ragged last one
     Wb, _ = synth.hetero_weights(22, 3000, 640)
     wq = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV)
-    for it, W in enumerate((Wa, Wb, Wa)):
-        case(f"select_weight_formats grouping call {it} N=3000 K=640")
+    wp = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV, want_packed=True)  # grouping in the packing launch
+    for it, (W, w) in enumerate(((Wa, wq), (Wb, wq), (Wa, wq), (Wb, wp), (Wa, wp))):
+        wq = w
+        case(f"select_weight_formats grouping call {it} N=3000 K=640 packed={w.packed is not None}")
         cham.select_weight_formats(torch.from_numpy(W).to(DEV), oracle.MASK_W4, out=wq)
         torch.cuda.synchronize()
         f = _np(wq.fmt)
         assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable"))
         assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(np.bincount(f, minlength=9))]))
-    for keep in ("perm", "group_off"):
-        case(f"select_weight_formats grouping with only {keep}")
-        w2 = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV)
+    for keep, pk in (("perm", False), ("group_off", False), ("perm", True), ("group_off", True)):
+        case(f"select_weight_formats grouping with only {keep} packed={pk}")
+        w2 = cham.alloc_wq(3000, 640, oracle.MASK_W4, DEV, want_packed=pk)
         setattr(w2, "group_off" if keep == "perm" else "perm", None)
         cham.select_weight_formats(torch.from_numpy(Wa).to(DEV), oracle.MASK_W4, out=w2)
         torch.cuda.synchronize()
