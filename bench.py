@@ -8,7 +8,7 @@ kurtosis and SNR (scaled-linear schedule 0.00085 -> 0.012, T = 1000) assigns.
 
 One step = one pass of every step of the path over one batch, all inputs resident in HBM:
   select_weight_formats_batch (the 4 layers, one call, also writing each layer's packed GEMM
-  layout) -> act_stats_accumulate (4 layer inputs) ->
+  layout) -> act_stats_accumulate_batch (the 4 layer inputs, one call) ->
   build_act_lut -> quantize_act_lut (4) -> mixed_linear (4).
 
 Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step time (GEMM
@@ -134,14 +134,14 @@ def main():
         del src, dst
 
     # prepared C structs and workspaces (the step issues raw C-ABI calls)
-    ws_stats = [torch.empty(max(cham.workspace_bytes(cham.OP_STATS, X.numel(), 0, 0), 256), dtype=torch.uint8,
-                            device=dev) for X in Xs]
     ws_q = [torch.empty(max(cham.workspace_bytes(cham.OP_QUANT_ACT, M_TOKENS, 0, X.shape[1]), 256),
                         dtype=torch.uint8, device=dev) for X in Xs]
     ws_lin = [torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=dev)
               for (_, K, N) in layers]
     wq_s = [w.struct() for w in wqs]
     sbatch = cham.SearchBatch(Ws, wqs)  # the block's four layers searched in one call
+    # the four layer inputs' statistics in one call (as one calibration forward pass gives them)
+    tbatch = cham.StatsBatch(Xs, list(range(len(layers))), [bucket] * len(layers), stats)
     st_s = stats.struct()
     sc_s = sched.struct()
     lut_s = lut.struct()
@@ -162,10 +162,9 @@ def main():
             e1 = torch.cuda.Event(enable_timing=True)
             e1.record(stream)
             ev["search"].append((e0, e1))
-        for li in range(len(layers)):
-            rc = L.cham_act_stats_accumulate(P(Xs[li]), Xs[li].numel(), li, bucket, ctypes.byref(st_s),
-                                             P(ws_stats[li]), ws_stats[li].numel(), S)
-            assert rc == 0, rc
+        rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, len(layers),
+                                               ctypes.byref(st_s), P(tbatch.ws), tbatch.ws_bytes, S)
+        assert rc == 0, rc
         rc = L.cham_build_act_lut(ctypes.byref(st_s), ctypes.byref(sc_s), None, ctypes.byref(lut_s), None, S)
         assert rc == 0, rc
         for li in range(len(layers)):

@@ -166,6 +166,16 @@ int cham_act_stats_reset(cham_act_stats* st, void* stream);
 int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t layer, int32_t bucket,
                               cham_act_stats* st, void* ws, size_t ws_bytes, void* stream);
 
+/* The same for n tensors X[i] (host array of device pointers) of (layer[i], bucket[i]),
+ * e.g. every instrumented layer's input of one calibration forward pass: the result is
+ * bitwise that of n calls in array order (tensors of the same (layer, bucket) are added in
+ * that order), in fewer launches.  numel, layer, bucket: host arrays of n.  ws: the sum of
+ * cham_workspace_bytes(CHAM_OP_STATS, numel[i], 0, 0) over i.  Every argument is checked
+ * before anything is launched.  Errors: as cham_act_stats_accumulate. */
+int cham_act_stats_accumulate_batch(const float* const* X, const int64_t* numel, const int32_t* layer,
+                                    const int32_t* bucket, int32_t n, cham_act_stats* st, void* ws,
+                                    size_t ws_bytes, void* stream);
+
 #define CHAM_SCHED_SCALED_LINEAR 0
 #define CHAM_SCHED_LINEAR 1
 typedef struct cham_schedule {

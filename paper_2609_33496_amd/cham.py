@@ -82,6 +82,8 @@ def lib():
     L.cham_select_weight_formats_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(_WQ), i32, _P]
     L.cham_act_stats_reset.argtypes = [ctypes.POINTER(_Stats), _P]
     L.cham_act_stats_accumulate.argtypes = [_P, i64, i32, i32, ctypes.POINTER(_Stats), _P, sz, _P]
+    L.cham_act_stats_accumulate_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(i64), ctypes.POINTER(i32),
+                                                  ctypes.POINTER(i32), i32, ctypes.POINTER(_Stats), _P, sz, _P]
     L.cham_schedule_default.argtypes = [ctypes.POINTER(_Sched)]
     L.cham_schedule_default.restype = None
     L.cham_build_act_lut.argtypes = [ctypes.POINTER(_Stats), ctypes.POINTER(_Sched), _P, ctypes.POINTER(_LUT), _P,
@@ -97,6 +99,7 @@ def lib():
     L.cham_packed_bytes.argtypes = [i64, i64]
     L.cham_packed_bytes.restype = sz
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
+                 "cham_act_stats_accumulate_batch",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -263,6 +266,35 @@ def alloc_stats(L: int, B: int, device="cuda") -> Stats:
 def act_stats_reset(st: Stats, stream=None):
     s = st.struct()
     _check(lib().cham_act_stats_reset(ctypes.byref(s), _stream(stream)), "act_stats_reset")
+
+
+class StatsBatch:
+    """Prepared C arguments of a batched statistics accumulation (several layer inputs),
+    reusable across calls with the same tensors."""
+
+    def __init__(self, Xs, layers, buckets, st: Stats, ws=None):
+        n = len(Xs)
+        assert n > 0 and len(layers) == n and len(buckets) == n
+        for X in Xs:
+            _dev_tensor(X, torch.float32, "X")
+        self.Xs, self.st = list(Xs), st
+        self.ptrs = (_P * n)(*[X.data_ptr() for X in Xs])
+        self.numel = (ctypes.c_int64 * n)(*[X.numel() for X in Xs])
+        self.layer = (ctypes.c_int32 * n)(*layers)
+        self.bucket = (ctypes.c_int32 * n)(*buckets)
+        nb = sum(workspace_bytes(OP_STATS, X.numel(), 0, 0) for X in Xs)
+        self.ws = ws if ws is not None else torch.empty(max(nb, 256), dtype=torch.uint8, device=Xs[0].device)
+        self.ws_bytes = self.ws.numel()
+        self.s = st.struct()
+
+    def run(self, stream=None):
+        _check(lib().cham_act_stats_accumulate_batch(self.ptrs, self.numel, self.layer, self.bucket, len(self.Xs),
+                                                     ctypes.byref(self.s), _ptr(self.ws), self.ws_bytes,
+                                                     _stream(stream)), "act_stats_accumulate_batch")
+
+
+def act_stats_accumulate_batch(Xs, layers, buckets, st: Stats, stream=None):
+    StatsBatch(Xs, layers, buckets, st).run(stream)
 
 
 def act_stats_accumulate(X: torch.Tensor, layer: int, bucket: int, st: Stats, ws=None, stream=None):

@@ -8,6 +8,8 @@
 // floating atomics).  The LUT build runs in one workgroup (B <= 1024 buckets).
 #include <math.h>
 
+#include <algorithm>
+
 #include "cham_device.h"
 
 namespace cham {
@@ -22,12 +24,27 @@ struct Partial {
     float pad0, pad1;
 };
 
-__global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const float* X, int64_t numel,
-                                                                       Partial* part) {
+// Tensors of one accumulate call (several for the batched call): workgroups of tensor i are
+// [blk_end[i-1], blk_end[i]); partials are stored at the workgroup index.
+constexpr int kStatsBatchMax = 16;
+struct StatsBatch {
+    int n;
+    int blk_end[kStatsBatchMax];
+    const float* X[kStatsBatchMax];
+    int64_t numel[kStatsBatchMax];
+};
+
+__global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(StatsBatch B, Partial* part) {
+    int ti = 0;
+    while (ti + 1 < B.n && (int)blockIdx.x >= B.blk_end[ti]) ++ti;
+    const int b0 = ti ? B.blk_end[ti - 1] : 0;
+    const int lb = (int)blockIdx.x - b0, nb = B.blk_end[ti] - b0;  // this tensor's workgroups
+    const float* X = B.X[ti];
+    const int64_t numel = B.numel[ti];
     double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
     float lo = INFINITY, hi = -INFINITY;
     const int64_t nq = numel >> 2;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t stride = (int64_t)nb * blockDim.x;
     const float4* X4 = reinterpret_cast<const float4*>(X);
     auto add = [&](const float4& t) {
         const float e[4] = {t.x, t.y, t.z, t.w};
@@ -44,7 +61,7 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
         }
     };
     // four loads in flight per thread, then their sums in index order
-    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t i = (int64_t)lb * blockDim.x + threadIdx.x;
     for (; i + 3 * stride < nq; i += 4 * stride) {
         const float4 t0 = X4[i], t1 = X4[i + stride], t2 = X4[i + 2 * stride], t3 = X4[i + 3 * stride];
         add(t0); add(t1); add(t2); add(t3);
@@ -58,8 +75,8 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
         if (v1) add(t1);
         if (v2) add(t2);
     }
-    // scalar tail (numel % 4), handled by the first threads of workgroup 0
-    if (blockIdx.x == 0 && threadIdx.x < (numel & 3)) {
+    // scalar tail (numel % 4), handled by the first threads of the tensor's workgroup 0
+    if (lb == 0 && threadIdx.x < (numel & 3)) {
         float x = X[(nq << 2) + threadIdx.x];
         double d = (double)x, d2 = d * d;
         s1 += d; s2 += d2; s3 += d2 * d; s4 += d2 * d2;
@@ -81,8 +98,23 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(const floa
     }
 }
 
-__global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Partial* part, int nparts,
-                                                                        int64_t numel, double* nS, float* lohi) {
+// Finalize of a batch: workgroup j owns accumulator target j and adds the sums of its
+// tensors in batch order (each tensor's partials in index order, as one call would), so
+// a batch gives the bits that one call per tensor would.
+struct FinBatch {
+    int ntgt;
+    int first[kStatsBatchMax], count[kStatsBatchMax];  // per target: its tensors in order[]
+    int order[kStatsBatchMax];                          // tensor indices grouped by target
+    int pbeg[kStatsBatchMax], pcnt[kStatsBatchMax];     // per tensor: its partials
+    int64_t numel[kStatsBatchMax];
+    double* nS[kStatsBatchMax];  // per target
+    float* lohi[kStatsBatchMax];
+};
+
+__global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(FinBatch F, const Partial* part) {
+    const int j = blockIdx.x;
+    double* nS = F.nS[j];
+    float* lohi = F.lohi[j];
     // the accumulator is read at the start so its latency overlaps the partial loads
     double acc[5] = {0.0, 0.0, 0.0, 0.0, 0.0};
     float alo = 0.0f, ahi = 0.0f;
@@ -92,32 +124,44 @@ __global__ __launch_bounds__(kStatsThreads) void stats_finalize_kernel(const Par
         alo = lohi[0];
         ahi = lohi[1];
     }
-    double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
-    float lo = INFINITY, hi = -INFINITY;
-#pragma unroll 4
-    for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {  // loads of 4 partials in flight
-        Partial p = part[i];
-        s1 += p.s1; s2 += p.s2; s3 += p.s3; s4 += p.s4;
-        lo = fminf(lo, p.lo); hi = fmaxf(hi, p.hi);
-    }
-    s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
-    lo = wave_min(lo); hi = wave_max(hi);
     __shared__ Partial wp[kStatsThreads / kWave];
-    if ((threadIdx.x & 63) == 0) wp[threadIdx.x >> 6] = Partial{s1, s2, s3, s4, lo, hi, 0.f, 0.f};
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        Partial r = wp[0];
-        for (int i = 1; i < kStatsThreads / kWave; ++i) {
-            r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
-            r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
+    for (int q = 0; q < F.count[j]; ++q) {
+        const int ti = F.order[F.first[j] + q];
+        const Partial* pt = part + F.pbeg[ti];
+        const int nparts = F.pcnt[ti];
+        double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
+        float lo = INFINITY, hi = -INFINITY;
+#pragma unroll 4
+        for (int i = threadIdx.x; i < nparts; i += kStatsThreads) {  // loads of 4 partials in flight
+            Partial p = pt[i];
+            s1 += p.s1; s2 += p.s2; s3 += p.s3; s4 += p.s4;
+            lo = fminf(lo, p.lo); hi = fmaxf(hi, p.hi);
         }
-        nS[0] = acc[0] + (double)numel;
-        nS[1] = acc[1] + r.s1;
-        nS[2] = acc[2] + r.s2;
-        nS[3] = acc[3] + r.s3;
-        nS[4] = acc[4] + r.s4;
-        lohi[0] = fminf(alo, r.lo);
-        lohi[1] = fmaxf(ahi, r.hi);
+        s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
+        lo = wave_min(lo); hi = wave_max(hi);
+        if ((threadIdx.x & 63) == 0) wp[threadIdx.x >> 6] = Partial{s1, s2, s3, s4, lo, hi, 0.f, 0.f};
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            Partial r = wp[0];
+            for (int i = 1; i < kStatsThreads / kWave; ++i) {
+                r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
+                r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
+            }
+            acc[0] = acc[0] + (double)F.numel[ti];
+            acc[1] = acc[1] + r.s1;
+            acc[2] = acc[2] + r.s2;
+            acc[3] = acc[3] + r.s3;
+            acc[4] = acc[4] + r.s4;
+            alo = fminf(alo, r.lo);
+            ahi = fmaxf(ahi, r.hi);
+        }
+        __syncthreads();  // wp is reused by the next tensor
+    }
+    if (threadIdx.x == 0) {
+#pragma unroll
+        for (int k = 0; k < 5; ++k) nS[k] = acc[k];
+        lohi[0] = alo;
+        lohi[1] = ahi;
     }
 }
 
@@ -245,22 +289,69 @@ static int stats_blocks(int64_t numel) {
 
 size_t cham_stats_workspace_bytes(int64_t numel) { return sizeof(Partial) * (size_t)stats_blocks(numel); }
 
-extern "C" int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t layer, int32_t bucket,
-                                         cham_act_stats* st, void* ws, size_t ws_bytes, void* stream) {
-    if (!X || !st || !st->nS || !st->lohi || numel < 1) return CHAM_EINVAL;
-    if (layer < 0 || layer >= st->L || bucket < 0 || bucket >= st->B) return CHAM_EINVAL;
-    if (((uintptr_t)X & 15u) != 0) return CHAM_EINVAL;
-    const int nb = stats_blocks(numel);
-    if (!ws || ws_bytes < sizeof(Partial) * (size_t)nb) return CHAM_EWORKSPACE;
+extern "C" int cham_act_stats_accumulate_batch(const float* const* X, const int64_t* numel, const int32_t* layer,
+                                               const int32_t* bucket, int32_t n, cham_act_stats* st, void* ws,
+                                               size_t ws_bytes, void* stream) {
+    if (!X || !numel || !layer || !bucket || n < 1 || !st || !st->nS || !st->lohi) return CHAM_EINVAL;
+    size_t parts = 0;
+    for (int i = 0; i < n; ++i) {
+        if (!X[i] || numel[i] < 1 || ((uintptr_t)X[i] & 15u) != 0) return CHAM_EINVAL;
+        if (layer[i] < 0 || layer[i] >= st->L || bucket[i] < 0 || bucket[i] >= st->B) return CHAM_EINVAL;
+        parts += (size_t)stats_blocks(numel[i]);
+    }
+    if (!ws || ws_bytes < sizeof(Partial) * parts) return CHAM_EWORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     Partial* part = (Partial*)ws;
-    hipLaunchKernelGGL(stats_partial_kernel, dim3(nb), dim3(kStatsThreads), 0, s, X, numel, part);
-    CHAM_CHECK_LAUNCH();
-    const int64_t i = (int64_t)layer * st->B + bucket;
-    hipLaunchKernelGGL(stats_finalize_kernel, dim3(1), dim3(kStatsThreads), 0, s, part, nb, numel, st->nS + 5 * i,
-                       st->lohi + 2 * i);
-    CHAM_CHECK_LAUNCH();
+    for (int i0 = 0; i0 < n; i0 += kStatsBatchMax) {  // launches in order: the accumulation order holds
+        const int m = std::min(kStatsBatchMax, n - i0);
+        StatsBatch B;
+        FinBatch F;
+        B.n = m;
+        F.ntgt = 0;
+        int blk = 0;
+        for (int q = 0; q < m; ++q) {
+            const int i = i0 + q;
+            const int nb = stats_blocks(numel[i]);
+            B.X[q] = X[i];
+            B.numel[q] = numel[i];
+            F.pbeg[q] = blk;
+            F.pcnt[q] = nb;
+            F.numel[q] = numel[i];
+            blk += nb;
+            B.blk_end[q] = blk;
+        }
+        // targets in order of first appearance, each with its tensors in batch order
+        int tgt_of[kStatsBatchMax];
+        for (int q = 0; q < m; ++q) {
+            const int64_t ti = (int64_t)layer[i0 + q] * st->B + bucket[i0 + q];
+            int j = 0;
+            while (j < F.ntgt && F.nS[j] != st->nS + 5 * ti) ++j;
+            if (j == F.ntgt) {
+                F.nS[j] = st->nS + 5 * ti;
+                F.lohi[j] = st->lohi + 2 * ti;
+                F.count[j] = 0;
+                ++F.ntgt;
+            }
+            tgt_of[q] = j;
+            ++F.count[j];
+        }
+        for (int j = 0, o = 0; j < F.ntgt; ++j) {
+            F.first[j] = o;
+            for (int q = 0; q < m; ++q)
+                if (tgt_of[q] == j) F.order[o++] = q;
+        }
+        hipLaunchKernelGGL(stats_partial_kernel, dim3(blk), dim3(kStatsThreads), 0, s, B, part);
+        CHAM_CHECK_LAUNCH();
+        hipLaunchKernelGGL(stats_finalize_kernel, dim3(F.ntgt), dim3(kStatsThreads), 0, s, F, part);
+        CHAM_CHECK_LAUNCH();
+        part += blk;
+    }
     return CHAM_OK;
+}
+
+extern "C" int cham_act_stats_accumulate(const float* X, int64_t numel, int32_t layer, int32_t bucket,
+                                         cham_act_stats* st, void* ws, size_t ws_bytes, void* stream) {
+    return cham_act_stats_accumulate_batch(&X, &numel, &layer, &bucket, 1, st, ws, ws_bytes, stream);
 }
 
 extern "C" void cham_schedule_default(cham_schedule* s) {

@@ -90,6 +90,14 @@ def test_other_argument_errors():
     assert L.cham_act_stats_accumulate(P(16), 100, 2, 0, ctypes.byref(st), P(256), 1 << 20, None) == cham.EINVAL
     assert L.cham_act_stats_accumulate(P(16), 100, 0, 3, ctypes.byref(st), P(256), 1 << 20, None) == cham.EINVAL
     assert L.cham_act_stats_accumulate(P(16), 1 << 20, 0, 0, ctypes.byref(st), None, 0, None) == cham.EWORKSPACE
+    xs = (ctypes.c_void_p * 2)(16, 16)
+    ne = (ctypes.c_int64 * 2)(100, 1 << 20)
+    ly = (ctypes.c_int32 * 2)(0, 1)
+    bk = (ctypes.c_int32 * 2)(0, 2)
+    bk_bad = (ctypes.c_int32 * 2)(0, 3)  # B = 3: bucket 3 is out of range
+    assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk_bad, 2, ctypes.byref(st), P(256), 1 << 30, None) == cham.EINVAL
+    assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk, 0, ctypes.byref(st), P(256), 1 << 30, None) == cham.EINVAL
+    assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk, 2, ctypes.byref(st), P(256), 64, None) == cham.EWORKSPACE
     aq = cham._AQ(4, 64, 0, P(16), P(16), P(16), P(16))
     assert L.cham_quantize_act(P(16), 7, 1, None, None, ctypes.byref(aq), P(256), 1 << 20, None) == cham.EFORMAT
     aq48 = cham._AQ(4, 48, 0, P(16), P(16), P(16), P(16))

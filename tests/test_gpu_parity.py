@@ -243,6 +243,33 @@ def test_stats_and_lut_match_oracle():
     assert np.array_equal(_np(lut2.F), F2) and np.array_equal(_np(lut2.S), S2) and np.array_equal(_np(lut2.Z), Z2)
 
 
+def test_stats_batch_matches_single_calls():
+    """The batched accumulate over 21 tensors (two launches' worth; ragged sizes; several
+    tensors of the same (layer, bucket), interleaved with others) gives the bits of one
+    call per tensor in array order, and matches the oracle."""
+    L, B = 3, 2
+    g = np.random.default_rng(7)
+    sizes = [int(v) for v in g.integers(1, 300_000, 21)] + [5, 2_000_003]
+    Xs = [g.standard_t(4, n).astype(np.float32) * (1 + i % 3) for i, n in enumerate(sizes)]
+    layers = [i % L for i in range(len(Xs))]
+    buckets = [(i // L) % B for i in range(len(Xs))]
+    sa, sb = cham.alloc_stats(L, B, DEV), cham.alloc_stats(L, B, DEV)
+    cham.act_stats_reset(sa)
+    cham.act_stats_reset(sb)
+    ost = oracle.Stats(L, B)
+    Xd = [torch.from_numpy(x).to(DEV) for x in Xs]
+    case(f"act_stats_accumulate_batch {len(Xs)} tensors")
+    cham.act_stats_accumulate_batch(Xd, layers, buckets, sa)
+    for x, xd, l, b in zip(Xs, Xd, layers, buckets):
+        cham.act_stats_accumulate(xd, l, b, sb)
+        ost.accumulate(x, l, b)
+    torch.cuda.synchronize()
+    assert np.array_equal(_np(sa.nS), _np(sb.nS))
+    assert np.array_equal(_np(sa.lohi), _np(sb.lohi))
+    assert np.allclose(_np(sa.nS), ost.nS, rtol=1e-12, atol=0)
+    assert np.array_equal(_np(sa.lohi), ost.lohi)
+
+
 def test_stats_ragged_and_tiny():
     for n in (1, 3, 5, 1023, 4097, 1_000_003):
         x = np.random.default_rng(n).standard_t(4, n).astype(np.float32)
