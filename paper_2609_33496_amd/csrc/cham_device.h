@@ -42,6 +42,23 @@ CHAM_DEV int mx_exponent(float a, int emax) {
     return e < -127 ? -127 : (e > 127 ? 127 : e);
 }
 
+// The same from fl = floor_log2(a) computed once for several emax (fl is ignored when the
+// block is all zero); branch-free.
+CHAM_DEV int mx_exponent_fl(int fl, bool nonzero, int emax) {
+    const int e = fl - emax;
+    return nonzero ? (e < -127 ? -127 : (e > 127 ? 127 : e)) : -127;
+}
+
+// Correctly rounded 1/a for a >= FLT_MIN: the hardware estimate refined by one
+// Newton-Raphson step with a fused multiply-add (Markstein's reciprocal iteration).  It
+// equals the IEEE quotient 1/a for every binary32 a in [2^-126, 2^126) (checked
+// exhaustively on gfx950); larger a, whose reciprocal is subnormal, take the division.
+CHAM_DEV float rcp_rn(float a) {
+    if (a >= 0x1p126f) return 1.0f / a;
+    const float r0 = __builtin_amdgcn_rcpf(a);
+    return __builtin_fmaf(__builtin_fmaf(-a, r0, 1.0f), r0, r0);
+}
+
 // ------------------------------------------------------------------------------------
 // E2M1 (FP4): magnitudes {0, .5, 1, 1.5, 2, 3, 4, 6}; round to nearest, ties to the even
 // code.  Adding 2^22 / 2^23 / 2^24 rounds to the format's step (0.5 below 2, 1 in [2, 4),

@@ -154,7 +154,7 @@ CHAM_DEV uint32_t quant_one(float w, const RowParams& p, float blk32, float blk6
     }
     case CHAM_W_NF4: {
         float a = floor_scale(blk64);
-        float y = w * (1.0f / a);
+        float y = w * rcp_rn(a);
         const NF4Cell cl = nf4_cell(cells, y);
         const bool up = y > cl.thr;
         *wh = (up ? cl.vhi : cl.vlo) * a;
@@ -197,8 +197,10 @@ CHAM_DEV v2f fp4_pair(float a, float b, float scale) {
     return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, scale, 0);
 }
 
+// e0 / e2: the chunk's MX block exponent for emax 0 (MXINT) and 2 (MXFP4)
 template <int F>
-CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, float blk64, const NF4Cell* cells) {
+CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, float blk64, const NF4Cell* cells,
+                         int e0, int e2) {
     float e = 0.0f;
     if (F == CHAM_W_INT8_ASYM || F == CHAM_W_INT4_ASYM) {
         const float r = F == CHAM_W_INT8_ASYM ? p.r_as8 : p.r_as4;
@@ -231,7 +233,7 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
             e = __builtin_fmaf(d1, d1, e);
         }
     } else if (F == CHAM_W_MXFP4) {
-        const float sc = e8m0_scale(mx_exponent(blk32, 2));
+        const float sc = e8m0_scale(e2);
 #pragma unroll
         for (int j = 0; j < 4; j += 2) {
             const v2f v = fp4_pair(w[j], w[j + 1], sc);
@@ -243,7 +245,7 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
         // in the block's scaled domain: y = w 2^(F-E) exactly, d = y - k exactly
         const int Fb = F == CHAM_W_MXINT8 ? 6 : 2;
         const float Q = F == CHAM_W_MXINT8 ? 127.0f : 7.0f;
-        const int E = mx_exponent(blk32, 0);
+        const int E = e0;
         float es = 0.0f;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -255,7 +257,7 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
         e = ldexpf(es, 2 * (E - Fb));
     } else {  // NF4
         const float a = floor_scale(blk64);
-        const float r = 1.0f / a;
+        const float r = rcp_rn(a);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const float y = w[j] * r;
@@ -272,7 +274,7 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
 // each code, so a channel that chooses NF4 needs no second quantization pass.
 CHAM_DEV float chunk_err_nf4(const float (&w)[4], float blk64, const NF4Cell* cells, int code_bits, uint32_t& cw) {
     const float a = floor_scale(blk64);
-    const float r = 1.0f / a;
+    const float r = rcp_rn(a);
     float e = 0.0f;
     cw = 0u;
 #pragma unroll
@@ -415,15 +417,19 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!valid[c]) continue;
-        if (mask & (1u << 0)) e[0] += chunk_err<0>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 1)) e[1] += chunk_err<1>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 2)) e[2] += chunk_err<2>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 3)) e[3] += chunk_err<3>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 4)) e[4] += chunk_err<4>(v[c], p, b32[c], b64[c], cells);
+        // the block exponent of both MX emax values from one floor(log2 amax)
+        const bool nz32 = b32[c] > 0.0f;
+        const int fl32 = floor_log2(nz32 ? b32[c] : 1.0f);
+        const int e0 = mx_exponent_fl(fl32, nz32, 0), e2 = mx_exponent_fl(fl32, nz32, 2);
+        if (mask & (1u << 0)) e[0] += chunk_err<0>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 1)) e[1] += chunk_err<1>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 2)) e[2] += chunk_err<2>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 3)) e[3] += chunk_err<3>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 4)) e[4] += chunk_err<4>(v[c], p, b32[c], b64[c], cells, e0, e2);
         if (mask & (1u << 5)) e[5] += chunk_err_nf4(v[c], b64[c], cells, a.code_bits, nf4cw[c]);
-        if (mask & (1u << 6)) e[6] += chunk_err<6>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 7)) e[7] += chunk_err<7>(v[c], p, b32[c], b64[c], cells);
-        if (mask & (1u << 8)) e[8] += chunk_err<8>(v[c], p, b32[c], b64[c], cells);
+        if (mask & (1u << 6)) e[6] += chunk_err<6>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 7)) e[7] += chunk_err<7>(v[c], p, b32[c], b64[c], cells, e0, e2);
+        if (mask & (1u << 8)) e[8] += chunk_err<8>(v[c], p, b32[c], b64[c], cells, e0, e2);
     }
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) {
