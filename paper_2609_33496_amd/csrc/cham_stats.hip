@@ -16,7 +16,8 @@ namespace cham {
 namespace {
 
 constexpr int kStatsThreads = 256;
-constexpr int kStatsMaxBlocks = 2048;
+constexpr int kStatsMaxBlocks = 1024;
+constexpr int kStatsLoads = 8;  // 16-byte loads in flight per thread
 
 struct Partial {
     double s1, s2, s3, s4;
@@ -60,20 +61,23 @@ __global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(StatsBatch
             hi = fmaxf(hi, e[j]);
         }
     };
-    // four loads in flight per thread, then their sums in index order
+    // kStatsLoads loads in flight per thread, then their sums in index order
     int64_t i = (int64_t)lb * blockDim.x + threadIdx.x;
-    for (; i + 3 * stride < nq; i += 4 * stride) {
-        const float4 t0 = X4[i], t1 = X4[i + stride], t2 = X4[i + 2 * stride], t3 = X4[i + 3 * stride];
-        add(t0); add(t1); add(t2); add(t3);
+    for (; i + (kStatsLoads - 1) * stride < nq; i += kStatsLoads * stride) {
+        float4 t[kStatsLoads];
+#pragma unroll
+        for (int q = 0; q < kStatsLoads; ++q) t[q] = X4[i + q * stride];
+#pragma unroll
+        for (int q = 0; q < kStatsLoads; ++q) add(t[q]);
     }
-    // the last up to three: all loads issued first, then the sums in index order
+    // the last few: all loads issued first, then the sums in index order
     {
-        const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-        const bool v0 = i < nq, v1 = i + stride < nq, v2 = i + 2 * stride < nq;
-        const float4 t0 = v0 ? X4[i] : z, t1 = v1 ? X4[i + stride] : z, t2 = v2 ? X4[i + 2 * stride] : z;
-        if (v0) add(t0);
-        if (v1) add(t1);
-        if (v2) add(t2);
+        float4 t[kStatsLoads - 1];
+#pragma unroll
+        for (int q = 0; q < kStatsLoads - 1; ++q) t[q] = i + q * stride < nq ? X4[i + q * stride] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int q = 0; q < kStatsLoads - 1; ++q)
+            if (i + q * stride < nq) add(t[q]);
     }
     // scalar tail (numel % 4), handled by the first threads of the tensor's workgroup 0
     if (lb == 0 && threadIdx.x < (numel & 3)) {
@@ -197,7 +201,7 @@ constexpr int kLutThreads = 256;
 constexpr int kLutMaxBuckets = 1024;
 
 __global__ __launch_bounds__(kLutThreads) void lut_kernel(LutArgs a) {
-    __shared__ double red[kLutThreads];
+    __shared__ double red[kLutThreads / kWave];
     __shared__ double snr_ws[kLutMaxBuckets];
     for (int b = 0; b < a.B; ++b) {
         const int tb = (int)(((int64_t)(2 * b + 1) * a.T) / (2LL * a.B));
@@ -213,14 +217,12 @@ __global__ __launch_bounds__(kLutThreads) void lut_kernel(LutArgs a) {
             }
             prod *= (1.0 - beta);
         }
-        red[threadIdx.x] = prod;
+        // product tree: within each wavefront by shuffles, then the wavefronts' products
+        for (int o = 32; o > 0; o >>= 1) prod *= __shfl_xor(prod, o, kWave);
+        if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = prod;
         __syncthreads();
-        for (int o = kLutThreads / 2; o > 0; o >>= 1) {
-            if ((int)threadIdx.x < o) red[threadIdx.x] *= red[threadIdx.x + o];
-            __syncthreads();
-        }
         if (threadIdx.x == 0) {
-            const double ab = red[0];
+            const double ab = (red[0] * red[1]) * (red[2] * red[3]);
             snr_ws[b] = ab / (1.0 - ab);
         }
         __syncthreads();
@@ -281,7 +283,7 @@ extern "C" int cham_act_stats_reset(cham_act_stats* st, void* stream) {
 
 static int stats_blocks(int64_t numel) {
     int64_t nq = numel >> 2;
-    int64_t b = (nq + kStatsThreads * 2 - 1) / (kStatsThreads * 2);  // >= 2 float4 per thread
+    int64_t b = (nq + kStatsThreads * kStatsLoads - 1) / (kStatsThreads * kStatsLoads);  // >= 8 float4 per thread
     if (b < 1) b = 1;
     if (b > kStatsMaxBlocks) b = kStatsMaxBlocks;
     return (int)b;
