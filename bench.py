@@ -10,6 +10,10 @@ One step = one pass of every step of the path over one batch, all inputs residen
   select_weight_formats_batch (the 4 layers, one call, also writing each layer's packed GEMM
   layout) -> act_stats_accumulate_batch (the 4 layer inputs, one call) ->
   build_act_lut -> quantize_act_lut (4) -> mixed_linear (4).
+The weight side and the activation side are independent until the GEMMs: the search runs on
+a second stream (default priority) while the statistics, LUT and quantization run on the
+launch stream, which waits for the search before the GEMMs; the next step's search waits
+for this step's GEMMs (they read the packed weights it rewrites).
 
 Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step time (GEMM
 flops / step time; the search, statistics, LUT and quantization count against it).  The
@@ -100,6 +104,8 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
     S = ctypes.c_void_p(stream.cuda_stream)
+    side = torch.cuda.Stream(device=dev)  # the weight search of each step (default priority)
+    S_side = ctypes.c_void_p(side.cuda_stream)
 
     layers = synth.sdxl_block_layers(D)
     # ---- inputs (synthetic, resident in HBM before timing)
@@ -150,18 +156,23 @@ def main():
     P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
 
     ev = {k: [] for k in ("search", "gemm")}
+    prev_end = [None]  # event: the previous step's GEMMs are done (or the timing start)
 
     def step(record=False):
         e0 = e1 = None
+        # weight side, on the second stream: after the previous step's GEMMs
+        if prev_end[0] is not None:
+            side.wait_event(prev_end[0])
         if record:
             e0 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, len(layers), S)
+            e0.record(side)
+        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, len(layers), S_side)
         assert rc == 0, rc
+        searched = torch.cuda.Event(enable_timing=record)
+        searched.record(side)
         if record:
-            e1 = torch.cuda.Event(enable_timing=True)
-            e1.record(stream)
-            ev["search"].append((e0, e1))
+            ev["search"].append((e0, searched))
+        # activation side, on the launch stream
         rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, len(layers),
                                                ctypes.byref(st_s), P(tbatch.ws), tbatch.ws_bytes, S)
         assert rc == 0, rc
@@ -171,6 +182,7 @@ def main():
             rc = L.cham_quantize_act_lut(P(Xs[li]), ctypes.byref(lut_s), Fh, li, args.t, 0, ctypes.byref(aq_s[li]),
                                          P(ws_q[li]), ws_q[li].numel(), S)
             assert rc == 0, rc
+        stream.wait_event(searched)
         if record:
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
@@ -178,10 +190,11 @@ def main():
             rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin[li]),
                                      ws_lin[li].numel(), S)
             assert rc == 0, rc
+        end = torch.cuda.Event(enable_timing=record)
+        end.record(stream)
+        prev_end[0] = end
         if record:
-            e3 = torch.cuda.Event(enable_timing=True)
-            e3.record(stream)
-            ev["gemm"].append((e2, e3))
+            ev["gemm"].append((e2, end))
 
     for _ in range(args.warmup):
         step()
@@ -189,6 +202,7 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
+    prev_end[0] = t0  # the first timed search starts after the timing start
     for _ in range(args.steps):
         step(record=True)
     t1.record(stream)
