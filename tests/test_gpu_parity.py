@@ -490,3 +490,66 @@ def test_linear_plans_sampled(M, N, K, mask, afmt):
     yr, bm = oracle.linear_pairs(xh, Wh, mm, nn)
     err = np.abs(Y[mm, nn] - yr)
     assert np.all(err <= 1e-3 * bm), (err / bm).max()
+
+
+# ---------------------------------------------------------------------------------------
+# the benchmark's two-stream step
+def test_two_streams_match_one_stream():
+    """The weight search on a second stream, concurrent with the activation statistics, LUT
+    and quantization on the launch stream (which waits for it before the GEMMs; the next
+    search waits for those GEMMs), gives the bits of the same calls on one stream."""
+    layers = [("a", 640, 384), ("b", 1280, 256), ("c", 2560, 320)]
+    M, T, B, t = 300, 1000, 4, 375
+    Ws = [torch.from_numpy(synth.hetero_weights(50 + i, N, K)[0]).to(DEV) for i, (_, K, N) in enumerate(layers)]
+    Xs = [torch.from_numpy(synth.diffusion_acts(3, i, t, M, K)).to(DEV) for i, (_, K, _) in enumerate(layers)]
+    sched = cham.Schedule(T=T)
+    b = cham.bucket(t, T, B)
+
+    def alloc():
+        wqs = [cham.alloc_wq(N, K, cham.MASK_W4, DEV, want_perm=True, want_packed=True) for (_, K, N) in layers]
+        for w in wqs:
+            w.packed.zero_()
+        st = cham.alloc_stats(len(layers), B, DEV)
+        aqs = [cham.alloc_aq(M, K, DEV) for (_, K, _) in layers]
+        Ys = [torch.empty((M, N), dtype=torch.float32, device=DEV) for (_, _, N) in layers]
+        return wqs, st, aqs, Ys
+
+    def run(wqs, st, aqs, Ys, side, main):
+        sb = cham.SearchBatch(Ws, wqs)
+        cham.act_stats_reset(st, stream=main)
+        end = None
+        for _ in range(2):  # two steps: the second search waits for the first step's GEMMs
+            if end is not None:
+                side.wait_event(end)
+            sb.run(stream=side)
+            searched = torch.cuda.Event()
+            searched.record(side)
+            cham.act_stats_accumulate_batch(Xs, list(range(len(layers))), [b] * len(layers), st, stream=main)
+            lut = cham.build_act_lut(st, sched, stream=main)
+            lut.mirror()  # a copy on the launch stream (the current one in both runs)
+            main.wait_event(searched)
+            for i in range(len(layers)):
+                cham.quantize_act_lut(Xs[i], lut, i, t, out=aqs[i], stream=main)
+                cham.mixed_linear(aqs[i], wqs[i], Ys[i], stream=main)
+            end = torch.cuda.Event()
+            end.record(main)
+        torch.cuda.synchronize()
+
+    cur = torch.cuda.current_stream()
+    case("one stream")
+    ref = alloc()
+    torch.cuda.synchronize()
+    run(*ref, cur, cur)
+    case("two streams")
+    two = alloc()
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    run(*two, side, cur)
+    for wa, wb in zip(ref[0], two[0]):
+        assert np.array_equal(_np(wa.fmt), _np(wb.fmt))
+        assert np.array_equal(_np(wa.codes), _np(wb.codes))
+        assert np.array_equal(_np(wa.perm), _np(wb.perm))
+        assert np.array_equal(_np(wa.packed), _np(wb.packed))
+    assert np.array_equal(_np(ref[1].nS), _np(two[1].nS))
+    for ya, yb in zip(ref[3], two[3]):
+        assert np.array_equal(_np(ya).view(np.uint32), _np(yb).view(np.uint32))
