@@ -5,12 +5,13 @@
 // weights are dequantized on the fly into a common half-precision operand.  Every 4-bit
 // code of every format is an entry of a 16-value decode table per (k-step of 64, channel,
 // half k-step of 32): base value (NF4 level, E2M1 value, integer, q - z) times the block
-// factor (NF4 block absmax, MX 2^E) relative to the channel's largest block, rounded once
-// to half precision.  A pre-pass packs, per (k-step, channel, half), the codes and this
-// table (two byte planes) into one record; the main kernel decodes with v_perm_b32, so
-// every 4-bit format decodes with the same instructions.  Integers, E2M1 values and MX
-// mantissas are exact in half precision; NF4 levels times their block absmax carry one
-// rounding (relative error <= 2^-11).  8-bit integer formats are decoded arithmetically
+// factor (NF4 block absmax, MX 2^E) relative to the channel's largest block, rounded to
+// binary32 and then to half precision.  A pre-pass packs, per (k-step, channel, half), the
+// codes and this table (two byte planes) into one record (layout in cham_records.h); the
+// main kernel decodes with v_perm_b32, so every 4-bit format decodes with the same
+// instructions.  Integers, E2M1 values and MX mantissas are exact in half precision; NF4
+// levels times their block absmax carry the two roundings (relative error <= 2^-11 +
+// 2^-24).  8-bit integer formats are decoded arithmetically
 // (1024 + c trick, exact) with parameters from the same table slot.
 //
 // Activations in a per-tensor format (INT8, E4M3, E5M2) are decoded to half precision
@@ -36,30 +37,18 @@
 // staged with its columns in that same order.
 #include "cham_device.h"
 #include "cham_group.h"
+#include "cham_records.h"
 
 namespace cham {
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
 constexpr int BN = 256, BK = 64;
 constexpr int kThreads = 256;
 constexpr int TN = 2;                     // 32-channel MFMA blocks per wavefront
 constexpr int kBufferFlags = 0x00020000;  // buffer descriptor word 3: 32-bit data, raw
-
-CHAM_DEV bool is_mx(int f) { return f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4; }
-CHAM_DEV bool is_8bit(int f) { return f == CHAM_W_INT8_SYM || f == CHAM_W_INT8_ASYM || f == CHAM_W_MXINT8; }
-CHAM_DEV int mx_F(int f) { return f == CHAM_W_MXINT8 ? 6 : (f == CHAM_W_MXINT4 ? 2 : 0); }
-
-// Per-channel parameters, computed by the pre-pass for every output channel.
-struct ColPrep {
-    int fmt;         // CHAM_W_NFMT: not a valid format of the palette (decodes as zero)
-    int eref;        // exponent removed from block-scaled values (NF4 / MX), 0 otherwise
-    float zero;      // INT-asym zero point
-    float colscale;  // epilogue factor: INT/FP4 scale, or 2^eref
-};
 
 // ------------------------------------------------------------------------------------
 // pre-pass for MX activation formats: codes -> half precision relative to the row's
@@ -114,60 +103,6 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
         *reinterpret_cast<half8*>(out + 8 * g) = h;
     }
     if (threadIdx.x == 0) p.rowscale[m] = ldexpf(1.0f, eref);
-}
-
-// ------------------------------------------------------------------------------------
-// pre-pass 2: weight records, one per (k-step, channel, half k-step): the half's codes
-// (16 bytes at 4 bits, 32 at 8 bits) followed by its 32-byte decode table
-// ------------------------------------------------------------------------------------
-
-// 16-entry half-precision table as byte planes: lo[j] holds the low bytes of entries
-// 4j..4j+3, hi[j] the high bytes.  8-bit integer formats use the same 32 bytes for
-// {xor mask, -(1024 + zero offset) and the block factor as half pairs}.
-struct Table {
-    uint32_t lo[4], hi[4];
-};
-
-CHAM_DEV float e2m1_value(int c) {
-    const float m[8] = {0.0f, 0.5f, 1.0f, 1.5f, 2.0f, 3.0f, 4.0f, 6.0f};
-    return (c & 8) ? -m[c & 7] : m[c & 7];
-}
-
-template <int F>
-CHAM_DEV Table table_fmt(float zero, float factor) {
-    Table t;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int c = 4 * j + e;
-            float b;
-            if (F == CHAM_W_NF4) b = nf4_level(c);
-            else if (F == CHAM_W_FP4 || F == CHAM_W_MXFP4) b = e2m1_value(c);
-            else if (F == CHAM_W_INT4_ASYM) b = (float)c - zero;
-            else b = (float)(c < 8 ? c : c - 16);  // INT4-sym, MXINT4
-            v[e] = b * factor;
-        }
-        half2v a01, a23;
-        a01.x = (_Float16)v[0]; a01.y = (_Float16)v[1];
-        a23.x = (_Float16)v[2]; a23.y = (_Float16)v[3];
-        const uint32_t w01 = __builtin_bit_cast(uint32_t, a01), w23 = __builtin_bit_cast(uint32_t, a23);
-        t.lo[j] = __builtin_amdgcn_perm(w23, w01, 0x06040200u);
-        t.hi[j] = __builtin_amdgcn_perm(w23, w01, 0x07050301u);
-    }
-    return t;
-}
-
-CHAM_DEV uint32_t half_pair(float v) {
-    half2v p;
-    p.x = (_Float16)v;
-    p.y = p.x;
-    return __builtin_bit_cast(uint32_t, p);
-}
-
-CHAM_DEV Table int8_record(uint32_t xmask, float zoff, float factor) {
-    return Table{{xmask, half_pair(-(1024.0f + zoff)), half_pair(factor), 0u}, {0u, 0u, 0u, 0u}};
 }
 
 // ------------------------------------------------------------------------------------
@@ -237,6 +172,10 @@ CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
     return r.h;
 }
 
+// ------------------------------------------------------------------------------------
+// pre-pass 2: weight records (layout in cham_records.h), one per (k-step, channel, half
+// k-step): the half's codes (16 bytes at 4 bits, 32 at 8 bits), then its decode table
+// ------------------------------------------------------------------------------------
 struct RecArgs {
     const uint8_t* wfmt;
     const float* wscale;
@@ -260,29 +199,6 @@ struct RecArgs {
 // passes' loads are in flight together.
 constexpr int kRecChannels = 32;
 constexpr int kRecPrefetch = 4;
-
-CHAM_DEV Table record_table(const ColPrep& c, float nf4a, int e8) {
-    Table tb;
-    switch (c.fmt) {
-    case CHAM_W_NF4: tb = table_fmt<CHAM_W_NF4>(0.0f, ldexpf(nf4a, -c.eref)); break;
-    case CHAM_W_MXFP4:
-    case CHAM_W_MXINT4:
-    case CHAM_W_MXINT8: {
-        const float factor = ldexpf(1.0f, e8 - 127 - mx_F(c.fmt) - c.eref);
-        if (c.fmt == CHAM_W_MXFP4) tb = table_fmt<CHAM_W_MXFP4>(0.0f, factor);
-        else if (c.fmt == CHAM_W_MXINT4) tb = table_fmt<CHAM_W_MXINT4>(0.0f, factor);
-        else tb = int8_record(0x80808080u, 128.0f, factor);
-        break;
-    }
-    case CHAM_W_FP4: tb = table_fmt<CHAM_W_FP4>(0.0f, 1.0f); break;
-    case CHAM_W_INT4_ASYM: tb = table_fmt<CHAM_W_INT4_ASYM>(c.zero, 1.0f); break;
-    case CHAM_W_INT4_SYM: tb = table_fmt<CHAM_W_INT4_SYM>(0.0f, 1.0f); break;
-    case CHAM_W_INT8_SYM: tb = int8_record(0x80808080u, 128.0f, 1.0f); break;
-    case CHAM_W_INT8_ASYM: tb = int8_record(0u, c.zero, 1.0f); break;
-    default: tb = Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}}; break;
-    }
-    return tb;
-}
 
 // Several weights' records in one launch: the workgroups of the batch's layers follow
 // each other (descriptors in the kernel arguments); before them, one workgroup per entry
