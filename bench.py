@@ -50,6 +50,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--t", type=int, default=375, help="timestep of the benchmarked batch")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-dense-reference", action="store_true",
+                   help="skip timing the library's dense f16 GEMM on the same shapes (a point of comparison)")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="before timing, copy a buffer of this many MiB once (a kernel of known HBM traffic "
@@ -249,9 +251,35 @@ def main():
                      "kernel": "mixed_linear (gemm_kernel, k-split reduce_kernel; the weights' decode layout comes packed from the search); achieved = 2MNK summed over the "
                                "4 calls / their HIP-event time; traffic = HBM bytes per call"},
     }
+    if not args.no_dense_reference:
+        out["dense_f16_reference"] = dense_reference(layers, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, Ws, Xs, fmts, args.cpu_budget_s)
     print(json.dumps(out), flush=True)
+
+
+def dense_reference(layers, stream, reps=20):
+    """For comparison only (not part of the path): the library's dense f16 GEMM (torch.matmul,
+    f16 inputs and output, no per-channel decode) on the same shapes, timed after the
+    benchmark with HIP events; TFLOP/s per layer."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(0)
+    res = {}
+    for (name, K, N) in layers:
+        a = torch.randn(M_TOKENS, K, dtype=torch.float16, device="cuda", generator=g)
+        b = torch.randn(K, N, dtype=torch.float16, device="cuda", generator=g)  # contiguous [K, N]
+        for _ in range(3):
+            torch.matmul(a, b)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            torch.matmul(a, b)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res[name] = round(2.0 * M_TOKENS * N * K / (ms * 1e-3) / 1e12, 1)
+    return {"tflops": res, "unit": "TFLOP/s",
+            "what": "torch.matmul f16 x f16 -> f16 (library GEMM), same M, N, K; no decode, 2-byte output"}
 
 
 def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
