@@ -22,6 +22,10 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
          "-Wno-unused-command-line-argument", "-I", os.path.join(ROOT, "include")]
 
+# The weight search takes finite weights only: without NaNs the compiler no longer quiets
+# each min/max operand first (a canonicalizing max per operand in the statistics).
+EXTRA_FLAGS = {"cham_search.hip": ["-fno-honor-nans"]}
+
 
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
@@ -32,7 +36,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     objs, procs = [], []
     for src in sources():
         obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-        cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+        cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))

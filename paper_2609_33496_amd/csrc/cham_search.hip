@@ -49,9 +49,11 @@ struct RowParams {
 // ------------------------------------------------------------------------------------
 // DPP reductions
 // ------------------------------------------------------------------------------------
+// Every control used here reads a lane of the same wavefront row, so no lane is invalid and
+// bound_ctrl is free to set: it lets the compiler fold the move into the consuming min/max/add.
 template <int CTRL>
 CHAM_DEV float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 // max over the aligned 8-lane group (quad_perm 1,0,3,2; quad_perm 2,3,0,1; row_half_mirror)
 CHAM_DEV float max8(float v) {
@@ -112,10 +114,9 @@ CHAM_DEV void nf4_cells_init(NF4Cell* cells) {
     }
 }
 
+// y = w fl(1/a) with |w| <= a, so |y| <= 1 + 2^-23: 16 y + 16 truncates to 0 .. 32.
 CHAM_DEV NF4Cell nf4_cell(const NF4Cell* cells, float y) {
-    int i = (int)__builtin_fmaf(y, 16.0f, 16.0f);  // y in [-1, 1] -> [0, 32]
-    i = i < 0 ? 0 : (i > 32 ? 32 : i);
-    return cells[i];
+    return cells[(int)__builtin_fmaf(y, 16.0f, 16.0f)];
 }
 
 // ------------------------------------------------------------------------------------
@@ -191,10 +192,14 @@ typedef float v2f __attribute__((ext_vector_type(2)));
 // 2^E as the binary32 scale operand of the FP4 converters (they read its exponent field)
 CHAM_DEV float e8m0_scale(int E) { return __uint_as_float((uint32_t)(E + 127) << 23); }
 
-// E2M1 round trip of a pair through the hardware converter with a power-of-two scale.
-CHAM_DEV v2f fp4_pair(float a, float b, float scale) {
-    const uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, a, b, scale, 0);
-    return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, scale, 0);
+// E2M1 round trip of four values through the hardware converter with a power-of-two scale:
+// the two pairs' codes go to bytes 0 and 1 of one register.  `old` is any value that is
+// dead after the call (the converter only replaces the selected byte).
+CHAM_DEV void fp4_quad(float y0, float y1, float y2, float y3, float scale, uint32_t old, v2f& lo, v2f& hi) {
+    uint32_t c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, y0, y1, scale, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, y2, y3, scale, 1);
+    lo = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, scale, 0);
+    hi = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(c, scale, 1);
 }
 
 // e0 / e2: the chunk's MX block exponent for emax 0 (MXINT) and 2 (MXFP4)
@@ -225,21 +230,22 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
             e = __builtin_fmaf(d, d, e);
         }
     } else if (F == CHAM_W_FP4) {
+        const float y0 = w[0] * p.r_fp4;
+        v2f v[2];
+        fp4_quad(y0, w[1] * p.r_fp4, w[2] * p.r_fp4, w[3] * p.r_fp4, 1.0f, __float_as_uint(y0), v[0], v[1]);
 #pragma unroll
-        for (int j = 0; j < 4; j += 2) {
-            const v2f v = fp4_pair(w[j] * p.r_fp4, w[j + 1] * p.r_fp4, 1.0f);
-            const float d0 = w[j] - v.x * p.s_fp4, d1 = w[j + 1] - v.y * p.s_fp4;
-            e = __builtin_fmaf(d0, d0, e);
-            e = __builtin_fmaf(d1, d1, e);
+        for (int j = 0; j < 4; ++j) {
+            const float d = w[j] - v[j >> 1][j & 1] * p.s_fp4;
+            e = __builtin_fmaf(d, d, e);
         }
     } else if (F == CHAM_W_MXFP4) {
         const float sc = e8m0_scale(e2);
+        v2f v[2];
+        fp4_quad(w[0], w[1], w[2], w[3], sc, 0u, v[0], v[1]);
 #pragma unroll
-        for (int j = 0; j < 4; j += 2) {
-            const v2f v = fp4_pair(w[j], w[j + 1], sc);
-            const float d0 = w[j] - v.x, d1 = w[j + 1] - v.y;
-            e = __builtin_fmaf(d0, d0, e);
-            e = __builtin_fmaf(d1, d1, e);
+        for (int j = 0; j < 4; ++j) {
+            const float d = w[j] - v[j >> 1][j & 1];
+            e = __builtin_fmaf(d, d, e);
         }
     } else if (F == CHAM_W_MXINT4 || F == CHAM_W_MXINT8) {
         // in the block's scaled domain: y = w 2^(F-E) exactly, d = y - k exactly
@@ -417,9 +423,10 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!valid[c]) continue;
-        // the block exponent of both MX emax values from one floor(log2 amax)
+        // the block exponent of both MX emax values from one floor(log2 amax): the exponent
+        // of frexp (mantissa in [1/2, 1)) less one, subnormal blocks included
         const bool nz32 = b32[c] > 0.0f;
-        const int fl32 = floor_log2(nz32 ? b32[c] : 1.0f);
+        const int fl32 = __builtin_amdgcn_frexp_expf(b32[c]) - 1;
         const int e0 = mx_exponent_fl(fl32, nz32, 0), e2 = mx_exponent_fl(fl32, nz32, 2);
         if (mask & (1u << 0)) e[0] += chunk_err<0>(v[c], p, b32[c], b64[c], cells, e0, e2);
         if (mask & (1u << 1)) e[1] += chunk_err<1>(v[c], p, b32[c], b64[c], cells, e0, e2);
