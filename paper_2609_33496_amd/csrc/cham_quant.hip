@@ -2,7 +2,8 @@
 // scales; ScaleZP) to the five activation formats of Sec. 4.2.
 //
 // HBM-bound elementwise pass: float4 loads, one packed 32-bit store of four codes per
-// thread.  MX formats: a 32-element block is 8 consecutive lanes; its amax comes from a
+// float4; each thread issues its kQLoads loads (a workgroup's consecutive float4 runs)
+// before it converts any of them, so they are in flight together.  MX formats: a 32-element block is 8 consecutive lanes; its amax comes from a
 // shuffle reduction and one lane writes the E8M0 byte.  Dynamic mode first reduces
 // min/max into per-workgroup partials (workspace); the quantize kernel folds them (min
 // and max are exact, so the result does not depend on the order).
@@ -13,16 +14,29 @@ namespace {
 
 constexpr int kQThreads = 256;
 constexpr int kQMaxBlocks = 1024;
+constexpr int kQLoads = 4;  // float4 loads in flight per thread
+
+// float4 index of load u of the thread's run starting at i0 (workgroup-strided)
+CHAM_DEV int64_t qidx(int64_t i0, int u) { return i0 + (int64_t)u * kQThreads; }
+CHAM_DEV int64_t qfirst() { return (int64_t)blockIdx.x * kQThreads * kQLoads + threadIdx.x; }
+CHAM_DEV int64_t qstep() { return (int64_t)gridDim.x * kQThreads * kQLoads; }
 
 __global__ __launch_bounds__(kQThreads) void minmax_partial_kernel(const float* X, int64_t n, float2* part) {
     float lo = INFINITY, hi = -INFINITY;
     const int64_t nq = n >> 2;
     const float4* X4 = reinterpret_cast<const float4*>(X);
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
-        float4 t = X4[i];
-        lo = fminf(fminf(lo, t.x), fminf(fminf(t.y, t.z), t.w));
-        hi = fmaxf(fmaxf(hi, t.x), fmaxf(fmaxf(t.y, t.z), t.w));
+    for (int64_t i0 = qfirst(); i0 < nq; i0 += qstep()) {
+        float4 t[kQLoads];
+#pragma unroll
+        for (int u = 0; u < kQLoads; ++u) {
+            const int64_t i = qidx(i0, u);
+            t[u] = X4[i < nq ? i : i0];  // past the end: a repeat of the first (i0 < nq)
+        }
+#pragma unroll
+        for (int u = 0; u < kQLoads; ++u) {
+            lo = fminf(fminf(lo, t[u].x), fminf(fminf(t[u].y, t[u].z), t[u].w));
+            hi = fmaxf(fmaxf(hi, t[u].x), fmaxf(fmaxf(t[u].y, t[u].z), t[u].w));
+        }
     }
     lo = wave_min(lo);
     hi = wave_max(hi);
@@ -99,24 +113,32 @@ __global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
     const int64_t nq = a.n >> 2;
     const float4* X4 = reinterpret_cast<const float4*>(a.X);
     uint32_t* C4 = reinterpret_cast<uint32_t*>(a.codes);
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nq; i += stride) {
-        float4 t = X4[i];
-        float e[4] = {t.x, t.y, t.z, t.w};
-        uint32_t w = 0;
+    for (int64_t i0 = qfirst(); i0 < nq; i0 += qstep()) {
+        float4 t[kQLoads];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            uint32_t c;
-            if (FMT == CHAM_A_INT8_ASYM) {
-                c = (uint32_t)clampf(rne(e[j] * r) + z, 0.0f, 255.0f);
-            } else if (FMT == CHAM_A_FP8_E4M3) {
-                c = e4m3_encode(clampf(e[j] * r, -448.0f, 448.0f));
-            } else {
-                c = e5m2_encode(clampf(e[j] * r, -57344.0f, 57344.0f));
-            }
-            w |= c << (8 * j);
+        for (int u = 0; u < kQLoads; ++u) {
+            const int64_t i = qidx(i0, u);
+            t[u] = i < nq ? X4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        C4[i] = w;
+#pragma unroll
+        for (int u = 0; u < kQLoads; ++u) {
+            const float e[4] = {t[u].x, t[u].y, t[u].z, t[u].w};
+            uint32_t w = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                uint32_t c;
+                if (FMT == CHAM_A_INT8_ASYM) {
+                    c = (uint32_t)clampf(rne(e[j] * r) + z, 0.0f, 255.0f);
+                } else if (FMT == CHAM_A_FP8_E4M3) {
+                    c = e4m3_encode(clampf(e[j] * r, -448.0f, 448.0f));
+                } else {
+                    c = e5m2_encode(clampf(e[j] * r, -57344.0f, 57344.0f));
+                }
+                w |= c << (8 * j);
+            }
+            const int64_t i = qidx(i0, u);
+            if (i < nq) C4[i] = w;
+        }
     }
 }
 
@@ -129,37 +151,45 @@ __global__ __launch_bounds__(kQThreads) void quant_mx_kernel(const float* X, int
     const int64_t nq = n >> 2;  // multiple of 8
     const float4* X4 = reinterpret_cast<const float4*>(X);
     uint32_t* C4 = reinterpret_cast<uint32_t*>(codes);
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    const int64_t iters = (nq + stride - 1) / stride;
+    // the same trip count for every lane: the 8-lane reductions run with whole wavefronts
+    const int64_t iters = (nq + qstep() - 1) / qstep();
     for (int64_t it = 0; it < iters; ++it) {
-        const int64_t i = it * stride + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-        const bool ok = i < nq;  // whole 8-lane groups are in or out together
-        float4 t = ok ? X4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-        float e[4] = {t.x, t.y, t.z, t.w};
-        float m = fmaxf(fmaxf(fabsf(e[0]), fabsf(e[1])), fmaxf(fabsf(e[2]), fabsf(e[3])));
-        m = group_max<8>(m);
-        const int E = mx_exponent(m, 0);
-        uint32_t w = 0;
+        const int64_t i0 = qfirst() + it * qstep();
+        float4 t[kQLoads];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            uint32_t c;
-            if (FMT == CHAM_A_MXFP8_E4M3) {
-                c = e4m3_encode(clampf(ldexpf(e[j], -E), -448.0f, 448.0f));
-            } else {
-                float k = clampf(rne(ldexpf(e[j], 6 - E)), -127.0f, 127.0f);
-                c = (uint32_t)(int)k & 0xFFu;
-            }
-            w |= c << (8 * j);
+        for (int u = 0; u < kQLoads; ++u) {
+            const int64_t i = qidx(i0, u);
+            t[u] = i < nq ? X4[i] : make_float4(0.f, 0.f, 0.f, 0.f);  // whole 8-lane groups are in or out
         }
-        if (ok) {
-            C4[i] = w;
-            if ((threadIdx.x & 7) == 0) e8[i >> 3] = (uint8_t)(E + 127);
+#pragma unroll
+        for (int u = 0; u < kQLoads; ++u) {
+            const float e[4] = {t[u].x, t[u].y, t[u].z, t[u].w};
+            float m = fmaxf(fmaxf(fabsf(e[0]), fabsf(e[1])), fmaxf(fabsf(e[2]), fabsf(e[3])));
+            m = group_max<8>(m);
+            const int E = mx_exponent(m, 0);
+            uint32_t w = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                uint32_t c;
+                if (FMT == CHAM_A_MXFP8_E4M3) {
+                    c = e4m3_encode(clampf(ldexpf(e[j], -E), -448.0f, 448.0f));
+                } else {
+                    float k = clampf(rne(ldexpf(e[j], 6 - E)), -127.0f, 127.0f);
+                    c = (uint32_t)(int)k & 0xFFu;
+                }
+                w |= c << (8 * j);
+            }
+            const int64_t i = qidx(i0, u);
+            if (i < nq) {
+                C4[i] = w;
+                if ((threadIdx.x & 7) == 0) e8[i >> 3] = (uint8_t)(E + 127);
+            }
         }
     }
 }
 
 int qblocks(int64_t nq) {
-    int64_t b = (nq + kQThreads * 4 - 1) / (kQThreads * 4);
+    int64_t b = (nq + kQThreads * kQLoads - 1) / (kQThreads * kQLoads);
     if (b < 1) b = 1;
     if (b > kQMaxBlocks) b = kQMaxBlocks;
     return (int)b;
