@@ -45,9 +45,10 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
-constexpr int BN = 256, BK = 64;
+constexpr int BK = 64;
 constexpr int kThreads = 256;
-constexpr int TN = 2;                     // 32-channel MFMA blocks per wavefront
+// TN = 32-channel MFMA blocks per wavefront: a tile is 128 TN channels wide (four wavefronts)
+constexpr int tile_width(int TN) { return 128 * TN; }
 constexpr int kBufferFlags = 0x00020000;  // buffer descriptor word 3: 32-bit data, raw
 
 // ------------------------------------------------------------------------------------
@@ -380,9 +381,10 @@ CHAM_DEV uint4 decode_act8(uint32_t w0, uint32_t w1, bool perm4, half2v negz) {
     return make_uint4(d[0], d[1], d[2], d[3]);
 }
 
-template <int CODE_BITS, int TM, int AF>
-__global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void gemm_kernel(GemmArgs a) {
+template <int CODE_BITS, int TM, int AF, int TN>
+__global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 2 : 1) void gemm_kernel(GemmArgs a) {
     constexpr int BM = 32 * TM;
+    constexpr int BN = tile_width(TN);
     constexpr int CW = CODE_BITS / 4;  // 16-byte code pieces per record
     constexpr int P = CW + 2;          // 16-byte pieces per record (codes + two table planes)
     constexpr int AQ = AF == kAF16 ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
@@ -452,10 +454,10 @@ __global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void g
         }
     };
 
-    // ---- weight records of the lane's channels (column l32 of the wave's two 32-channel
+    // ---- weight records of the lane's channels (column l32 of the wave's TN 32-channel
     // blocks, half h): global -> registers one k-step ahead; past the last channel the
     // range check returns zeros (zero codes, zero table)
-    const int nl = 64 * wave + l32;
+    const int nl = 32 * TN * wave + l32;
     const int chans = N - n0 < BN ? N - n0 : BN;
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(a.rec + ((int64_t)kb * N + n0) * 2 * P), (short)0, (int)(((int64_t)(K / BK - kb) * N - n0) * 2 * P * 16),
@@ -483,7 +485,7 @@ __global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void g
         }
     };
 
-    // per-channel parameters of the lane's two channels: 8-bit code layout decoded
+    // per-channel parameters of the lane's TN channels: 8-bit code layout decoded
     // arithmetically, epilogue factor (loaded here, off the tail of the kernel)
     bool int8[TN];
     float cs[TN];
@@ -617,10 +619,18 @@ __global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void g
         for (int j = 0; j < TN; ++j) {
             const int n = n0 + nl + 32 * j;
             float* base = out + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
-            if (full) {
+            if (full && a.splits > 1) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = (acc[i][j][r] * rs[r]) * cs[j];
+            } else if (full) {
+                // the output is not read again here: non-temporal stores keep the L2 for the
+                // operand tiles other workgroups still read (partials, read back by the
+                // reduction, take ordinary stores)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    __builtin_nontemporal_store((acc[i][j][r] * rs[r]) * cs[j],
+                                                &base[(int64_t)(8 * (r >> 2) + (r & 3)) * N]);
             } else if (n < N) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -634,6 +644,9 @@ __global__ __launch_bounds__(kThreads, TM == 4 && CODE_BITS == 4 ? 2 : 1) void g
 
 // Sum of the k-split partial outputs in split order (the result does not depend on the
 // order in which workgroups ran); 4 outputs per thread when M N is a multiple of 4.
+constexpr int kMaxSplits = 8;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ part, float* __restrict__ Y,
                                                      int64_t MN, int splits) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -642,12 +655,18 @@ __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ p
         float4* y4 = reinterpret_cast<float4*>(Y);
         const int64_t n4 = MN >> 2;
         for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-            float4 acc = p4[i];
-            for (int sp = 1; sp < splits; ++sp) {
-                const float4 v = p4[(int64_t)sp * n4 + i];
-                acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+            // every split's load issued before the first sum (splits <= kMaxSplits)
+            float4 v[kMaxSplits];
+#pragma unroll
+            for (int sp = 0; sp < kMaxSplits; ++sp)
+                v[sp] = sp < splits ? p4[(int64_t)sp * n4 + i] : make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 acc = v[0];
+#pragma unroll
+            for (int sp = 1; sp < kMaxSplits; ++sp) {
+                if (sp < splits) { acc.x += v[sp].x; acc.y += v[sp].y; acc.z += v[sp].z; acc.w += v[sp].w; }
             }
-            y4[i] = acc;
+            const f32x4 o = {acc.x, acc.y, acc.z, acc.w};
+            __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(&y4[i]));
         }
     } else {
         for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < MN; i += stride) {
@@ -675,25 +694,30 @@ int cu_count() {
     return cached[dev];
 }
 
-// Modeled time (us) of a launch of one tile height: per-step and fixed (prologue, output
-// write) cost of a workgroup, measured on MI355X for these kernels.  Tile height 128 with
-// 4-bit codes fits two workgroups on a CU; each then runs at the slower shared-CU step cost.
+// Modeled time (us) of a launch of one tile shape, fitted to measurements on MI355X: one
+// fixed cost (prologue, output write) per launch -- the workgroups of later rounds start
+// while earlier ones finish -- plus the k-steps of the rounds of workgroups.  Tiles 128 high
+// fit two workgroups on a CU; a round that shares the CUs runs at the slower shared step.
+// The half-width tile (128 x 128) is for layers whose full-width tiles cannot fill the CUs.
 struct TileCost {
-    int bm, occ;
-    double step1, step2, fixed;  // us: step alone on the CU, step sharing it, fixed
+    int bm, tn, occ;             // tile height, 32-channel blocks per wavefront, workgroups per CU
+    double step1, step2, fixed;  // us: k-step alone on the CU, k-step sharing it, per launch
 };
-constexpr TileCost kTileCosts[3] = {{256, 1, 1.75, 1.75, 14.0}, {128, 2, 1.12, 1.35, 9.0}, {64, 1, 0.78, 0.78, 6.0}};
+constexpr int kNumTiles = 4;
+constexpr TileCost kTileCosts[kNumTiles] = {{256, 2, 1, 2.13, 2.13, 8.0},
+                                            {128, 2, 2, 1.21, 1.89, 9.0},
+                                            {128, 1, 2, 0.715, 1.26, 6.0},
+                                            {64, 2, 1, 0.82, 0.82, 6.2}};
 
 double launch_cost(int64_t wgs, int nsteps, const TileCost& c, int P) {
     if (wgs <= 0) return 0.0;
     const int64_t slots = (int64_t)c.occ * P;
     const int64_t full = wgs / slots, rem = wgs % slots;
-    const double t_alone = nsteps * c.step1 + c.fixed, t_shared = nsteps * c.step2 + c.fixed;
-    return full * t_shared + (rem == 0 ? 0.0 : (rem <= P ? t_alone : t_shared));
+    return c.fixed + (double)full * nsteps * c.step2 + (rem == 0 ? 0.0 : nsteps * (rem <= P ? c.step1 : c.step2));
 }
 
 struct Launch {
-    int row0, row1, bm;
+    int row0, row1, bm, tn;
 };
 struct Plan {
     int n;       // launches
@@ -701,39 +725,52 @@ struct Plan {
     Launch l[2];
 };
 // k-split reduction: one extra launch reading the partials and writing the output
-// (modeled at 5 TB/s)
+// (measured ≈ 7 TB/s: the partials come back from the last-level cache in part)
 double reduce_cost(int64_t M, int64_t N, int splits) {
-    return splits > 1 ? 3.0 + (double)(splits + 1) * (double)(M * N * 4) / 5.0e6 : 0.0;
+    return splits > 1 ? 2.0 + (double)(splits + 1) * (double)(M * N * 4) / 7.0e6 : 0.0;
 }
-constexpr int kMaxSplits = 8;
+
+int col_tiles(int N, int tn) { return (N + tile_width(tn) - 1) / tile_width(tn); }
 
 Plan plan_gemm(int M, int N, int K, int code_bits) {
     const int P = cu_count();
-    const int tn = (N + BN - 1) / BN, nsteps = K / BK;
-    TileCost costs[3] = {kTileCosts[0], kTileCosts[1], kTileCosts[2]};
-    if (code_bits != 4) costs[1].occ = 1;
+    const int nsteps = K / BK;
+    TileCost costs[kNumTiles];
+    for (int b = 0; b < kNumTiles; ++b) costs[b] = kTileCosts[b];
+    if (code_bits != 4) {  // the full-width 128-high tile with 8-bit codes: one per CU
+        costs[1].occ = 1;
+        costs[1].step2 = costs[1].step1;
+    }
+    // half-width tiles only where the full-width ones leave CUs idle
+    const bool narrow = (int64_t)((M + 127) / 128) * col_tiles(N, 2) < P;
     double best = 1e300;
-    Plan plan{1, 1, {Launch{0, M, 64}, Launch{0, 0, 0}}};
-    for (int b = 0; b < 3; ++b) {
+    Plan plan{1, 1, {Launch{0, M, 64, 2}, Launch{0, 0, 0, 0}}};
+    for (int b = 0; b < kNumTiles; ++b) {
+        if (costs[b].tn == 1 && !narrow) continue;
+        const int tn = col_tiles(N, costs[b].tn);
         for (int sp = 1; sp <= kMaxSplits && sp <= nsteps; ++sp) {
             const int kchunk = (nsteps + sp - 1) / sp;
             if (sp > 1 && (sp - 1) * kchunk >= nsteps) continue;  // an empty split
             const int64_t tiles = (int64_t)((M + costs[b].bm - 1) / costs[b].bm) * tn;
             const double c = launch_cost(tiles * sp, kchunk, costs[b], P) + reduce_cost(M, N, sp);
-            if (c < best) { best = c; plan = Plan{1, sp, {Launch{0, M, costs[b].bm}, Launch{0, 0, 0}}}; }
+            if (c < best) { best = c; plan = Plan{1, sp, {Launch{0, M, costs[b].bm, costs[b].tn}, Launch{0, 0, 0, 0}}}; }
         }
     }
-    // larger tiles for whole rounds of full tile rows, then smaller tiles for the rest
-    for (int b = 0; b < 2; ++b) {
+    // one tile shape for whole rounds of full tile rows, another for the rows left
+    for (int b = 0; b < kNumTiles; ++b) {
+        if (costs[b].tn == 1 && !narrow) continue;
         const TileCost& c1 = costs[b];
-        const int rows_per_round = (c1.occ * P / tn) * c1.bm;
+        const int tn1 = col_tiles(N, c1.tn);
+        const int rows_per_round = (c1.occ * P / tn1) * c1.bm;
         if (rows_per_round <= 0) continue;
         const int r1 = (M / rows_per_round) * rows_per_round;
         if (r1 <= 0 || r1 >= M) continue;
-        for (int b2 = b + 1; b2 < 3; ++b2) {
-            const double c = launch_cost((int64_t)(r1 / c1.bm) * tn, nsteps, c1, P) +
-                             launch_cost((int64_t)((M - r1 + costs[b2].bm - 1) / costs[b2].bm) * tn, nsteps, costs[b2], P);
-            if (c < best) { best = c; plan = Plan{2, 1, {Launch{0, r1, c1.bm}, Launch{r1, M, costs[b2].bm}}}; }
+        for (int b2 = 0; b2 < kNumTiles; ++b2) {
+            if (b2 == b || (costs[b2].tn == 1 && !narrow)) continue;
+            const TileCost& c2 = costs[b2];
+            const double c = launch_cost((int64_t)(r1 / c1.bm) * tn1, nsteps, c1, P) +
+                             launch_cost((int64_t)((M - r1 + c2.bm - 1) / c2.bm) * col_tiles(N, c2.tn), nsteps, c2, P);
+            if (c < best) { best = c; plan = Plan{2, 1, {Launch{0, r1, c1.bm, c1.tn}, Launch{r1, M, c2.bm, c2.tn}}}; }
         }
     }
     return plan;
@@ -752,15 +789,18 @@ size_t split_bytes(int64_t M, int64_t N, int64_t K) {
 template <int CODE_BITS, int AF>
 void launch_gemm_af(const GemmArgs& a, const Launch& l, hipStream_t s) {
     const unsigned grid = (unsigned)(((l.row1 - l.row0 + l.bm - 1) / l.bm) * a.tn * a.splits);
-    if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8, AF>), dim3(grid), dim3(kThreads), 0, s, a);
-    else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4, AF>), dim3(grid), dim3(kThreads), 0, s, a);
-    else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2, AF>), dim3(grid), dim3(kThreads), 0, s, a);
+    if (l.bm == 256) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 8, AF, 2>), dim3(grid), dim3(kThreads), 0, s, a);
+    else if (l.bm == 128 && l.tn == 1)
+        hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4, AF, 1>), dim3(grid), dim3(kThreads), 0, s, a);
+    else if (l.bm == 128) hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 4, AF, 2>), dim3(grid), dim3(kThreads), 0, s, a);
+    else hipLaunchKernelGGL((gemm_kernel<CODE_BITS, 2, AF, 2>), dim3(grid), dim3(kThreads), 0, s, a);
 }
 
 template <int CODE_BITS>
 void launch_gemm(GemmArgs a, const Launch& l, int af, hipStream_t s) {
     a.row0 = l.row0;
     a.row1 = l.row1;
+    a.tn = col_tiles(a.N, l.tn);
     switch (af) {
     case kAInt8: launch_gemm_af<CODE_BITS, kAInt8>(a, l, s); break;
     case kAE4M3: launch_gemm_af<CODE_BITS, kAE4M3>(a, l, s); break;
@@ -909,7 +949,6 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     a.K = K;
     a.row0 = 0;
     a.row1 = M;
-    a.tn = (N + BN - 1) / BN;
     a.part = part;
     const int af = amx ? kAF16
                        : (xq->fmt == CHAM_A_INT8_ASYM ? kAInt8 : (xq->fmt == CHAM_A_FP8_E4M3 ? kAE4M3 : kAE5M2));
