@@ -458,10 +458,12 @@ def test_linear_full_size_sampled():
 
 @pytest.mark.parametrize("M,N,K,mask,afmt", [
     (1500, 3000, 2560, oracle.MASK_W4, cham.A_FP8_E5M2),   # 128-row tiles, 3 k-splits, ragged M
-    (1500, 3000, 2560, oracle.MASK_W8, cham.A_INT8_ASYM),  # 8-bit codes, 128-row tiles
+    (1500, 3000, 2560, oracle.MASK_W8, cham.A_INT8_ASYM),  # 8-bit codes, 256-row tiles, 3 k-splits
     (3000, 4000, 1280, oracle.MASK_W8, cham.A_MXFP8),      # 8-bit codes, 256-row tiles, MX activations
     (3000, 4000, 1280, oracle.MASK_W4, cham.A_MXINT8),     # 128-row tiles, MX activations
-    (2048, 10240, 1280, oracle.MASK_W8, cham.A_FP8_E4M3),  # two launches: 256-row then 128-row tiles
+    (8192, 4608, 1152, oracle.MASK_W8, cham.A_FP8_E4M3),   # two launches: 256-row then 128-row tiles
+    (1000, 1000, 1280, oracle.MASK_W4, cham.A_FP8_E4M3),   # half-width tiles, 4 k-splits, ragged M and N
+    (700, 777, 1280, oracle.MASK_W8, cham.A_INT8_ASYM),    # half-width tiles, 8-bit codes, 5 k-splits
 ])
 def test_linear_plans_sampled(M, N, K, mask, afmt):
     """Tile heights, k-splits and two-launch plans the sizes above select (each code width,
