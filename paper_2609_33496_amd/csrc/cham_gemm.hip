@@ -199,7 +199,7 @@ struct RecArgs {
 // thread's first kRecPrefetch records are loaded before the ColPrep pass, so both
 // passes' loads are in flight together.
 constexpr int kRecChannels = 32;
-constexpr int kRecPrefetch = 4;
+constexpr int kRecPrefetch = 3;
 
 // Several weights' records in one launch: the workgroups of the batch's layers follow
 // each other (descriptors in the kernel arguments); before them, one workgroup per entry
@@ -830,9 +830,10 @@ static RecArgs record_args(const cham_wq* wq, ColPrep* cols, uint4* rec, int* wg
     const int N = (int)wq->N, K = (int)wq->K;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
-    // enough workgroups to fill the chip, at least 4 k-steps each
+    // about one workgroup per CU per layer (all of a batch resident at once), at least 4
+    // k-steps each
     const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
-    const int nkc = std::max(1, std::min((512 + nblk - 1) / nblk, (nst + 3) / 4));
+    const int nkc = std::max(1, std::min((256 + nblk - 1) / nblk, (nst + 3) / 4));
     const int rchunk = (nst + nkc - 1) / nkc;
     *wgs = nblk * ((nst + rchunk - 1) / rchunk);
     // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
