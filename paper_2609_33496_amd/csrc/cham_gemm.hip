@@ -18,9 +18,10 @@
 // while they are staged into LDS (exact); MX activations are decoded by a pre-pass into a
 // half-precision copy relative to the row's largest block exponent, with a row scale.
 //
-// Main kernel: BM x 256 output tiles (BM = 256, 128 or 64), k-steps of 64, four
-// wavefronts that each own BM rows x 64 channels (BM/32 x 2 blocks of
-// v_mfma_f32_32x32x16_f16, binary32 accumulation), so a decoded weight feeds BM/16 MFMAs.
+// Main kernel: BM x 256 output tiles (BM = 256, 128 or 64), or 128 x 128 for layers whose
+// full-width tiles leave CUs idle; k-steps of 64; four wavefronts that each own BM rows x
+// 32 TN channels (BM/32 x TN blocks of v_mfma_f32_32x32x16_f16, binary32 accumulation), so
+// a decoded weight feeds BM/32 MFMAs per k sub-step.
 // Activation tiles and weight records go global -> registers with coalesced 16-byte
 // buffer loads one or more k-steps ahead (deeper register rings for the short steps of
 // small tiles); the activation tile is stored into one of two LDS buffers with its
@@ -677,11 +678,11 @@ __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ p
     }
 }
 
-// ---- launch plan.  A launch covers rows [row0, row1) with one tile height.  The plan is
+// ---- launch plan.  A launch covers rows [row0, row1) with one tile shape.  The plan is
 // either one launch, optionally split along k into partial outputs that reduce_kernel
 // sums (for layers with too few output tiles to fill the CUs), or two launches of
-// different tile heights: the larger for whole rounds of workgroups, the smaller for the
-// rows left, so the last round does not leave most CUs idle.
+// different tile shapes: one for whole rounds of workgroups, the other for the rows left,
+// so the last round does not leave most CUs idle.
 int cu_count() {
     static int cached[64] = {0};
     int dev = 0;
