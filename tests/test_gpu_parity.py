@@ -129,6 +129,37 @@ def test_search_full_size_sampled():
         assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(counts)]))
 
 
+@pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8])
+def test_search_pixart_block_sampled(mask):
+    """One PixArt-like DiT block (QKV 1152->3456, proj 1152->1152, MLP 1152->4608->1152,
+    cross-attn KV 4096->1152) searched in one batched call, at W4 and at W8 {INT8, MXINT8}:
+    sampled channels of every layer against the oracle (formats, codes, metadata), and the
+    grouping of each layer's own format vector."""
+    layers = synth.pixart_block_layers()
+    Ws = [synth.hetero_weights(70 + i, N, K)[0] for i, (_, K, N, _) in enumerate(layers)]
+    case(f"select_weight_formats_batch PixArt-like block mask={mask:#x}")
+    outs = cham.select_weight_formats_batch([torch.from_numpy(W).to(DEV) for W in Ws], mask)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(mask)
+    for (name, K, N, _), W, wq in zip(layers, Ws, outs):
+        rows = np.sort(g.choice(N, 96, replace=False))
+        ref = oracle.select_weight_formats(W[rows], mask)
+        f = _np(wq.fmt)
+        assert np.array_equal(f[rows], ref["fmt"]), name
+        assert np.array_equal(_np(wq.codes)[rows], ref["codes"]), name
+        assert np.array_equal(_np(wq.scale)[rows], ref["scale"]), name
+        assert np.array_equal(_np(wq.zero)[rows], ref["zero"]), name
+        for meta in ("nf4_absmax", "e8m0"):  # a palette without the kind allocates no buffer
+            buf = getattr(wq, meta)
+            if buf is None:
+                assert not np.any(ref[meta]), (name, meta)
+            else:
+                assert np.array_equal(_np(buf)[rows], ref[meta]), (name, meta)
+        assert np.array_equal(_np(wq.perm), np.argsort(f, kind="stable")), name
+        counts = np.bincount(f, minlength=9)
+        assert np.array_equal(_np(wq.group_off), np.concatenate([[0], np.cumsum(counts)])), name
+
+
 def test_search_batch_matches_single_calls():
     """The batched search over 19 layers of mixed shapes, kernel variants and palettes (more
     layers than one launch takes) equals one call per layer, bit for bit."""
@@ -464,6 +495,9 @@ def test_linear_full_size_sampled():
     (8192, 4608, 1152, oracle.MASK_W8, cham.A_FP8_E4M3),   # two launches: 256-row then 128-row tiles
     (1000, 1000, 1280, oracle.MASK_W4, cham.A_FP8_E4M3),   # half-width tiles, 4 k-splits, ragged M and N
     (700, 777, 1280, oracle.MASK_W8, cham.A_INT8_ASYM),    # half-width tiles, 8-bit codes, 5 k-splits
+    (240, 1152, 4096, oracle.MASK_W4, cham.A_FP8_E4M3),    # PixArt-like cross-attn KV: 240 rows, 8 k-splits
+    (4096, 5120, 640, oracle.MASK_W4, cham.A_INT8_ASYM),   # 640-wide GEGLU at 4096 tokens
+    (1024, 1280, 5120, oracle.MASK_W4, cham.A_FP8_E5M2),   # 1280-wide FF-out at 1024 tokens
 ])
 def test_linear_plans_sampled(M, N, K, mask, afmt):
     """Tile heights, k-splits and two-launch plans the sizes above select (each code width,
