@@ -53,6 +53,8 @@ def parse():
     p.add_argument("--no-dense-reference", action="store_true",
                    help="skip timing the library's dense f16 GEMM on the same shapes (a point of comparison)")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--layer-steps", type=int, default=10,
+                   help="untimed steps after the timed ones for the per-layer GEMM breakdown (0: none)")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="before timing, copy a buffer of this many MiB once (a kernel of known HBM traffic "
                         "for scaling hardware byte counters)")
@@ -157,10 +159,10 @@ def main():
     Fh = ctypes.c_void_p(lut.F_host.data_ptr())
     P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
 
-    ev = {k: [] for k in ("search", "gemm")}
+    ev = {k: [] for k in ("search", "gemm", "layer")}
     prev_end = [None]  # event: the previous step's GEMMs are done (or the timing start)
 
-    def step(record=False):
+    def step(record=False, per_layer_events=False):
         e0 = e1 = None
         # weight side, on the second stream: after the previous step's GEMMs
         if prev_end[0] is not None:
@@ -188,14 +190,21 @@ def main():
         if record:
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
+        marks = [e2] if record else []
         for li in range(len(layers)):
             rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin[li]),
                                      ws_lin[li].numel(), S)
             assert rc == 0, rc
+            if per_layer_events and li + 1 < len(layers):
+                marks.append(torch.cuda.Event(enable_timing=True))
+                marks[-1].record(stream)
         end = torch.cuda.Event(enable_timing=record)
         end.record(stream)
         prev_end[0] = end
-        if record:
+        if per_layer_events:
+            marks.append(end)
+            ev["layer"].append(list(zip(marks[:-1], marks[1:])))
+        elif record:
             ev["gemm"].append((e2, end))
 
     for _ in range(args.warmup):
@@ -213,6 +222,22 @@ def main():
     ms_step = ms_total / args.steps
     ms_search = float(np.mean([a.elapsed_time(b) for a, b in ev["search"]]))
     ms_gemm = float(np.mean([a.elapsed_time(b) for a, b in ev["gemm"]]))
+    # per-layer breakdown from extra steps after the timed region: an event between calls
+    # adds a launch gap (≈ 2–3 µs each), so the timed steps carry only the two around the GEMMs
+    for _ in range(args.layer_steps):
+        step(record=True, per_layer_events=True)
+    torch.cuda.synchronize()
+    # per layer: HIP-event time of its call (launch gap to the previous call included), and
+    # its roofline time max(flops / f16 MFMA peak, algorithmic bytes / HBM peak), the bytes
+    # being activation codes, 4-bit weight codes and the binary32 output
+    per_layer = {}
+    for li, (name, K, N) in enumerate(layers if args.layer_steps > 0 else []):
+        us = float(np.mean([a.elapsed_time(b) for a, b in (st[li] for st in ev["layer"])])) * 1e3
+        fl = 2.0 * M_TOKENS * N * K
+        by = M_TOKENS * K + N * K / 2 + 4.0 * M_TOKENS * N
+        t_roof = max(fl / (F16_PEAK_TFLOPS * 1e6), by / (HBM_PEAK_GBPS * 1e3))
+        per_layer[name] = {"us": round(us, 2), "tflops": round(fl / us / 1e6, 1), "t_roof_us": round(t_roof, 2),
+                           "frac_t_roof": round(t_roof / us, 4)}
 
     flops = sum(2.0 * M_TOKENS * N * K for (_, K, N) in layers)
     sbytes = sum(N * K * search_bytes_per_weight(K) for (_, K, N) in layers)
@@ -248,6 +273,10 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4),
                      "traffic": committed_traffic(),
+                     "per_layer": {"layers": per_layer,
+                                   "what": f"{args.layer_steps} untimed steps after the timed ones with an event between "
+                                           "the GEMM calls (each adds a launch gap of about 2-3 us); t_roof = max("
+                                           "2MNK / f16 MFMA peak, (MK + NK/2 + 4MN) bytes / HBM peak)"},
                      "kernel": "mixed_linear (gemm_kernel, k-split reduce_kernel; the weights' decode layout comes packed from the search); achieved = 2MNK summed over the "
                                "4 calls / their HIP-event time; traffic = HBM bytes per call"},
     }
