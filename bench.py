@@ -19,7 +19,10 @@ Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step tim
 flops / step time; the search, statistics, LUT and quantization count against it).  The
 `roofline` object is for the dominant kernel (the mixed-format GEMM), timed with HIP events
 on the launch stream over the timed steps; the weight search's own HBM rate is reported
-beside it.  `cpu_baseline` times the CPU oracle on a bounded sample of the same step.
+beside it.  `roofline.per_layer` breaks the GEMM time down by layer, from untimed steps run
+after the timed ones with an event between the calls (--layer-steps; each such event adds a
+launch gap, so the timed steps carry none).  `cpu_baseline` times the CPU oracle on a
+bounded sample of the same step.
 """
 from __future__ import annotations
 
