@@ -18,7 +18,8 @@
  * Conventions shared by every call:
  *   - Every pointer inside a descriptor or passed as a buffer is DEVICE memory unless its
  *     comment says "host".  The caller owns every buffer; the library allocates nothing and
- *     keeps no mutable global state.  Calls are thread-safe.
+ *     keeps no mutable global state beyond a per-device cache of the CU count (filled once,
+ *     atomically).  Calls are thread-safe.
  *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only enqueues work
  *     on that stream and returns without synchronizing.
  *   - Argument errors are detected on the host and returned synchronously before anything is

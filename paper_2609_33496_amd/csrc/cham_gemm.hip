@@ -36,6 +36,8 @@
 // k-step takes k = 32h .. 32h+31, sub-step s the 8 k at 32h + 8s, and with two codes per
 // byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation operand is
 // staged with its columns in that same order.
+#include <atomic>
+
 #include "cham_device.h"
 #include "cham_group.h"
 #include "cham_records.h"
@@ -683,16 +685,18 @@ __global__ __launch_bounds__(256) void reduce_kernel(const float* __restrict__ p
 // sums (for layers with too few output tiles to fill the CUs), or two launches of
 // different tile shapes: one for whole rounds of workgroups, the other for the rows left,
 // so the last round does not leave most CUs idle.
+// CU count of the current device, queried once per device (every thread that races to
+// fill the cache stores the same value, so relaxed atomics suffice)
 int cu_count() {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int n = 0;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-        cached[dev] = n;
+        cached[dev].store(n, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return n;
 }
 
 // Modeled time (us) of a launch of one tile shape, fitted to measurements on MI355X: one
