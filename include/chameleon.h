@@ -267,6 +267,14 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
 int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* The launch plan cham_mixed_linear takes for M x N x K with 4- or 8-bit weight codes
+ * (diagnostics; host only, launches nothing).  out (host, out_len >= 10 int32) receives
+ * {launches (1 or 2), k-splits, then per launch: first row, end row, tile rows, tile
+ * channels}; entries of an absent second launch are 0.  The plan depends on the current
+ * device's CU count (256 when no device is visible).  Errors: CHAM_EINVAL (NULL out,
+ * out_len < 10, sizes < 1, code_bits not 4 or 8). */
+int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bits, int32_t* out, int32_t out_len);
+
 /* ---------------------------------------------------------------------------------------
  * workspace sizes
  * ------------------------------------------------------------------------------------- */

@@ -98,9 +98,11 @@ def lib():
     L.cham_workspace_bytes.restype = sz
     L.cham_packed_bytes.argtypes = [i64, i64]
     L.cham_packed_bytes.restype = sz
+    L.cham_linear_plan.argtypes = [i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32), i32]
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
-                 "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear"):
+                 "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear",
+                 "cham_linear_plan"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
@@ -138,6 +140,15 @@ def _dev_tensor(t: torch.Tensor, dtype, name):
 
 def workspace_bytes(op: int, M: int, N: int, K: int) -> int:
     return int(lib().cham_workspace_bytes(op, M, N, K))
+
+
+def linear_plan(M: int, N: int, K: int, code_bits: int) -> dict:
+    """The launch plan mixed_linear takes for these sizes (host only)."""
+    out = (ctypes.c_int32 * 10)()
+    _check(lib().cham_linear_plan(M, N, K, code_bits, out, 10), "cham_linear_plan")
+    launches = [{"rows": (out[2 + 4 * i], out[3 + 4 * i]), "tile": (out[4 + 4 * i], out[5 + 4 * i])}
+                for i in range(out[0])]
+    return {"splits": out[1], "launches": launches}
 
 
 def _workspace(op, M, N, K, device, ws):

@@ -885,6 +885,23 @@ size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
            align256((size_t)record_bytes(N, K)) + split_bytes(M, N, K);
 }
 
+extern "C" int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bits, int32_t* out, int32_t out_len) {
+    if (!out || out_len < 10 || M < 1 || N < 1 || K < 1 || M > INT32_MAX || N > INT32_MAX || K > INT32_MAX ||
+        (code_bits != 4 && code_bits != 8))
+        return CHAM_EINVAL;
+    const Plan p = plan_gemm((int)M, (int)N, (int)K, code_bits);
+    for (int i = 0; i < 10; ++i) out[i] = 0;
+    out[0] = p.n;
+    out[1] = p.splits;
+    for (int i = 0; i < p.n; ++i) {
+        out[2 + 4 * i] = p.l[i].row0;
+        out[3 + 4 * i] = p.l[i].row1;
+        out[4 + 4 * i] = p.l[i].bm;
+        out[5 + 4 * i] = tile_width(p.l[i].tn);
+    }
+    return CHAM_OK;
+}
+
 extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
                                  void* stream) {
     if (!xq || !wq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;

@@ -121,3 +121,33 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cham, "_lib", None)
     with pytest.raises(RuntimeError):
         cham.lib()
+
+
+def test_linear_plans_are_valid():
+    """The GEMM planner on the host (no GPU: 256 CUs assumed): for a grid of shapes the
+    launches tile the rows in order with shapes the kernels exist for, every k-split holds
+    at least one k-step, only single launches split k, and the workspace the library asks
+    for holds the split partial outputs."""
+    for M in (1, 7, 64, 240, 1000, 2048, 4096, 8192):
+        for N in (32, 640, 777, 1280, 3840, 10240):
+            for K in (64, 640, 1280, 5120):
+                for bits in (4, 8):
+                    p = cham.linear_plan(M, N, K, bits)
+                    ls = p["launches"]
+                    assert 1 <= len(ls) <= 2, (M, N, K, bits, p)
+                    assert ls[0]["rows"][0] == 0 and ls[-1]["rows"][1] == M, p
+                    if len(ls) == 2:
+                        assert ls[0]["rows"][1] == ls[1]["rows"][0] and p["splits"] == 1, p
+                    for l in ls:
+                        assert l["rows"][0] < l["rows"][1], p
+                        assert l["tile"] in ((256, 256), (128, 256), (128, 128), (64, 256)), p
+                    steps, sp = K // 64, p["splits"]
+                    assert 1 <= sp <= 8, p
+                    chunk = -(-steps // sp)
+                    assert sp == 1 or (sp - 1) * chunk < steps, p
+                    if sp > 1:
+                        assert cham.workspace_bytes(cham.OP_LINEAR, M, N, K) >= sp * M * N * 4, p
+    with pytest.raises(cham.ChamError):
+        cham.linear_plan(0, 64, 64, 4)
+    with pytest.raises(cham.ChamError):
+        cham.linear_plan(64, 64, 64, 6)
