@@ -375,7 +375,10 @@ def test_fp8_conversion_on_every_tie_and_boundary():
         _check_aq(aq, xs, fmt, 1.0, 0.0, dynamic=False)
 
 
-def test_quantize_act_lut_lookup():
+@pytest.mark.parametrize("dynamic", [False, True])
+def test_quantize_act_lut_lookup(dynamic):
+    """Alg. runtime (static: the bucket's calibrated S, Z) and Alg. runtime_dit (dynamic:
+    the LUT's format with ScaleZP of this tensor's own min / max)."""
     L, B = 3, 4
     st, ost = _calibrate(L, B, 64, 256, seed=2, steps_per_bucket=1)
     lut = cham.build_act_lut(st).mirror()
@@ -383,12 +386,15 @@ def test_quantize_act_lut_lookup():
     for l in range(L):
         for t in (0, 260, 600, 999):
             X = synth.diffusion_acts(5, l, t, 64, 256)
-            case(f"quantize_act_lut layer={l} t={t}")
-            aq = cham.quantize_act_lut(torch.from_numpy(X).to(DEV), lut, l, t, dynamic=False)
+            case(f"quantize_act_lut layer={l} t={t} dynamic={dynamic}")
+            aq = cham.quantize_act_lut(torch.from_numpy(X).to(DEV), lut, l, t, dynamic=dynamic)
             torch.cuda.synchronize()
             i = l * B + oracle.bucket(t, 1000, B)
             assert aq.fmt == F[i]
-            _check_aq(aq, X, int(F[i]), S[i], Z[i], dynamic=False)
+            if dynamic:
+                _check_aq(aq, X, int(F[i]))
+            else:
+                _check_aq(aq, X, int(F[i]), S[i], Z[i], dynamic=False)
 
 
 # ---------------------------------------------------------------------------------------
