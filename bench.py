@@ -56,6 +56,7 @@ def parse():
     p.add_argument("--no-dense-reference", action="store_true",
                    help="skip timing the library's dense f16 GEMM on the same shapes (a point of comparison)")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--no-w8", action="store_true", help="skip the W8 x A8 GEMM timing after the benchmark")
     p.add_argument("--layer-steps", type=int, default=10,
                    help="untimed steps after the timed ones for the per-layer GEMM breakdown (0: none)")
     p.add_argument("--calib-copy-mib", type=int, default=0,
@@ -285,6 +286,10 @@ def main():
     }
     if not args.no_dense_reference:
         out["dense_f16_reference"] = dense_reference(layers, stream)
+    if not args.no_w8:
+        for a, st_c in zip(aqs, aq_s):
+            a.fmt = st_c.fmt  # the format the step's quantize calls wrote into the C structs
+        out["w8a8_linear"] = w8_linear(cham, layers, Ws, aqs, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(layers, Ws, Xs, fmts, args.cpu_budget_s)
     print(json.dumps(out), flush=True)
@@ -312,6 +317,34 @@ def dense_reference(layers, stream, reps=20):
         res[name] = round(2.0 * M_TOKENS * N * K / (ms * 1e-3) / 1e12, 1)
     return {"tflops": res, "unit": "TFLOP/s",
             "what": "torch.matmul f16 x f16 -> f16 (library GEMM), same M, N, K; no decode, 2-byte output"}
+
+
+def w8_linear(cham, layers, Ws, aqs, stream, reps=20):
+    """The same four GEMMs with W8 weights (INT8-sym, INT8-asym, MXINT8 per channel: the
+    8-bit palette) against the step's A8 activation codes, after the benchmark: each call
+    timed with HIP events over `reps` calls; TFLOP/s per layer and over the four."""
+    import torch
+    res, tot_ms, tot_fl = {}, 0.0, 0.0
+    for (name, K, N), W, aq in zip(layers, Ws, aqs):
+        wq = cham.select_weight_formats(W, cham.MASK_W8, want_packed=True)
+        Y = torch.empty((M_TOKENS, N), dtype=torch.float32, device=W.device)
+        ws = torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=W.device)
+        for _ in range(3):
+            cham.mixed_linear(aq, wq, Y=Y, ws=ws)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            cham.mixed_linear(aq, wq, Y=Y, ws=ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        fl = 2.0 * M_TOKENS * N * K
+        res[name] = round(fl / (ms * 1e-3) / 1e12, 1)
+        tot_ms += ms
+        tot_fl += fl
+    return {"tflops": res, "all_tflops": round(tot_fl / (tot_ms * 1e-3) / 1e12, 1), "unit": "TFLOP/s",
+            "what": "mixed_linear with W8 per-channel weights (8-bit palette), the step's A8 codes; each call "
+                    "timed alone after the benchmark"}
 
 
 def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
