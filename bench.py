@@ -349,10 +349,19 @@ def w8_linear(cham, layers, Ws, aqs, stream, reps=20):
 
 def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
     """The CPU oracle (single-threaded C) on a bounded sample of the same step, scaled to
-    the step's GEMM-flop throughput: a sample of output channels is searched, a sample of
-    activation rows quantized and a sample of outputs computed; the per-layer times are
-    extrapolated to the full sizes."""
+    the step's GEMM-flop throughput: per layer, output channels are searched, activation
+    rows quantized and single outputs computed, each in chunks until its share of the
+    budget is spent; the per-layer times are extrapolated to the full sizes."""
     import oracle
+
+    def until(share, total, chunk, fn):  # run fn(first, count) in chunks for `share` seconds
+        done, t0 = 0, time.perf_counter()
+        while done < total and (done == 0 or time.perf_counter() - t0 < share):
+            n = min(chunk, total - done)
+            fn(done, n)
+            done += n
+        return done, time.perf_counter() - t0
+
     per_layer = budget_s / len(layers)
     total_s = 0.0
     flops = 0.0
@@ -360,30 +369,35 @@ def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
     for li, (name, K, N) in enumerate(layers):
         W = Ws[li].cpu().numpy()
         X = Xs[li].cpu().numpy()
-        nrows = max(8, min(N, int(per_layer * 0.4 * 4e6 / K)))
-        t = time.perf_counter()
-        wq = oracle.select_weight_formats(W[:nrows], oracle.MASK_W4, want_err=False, want_perm=False)
-        t_search = (time.perf_counter() - t) * N / nrows
-        mrows = max(4, min(X.shape[0], int(per_layer * 0.2 * 2e6 / K)))
+        M = X.shape[0]
+        first = {}
+
+        def search(a, n):
+            wq = oracle.select_weight_formats(W[a:a + n], oracle.MASK_W4, want_err=False, want_perm=False)
+            first.setdefault("wq", wq)
+        nrows, ts = until(0.4 * per_layer, N, 32, search)
         t = time.perf_counter()
         lo, hi = oracle.minmax(X)
         s, z = oracle.scale_zp(act_fmts[li], lo, hi)
-        _, _, xh = oracle.quantize_act(X[:mrows], act_fmts[li], s, z, want_xhat=True)
-        t_q = (time.perf_counter() - t) * X.shape[0] / mrows
-        Wh = oracle.dequant_weights(wq, K)
-        npairs = max(64, int(per_layer * 0.3 * 2e8 / K))
+        t_mm = time.perf_counter() - t
+
+        def quant(a, n):
+            xh = oracle.quantize_act(X[a:a + n], act_fmts[li], s, z, want_xhat=True)[2]
+            first.setdefault("xh", xh)
+        mrows, tq = until(0.2 * per_layer, M, 64, quant)
+        Wh = oracle.dequant_weights(first["wq"], K)
+        xh = first["xh"]
         g = np.random.default_rng(li)
-        mm = g.integers(0, mrows, npairs)
-        nn = g.integers(0, nrows, npairs)
-        t = time.perf_counter()
-        oracle.linear_pairs(xh, Wh, mm, nn)
-        t_g = (time.perf_counter() - t) * (X.shape[0] * N) / npairs
-        total_s += t_search + t_q + t_g
-        flops += 2.0 * X.shape[0] * N * K
-        samples.append(f"{name}: {nrows}/{N} channels searched, {mrows}/{X.shape[0]} rows quantized, "
-                       f"{npairs} outputs")
+
+        def pairs(a, n):
+            oracle.linear_pairs(xh, Wh, g.integers(0, xh.shape[0], n), g.integers(0, Wh.shape[0], n))
+        npairs, tg = until(0.4 * per_layer, M * N, 4096, pairs)
+        total_s += ts * N / nrows + t_mm + tq * M / mrows + tg * (M * N) / npairs
+        flops += 2.0 * M * N * K
+        samples.append(f"{name}: {nrows}/{N} channels searched, {mrows}/{M} rows quantized, {npairs} outputs")
     return {"value": round(flops / total_s / 1e12, 9), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
-            "sample": "; ".join(samples) + "; per-layer times extrapolated to full size (stats/LUT omitted)"}
+            "sample": "; ".join(samples) + f"; each part run for its share of {budget_s:.0f} s of CPU time, "
+                      "per-layer times extrapolated to full size (stats/LUT omitted)"}
 
 
 if __name__ == "__main__":
