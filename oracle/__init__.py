@@ -140,16 +140,16 @@ def wq_row(fmt: int, w: np.ndarray):
     codes = np.zeros(K, np.uint8)
     wh = np.zeros(K, np.float32)
     s = np.zeros(1, np.float32)
-    z = np.zeros(1, np.int32)
+    z = np.zeros(1, np.float32)
     nf = np.zeros(max(K // 64, 1), np.float32)
     e8 = np.zeros(max(K // 32, 1), np.uint8)
     _load().orc_wq_row(fmt, _p(w), K, _p(codes), _p(wh), _p(s), _p(z), _p(nf), _p(e8))
-    return codes, wh, float(s[0]), int(z[0]), nf[:K // 64], e8[:K // 32]
+    return codes, wh, float(s[0]), float(z[0]), nf[:K // 64], e8[:K // 32]
 
 
 def select_weight_formats(W: np.ndarray, mask: int, want_err: bool = True, want_perm: bool = True):
     """Per-output-channel format search.  Returns a dict of numpy arrays:
-    fmt [N] u8, codes [N, K*bits/8] u8, scale [N] f32, zero [N] i32, nf4_absmax [N, K/64] f32,
+    fmt [N] u8, codes [N, K*bits/8] u8, scale [N] f32, zero [N] f32 (integral), nf4_absmax [N, K/64] f32,
     e8m0 [N, K/32] u8, perm [N] i32, group_off [10] i32, err [N, 9] f64."""
     W = _f32(W)
     N, K = W.shape
@@ -158,7 +158,7 @@ def select_weight_formats(W: np.ndarray, mask: int, want_err: bool = True, want_
         fmt=np.zeros(N, np.uint8),
         codes=np.zeros((N, K * cb // 8), np.uint8),
         scale=np.zeros(N, np.float32),
-        zero=np.zeros(N, np.int32),
+        zero=np.zeros(N, np.float32),
         nf4_absmax=np.zeros((N, K // 64), np.float32),
         e8m0=np.zeros((N, K // 32), np.uint8),
         perm=np.zeros(N, np.int32) if want_perm else None,

@@ -183,17 +183,20 @@ static void q_int_sym(const float* x, int64_t n, int Q, unsigned bits, uint8_t* 
     *scale = s;
 }
 
-/* INT-asym, L = 255 or 15 (App. A.7 ScaleZP; App. A.11): s = (hi-lo)/L, z = round(-lo/s),
- * q = clamp(round(x/s) + z, 0, L), x^ = (q - z) s.
- * READING: the observed range is widened to contain zero (lo <= 0 <= hi), so the zero
- * point is itself a code in [0, L]; x/s is computed as x * (1/s) per element. */
+/* INT-asym, L = 255 or 15 (App. A.7 ScaleZP; App. A.11: L + 1 evenly spaced levels from
+ * min to max): s = (hi - lo)/L, z = round(-lo/s), both taken literally -- the range is the
+ * observed one and z is not clamped, so for a one-sided range z lies outside [0, L] and the
+ * levels (q - z) s, q = 0..L, run from lo to hi.  Quantization q = clamp(round(x/s) + z,
+ * 0, L), x^ = (q - z) s, each step one binary32 operation (x/s as x * (1/s)).
+ * READING: a constant group (hi == lo) has no spread to divide; it takes s = |lo| (1 if
+ * lo = 0), so z = -sign(lo) and every element is reconstructed exactly. */
 static void scalezp_int_asym(float lo, float hi, int L, float* s_out, float* z_out) {
-    lo = fminf(lo, 0.0f);
-    hi = fmaxf(hi, 0.0f);
-    float s = floor_scale((hi - lo) / (float)L);
-    float z = clampf(rne(-lo / s), 0.0f, (float)L);
+    float d = hi - lo;
+    float s;
+    if (d == 0.0f) s = lo != 0.0f ? fabsf(lo) : 1.0f;
+    else s = floor_scale(d / (float)L);
     *s_out = s;
-    *z_out = z;
+    *z_out = rne(-lo / s);
 }
 
 static void q_int_asym_with(const float* x, int64_t n, int L, float s, float z, uint8_t* code,
@@ -207,14 +210,14 @@ static void q_int_asym_with(const float* x, int64_t n, int L, float s, float z, 
 }
 
 static void q_int_asym(const float* x, int64_t n, int L, uint8_t* code, float* xh,
-                       float* scale, int32_t* zero) {
+                       float* scale, float* zero) {
     float lo = INFINITY, hi = -INFINITY;
     for (int64_t i = 0; i < n; ++i) { lo = fminf(lo, x[i]); hi = fmaxf(hi, x[i]); }
     float s, z;
     scalezp_int_asym(lo, hi, L, &s, &z);
     q_int_asym_with(x, n, L, s, z, code, xh);
     *scale = s;
-    *zero = (int32_t)z;
+    *zero = z;
 }
 
 /* FP4 E2M1 with one scale per output channel (READING: s = amax/6, saturating at +-6). */
@@ -297,9 +300,9 @@ static int wfmt_bits(int f) { return (f == W_INT8_SYM || f == W_INT8_ASYM || f =
  * codes[K] unpacked; scale/zero per row; nf4a[K/64]; e8[K/32]; wh[K] = DQ_f(Q_f(w)).
  * Metadata a format does not use is written as 0. */
 static void wq_row(int f, const float* w, int64_t K, uint8_t* codes, float* wh, float* scale,
-                   int32_t* zero, float* nf4a, uint8_t* e8) {
+                   float* zero, float* nf4a, uint8_t* e8) {
     *scale = 0.0f;
-    *zero = 0;
+    *zero = 0.0f;
     if (nf4a) for (int64_t b = 0; b < K / 64; ++b) nf4a[b] = 0.0f;
     if (e8) for (int64_t b = 0; b < K / 32; ++b) e8[b] = 0;
     switch (f) {
@@ -329,7 +332,7 @@ static void wq_row(int f, const float* w, int64_t K, uint8_t* codes, float* wh, 
 
 /* Decode one weight row from codes + metadata (the same DQ_f as above, from the stored
  * representation).  codes unpacked. */
-static void wdq_row(int f, const uint8_t* c, int64_t K, float scale, int32_t zero,
+static void wdq_row(int f, const uint8_t* c, int64_t K, float scale, float zero,
                     const float* nf4a, const uint8_t* e8, float* wh) {
     nf4_build();
     for (int64_t k = 0; k < K; ++k) {
@@ -339,7 +342,7 @@ static void wdq_row(int f, const uint8_t* c, int64_t K, float scale, int32_t zer
         case W_INT8_SYM: v = (float)(int8_t)u * scale; break;
         case W_INT4_SYM: v = (float)((int)(u << 28) >> 28) * scale; break;
         case W_INT8_ASYM:
-        case W_INT4_ASYM: v = ((float)u - (float)zero) * scale; break;
+        case W_INT4_ASYM: v = ((float)u - zero) * scale; break;
         case W_FP4: v = (float)mf_decode(&MF_E2M1, u) * scale; break;
         case W_NF4: v = NF4[u & 15u] * nf4a[k / 64]; break;
         case W_MXINT8: v = ldexpf((float)(int8_t)u, (int)e8[k / 32] - 127 - 6); break;
@@ -359,14 +362,14 @@ static void wdq_row(int f, const uint8_t* c, int64_t K, float scale, int32_t zer
  * palette id.  The codes and metadata of the chosen format are emitted:
  *   codes : two 4-bit codes per byte (even k in the low nibble) when every enabled
  *           format is 4-bit, otherwise one code per byte; row-major [N][K/2] or [N][K].
- *   scale[N], zero[N], nf4a[N][K/64] (may be NULL if NF4 disabled),
+ *   scale[N], zero[N] (integral binary32), nf4a[N][K/64] (may be NULL if NF4 disabled),
  *   e8[N][K/32] (may be NULL if no MX format enabled), err[N][9] (may be NULL; -1 for
  *   disabled formats).
  * perm / group_off: stable sort of channels by chosen format (may be NULL).
  * scratch: caller buffer of at least 4*K floats + 2*K bytes + K/64 floats + K/32 bytes.
  * Returns 0, or -1 on a bad mask/shape. */
 int orc_select_weight_formats(const float* W, int64_t N, int64_t K, uint32_t mask, uint8_t* fmt,
-                              uint8_t* codes, float* scale, int32_t* zero, float* nf4a,
+                              uint8_t* codes, float* scale, float* zero, float* nf4a,
                               uint8_t* e8, int32_t* perm, int32_t* group_off, double* err) {
     if (N < 0 || K <= 0 || (mask & ~0x1FFu) || mask == 0) return -1;
     int code_bits = 4;
@@ -387,11 +390,10 @@ int orc_select_weight_formats(const float* W, int64_t N, int64_t K, uint32_t mas
         int best = -1;
         double best_err = 0.0;
         float bs = 0.0f;
-        int32_t bz = 0;
+        float bz = 0.0f;
         for (int f = 0; f < W_NFMT; ++f) {
             if (!((mask >> f) & 1u)) { if (err) err[n * W_NFMT + f] = -1.0; continue; }
-            float s;
-            int32_t z;
+            float s, z;
             wq_row(f, w, K, cbuf, wh, &s, &z, nfa, eb);
             double e = 0.0;
             for (int64_t k = 0; k < K; ++k) {
@@ -439,7 +441,7 @@ int orc_select_weight_formats(const float* W, int64_t N, int64_t K, uint32_t mas
 
 /* Dequantize a whole packed weight matrix (as emitted above) to binary32. */
 int orc_dequant_weights(int64_t N, int64_t K, int code_bits, const uint8_t* fmt,
-                        const uint8_t* codes, const float* scale, const int32_t* zero,
+                        const uint8_t* codes, const float* scale, const float* zero,
                         const float* nf4a, const uint8_t* e8, float* Wh) {
     static uint8_t cb[1 << 16];
     if (K > (1 << 16)) return -1;
@@ -461,7 +463,7 @@ int orc_dequant_weights(int64_t N, int64_t K, int code_bits, const uint8_t* fmt,
 
 /* Round-trip one row in one format (diagnostics and pins). codes unpacked. */
 void orc_wq_row(int f, const float* w, int64_t K, uint8_t* codes, float* wh, float* scale,
-                int32_t* zero, float* nf4a, uint8_t* e8) {
+                float* zero, float* nf4a, uint8_t* e8) {
     wq_row(f, w, K, codes, wh, scale, zero, nf4a, e8);
 }
 

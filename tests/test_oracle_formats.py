@@ -198,6 +198,80 @@ def test_degenerate_rows():
         codes, wh, s, z, nf, e8 = oracle.wq_row(fmt, np.full(K, c, np.float32))
         # a constant row reconstructs to within one grid step of the constant
         assert np.all(np.abs(wh - c) <= 0.5 * c), fmt
+    # INT-asym on a constant row (hi == lo): s = |c|, z = -sign(c), exact reconstruction
+    for fmt in (oracle.W_INT4_ASYM, oracle.W_INT8_ASYM):
+        for c, zexp in ((np.float32(0.37), -1.0), (np.float32(-2.5), 1.0), (np.float32(0.0), 0.0)):
+            codes, wh, s, z, nf, e8 = oracle.wq_row(fmt, np.full(K, c, np.float32))
+            assert np.array_equal(wh, np.full(K, c, np.float32)), (fmt, c)
+            assert z == zexp and s == (abs(c) if c != 0 else 1.0), (fmt, c, s, z)
+
+
+# INT-asym (App. A.7 ScaleZP, App. A.11): L + 1 evenly spaced levels from min to max, the
+# zero point round(-lo/s) not clamped.  Ranges whose every step is exact in binary32, with
+# their scale, zero point and the codes of the range ends worked out by hand.
+INT_ASYM_HAND = [
+    # (L, lo, hi, s, z): one-sided positive, one-sided negative, crossing zero
+    (15, 1.0, 16.0, 1.0, -1.0),
+    (15, -16.0, -1.0, 1.0, 16.0),
+    (15, -5.0, 10.0, 1.0, 5.0),
+    (255, 2.0, 257.0, 1.0, -2.0),
+    (255, -0.5, -0.5 + 255 * 0.125, 0.125, 4.0),
+    (255, 64.0, 64.0 + 255 * 0.25, 0.25, -256.0),
+]
+
+
+@pytest.mark.parametrize("L,lo,hi,s_exp,z_exp", INT_ASYM_HAND)
+def test_int_asym_scale_zp_hand_computed(L, lo, hi, s_exp, z_exp):
+    fmt = oracle.W_INT4_ASYM if L == 15 else oracle.W_INT8_ASYM
+    K = 64
+    w = np.linspace(lo, hi, K).astype(np.float32)
+    w[0], w[-1] = lo, hi
+    codes, wh, s, z, *_ = oracle.wq_row(fmt, w)
+    assert s == s_exp and z == z_exp
+    assert codes[0] == 0 and codes[-1] == L  # the range ends are the first and last level
+    assert wh[0] == np.float32(lo) and wh[-1] == np.float32(hi)
+    if L == 255:  # the activation ScaleZP is the same helper
+        sa, za = oracle.scale_zp(oracle.A_INT8_ASYM, lo, hi)
+        assert sa == s_exp and za == z_exp
+
+
+@pytest.mark.parametrize("L", [15, 255])
+def test_int_asym_one_sided_levels_span_the_range(L):
+    """For one-sided rows the L + 1 levels (q - z) s run from min to max (App. A.11), every
+    element lands on its nearest level (brute force over the grid), and the zero point is
+    outside [0, L] -- a range widened to contain zero, or a clamped z, fails these."""
+    fmt = oracle.W_INT4_ASYM if L == 15 else oracle.W_INT8_ASYM
+    g = np.random.default_rng(21 + L)
+    for trial in range(30):
+        sign = 1 if trial % 2 == 0 else -1
+        base = np.float32(np.exp(g.normal(0, 2)))
+        w = (sign * (base * (1.0 + g.uniform(0.01, 2.0) * g.random(256)))).astype(np.float32)
+        lo, hi = np.float64(w.min()), np.float64(w.max())
+        codes, wh, s, z, *_ = oracle.wq_row(fmt, w)
+        assert (z < 0) if sign > 0 else (z > L), (trial, z)
+        step = (hi - lo) / L
+        assert abs(s - step) <= 2 ** -22 * step
+        levels = (np.arange(L + 1, dtype=np.float64) - z) * s
+        assert abs(levels[0] - lo) <= 0.5 * s * (1 + 1e-5) and abs(levels[-1] - hi) <= 0.5 * s * (1 + 1e-5)
+        near = np.min(np.abs(levels[None, :] - w.astype(np.float64)[:, None]), axis=1)
+        err = np.abs(wh.astype(np.float64) - w)
+        assert np.all(err <= near + 4e-7 * np.abs(w)), trial
+        assert np.max(err) <= 0.5 * step * (1 + 1e-4) + 4e-7 * np.max(np.abs(w))
+
+
+def test_nf4_exact_midpoint_goes_to_lower_level():
+    """An input exactly on the midpoint of two NF4 levels (representable in binary32 for
+    four of the fifteen pairs) is assigned the lower level (the stated tie rule)."""
+    v = oracle.nf4_table().astype(np.float64)
+    ties = [i for i in range(15) if np.float32((v[i] + v[i + 1]) / 2) == (v[i] + v[i + 1]) / 2]
+    assert ties == [2, 6, 7, 14]
+    for i in ties:
+        w = np.zeros(64, np.float32)
+        w[0] = 1.0  # block absmax exactly 1, so w * fl(1/a) = w
+        w[1] = np.float32((v[i] + v[i + 1]) / 2)
+        w[2] = np.nextafter(w[1], np.float32(2))  # just above: the upper level
+        codes, wh, *_ = oracle.wq_row(oracle.W_NF4, w)
+        assert codes[1] == i and codes[2] == i + 1, (i, codes[:3])
 
 
 def test_mx_exponents():
@@ -223,6 +297,11 @@ def test_scale_zp_printed_formulas():
     assert s == np.float32(np.float32(2.0) / np.float32(255.0))
     # z = round(-lo/s) with -lo/s = 1/fl(2/255) = 127.4999.. in binary32
     assert z == np.rint(np.float32(1.0) / s) == 127.0
+    # one-sided ranges keep their own end points: X in [0.5, 1.5] puts z near -127.5
+    s, z = oracle.scale_zp(oracle.A_INT8_ASYM, 0.5, 1.5)
+    assert s == np.float32(np.float32(1.0) / np.float32(255.0)) and z in (-127.0, -128.0)
+    s, z = oracle.scale_zp(oracle.A_INT8_ASYM, -3.0, -1.0)
+    assert s == np.float32(np.float32(2.0) / np.float32(255.0)) and z in (382.0, 383.0)
     s, z = oracle.scale_zp(oracle.A_FP8_E4M3, -3.0, 2.0)
     assert s == np.float32(np.float32(3.0) / np.float32(448.0)) and z == 0
     s, z = oracle.scale_zp(oracle.A_FP8_E5M2, -3.0, 2.0)
