@@ -45,7 +45,7 @@ extern "C" {
 #define CHAM_OK 0
 #define CHAM_EINVAL (-1)     /* NULL pointer, negative or zero size, bad layer/bucket index  */
 #define CHAM_ESHAPE (-2)     /* K not a multiple of 32 (every call) or of 64 (NF4 enabled;
-                                mixed_linear)                                                */
+                                mixed_linear), or beyond a call's size limit               */
 #define CHAM_EFORMAT (-3)    /* unknown format id, empty or out-of-range palette mask        */
 #define CHAM_EHIP (-4)       /* a HIP launch or runtime call failed                          */
 #define CHAM_EWORKSPACE (-5) /* ws NULL or smaller than cham_workspace_bytes()               */
@@ -90,8 +90,10 @@ int cham_version(void);
  * format with the smallest sum of squared reconstruction errors (= the largest SQNR; ties go
  * to the lowest id) is kept, with its codes and metadata.  Quantizers (App. A.11, App. A.12):
  *   INT-sym   s = amax/Q (Q = 127, 7), q = clamp(round(w/s), -Q, Q), w^ = q s
- *   INT-asym  lo/hi widened to contain 0, s = (hi-lo)/L (L = 255, 15), z = round(-lo/s),
- *             q = clamp(round(w/s) + z, 0, L), w^ = (q - z) s
+ *   INT-asym  App. A.7 ScaleZP on the channel's own [lo, hi]: s = (hi-lo)/L (L = 255, 15),
+ *             z = round(-lo/s), not clamped (a one-sided row has z outside [0, L]);
+ *             q = clamp(round(w/s) + z, 0, L), w^ = (q - z) s; a constant row (hi == lo)
+ *             takes s = |lo| (1 if lo == 0), so z = -sign(lo) and w^ = w
  *   FP4 E2M1  per channel s = amax/6, e = E2M1(clamp(w/s, +-6)), w^ = e s
  *   NF4       per 64-block a = absmax, c = nearest NF4 level to w/a, w^ = v_c a
  *   MXINT8/4  per 32-block E = floor(log2 amax), k = clamp(round(w 2^(F-E)), +-Q),
@@ -113,7 +115,8 @@ typedef struct cham_wq {
                                Codes: INT-sym, MXINT two's complement; INT-asym unsigned q;
                                NF4 level index 0..15 (ascending); E2M1 sign|exp(2)|mantissa */
     float* scale;           /* [N]      s of INT-sym/INT-asym/FP4 channels, 0 otherwise       */
-    int32_t* zero;          /* [N]      z of INT-asym channels, 0 otherwise                   */
+    float* zero;            /* [N]      z of INT-asym channels (an integral binary32, any
+                               magnitude), 0 otherwise                                        */
     float* nf4_absmax;      /* [N][K/64] block absmax of NF4 channels, 0 otherwise;
                                may be NULL iff NF4 is not enabled                             */
     uint8_t* e8m0;          /* [N][K/32] biased block exponent of MX channels, 0 otherwise;
@@ -134,7 +137,9 @@ typedef struct cham_wq {
 
 /* Search the formats of W [N][K] (device, binary32, finite) and fill *wq's buffers.
  * Ownership: the caller owns W and every buffer in *wq.  Errors: CHAM_EINVAL (NULL W/wq/
- * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K), CHAM_EHIP. */
+ * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K not a multiple of 32, or of
+ * 64 with NF4 enabled or a packed layout requested, or K > 8192: a row is held in the
+ * registers of one workgroup), CHAM_EHIP. */
 int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream);
 
 /* Bytes of the packed GEMM layout of an N x K weight (see cham_wq.packed). */
@@ -227,7 +232,8 @@ typedef struct cham_aq {
 
 /* Quantize X [M][K] (device, finite binary32, 16-byte aligned; out->codes 4-byte aligned)
  * to activation format `fmt`:
- *   INT8-asym  q = clamp(round(x/s) + z, 0, 255)
+ *   INT8-asym  q = clamp(round(x/s) + z, 0, 255); dynamic (s, z) by ScaleZP on this X's own
+ *              [lo, hi] (App. A.7: s = (hi-lo)/255, z = round(-lo/s), z not clamped)
  *   FP8        e = E4M3 / E5M2(clamp(x/s, +-448 / +-57344)), round to nearest even
  *   MXFP8      per 32-block E = floor(log2 amax) (the paper's exponent: values in (-2, 2)),
  *              e = E4M3(x / 2^E)
@@ -253,8 +259,15 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  *
  * Y[m][n] = sum_k x^[m][k] w^[n][k], with x^ = DQ(xq) and w^ = DQ(wq) exactly as the
  * quantizers above define them, accumulated in binary32 on the matrix cores.  Accuracy:
- * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element (NF4 levels are carried at half
- * precision; every other operand is exact).  xq->K must equal wq->K and be a multiple of
+ * |Y - Y_exact| <= 1e-3 * sum_k |x^ w^| per element.  Operands are decoded to half
+ * precision: NF4 levels times their block absmax, and INT-asym weight levels q - z beyond
+ * 2^11 in magnitude, carry one rounding (relative 2^-11; INT8-asym channels with |z| beyond
+ * 2^22, whose values agree to 6e-5, up to 2^-10); INT8-asym activations are decoded
+ * exactly, a zero point beyond +-1024 through a per-channel correction (the channel's sum of
+ * dequantized weights, binary64, times (z - z') s in the epilogue).  Block-scaled operands
+ * (NF4 and MX weights, MX activations) are held relative to the largest block of their
+ * channel or row: blocks within 2^28 of it are exact (NF4: one rounding), blocks further
+ * below fall into half precision's subnormal range and lose bits.  xq->K must equal wq->K and be a multiple of
  * 64; xq->codes, wq->codes and Y must be 16-byte aligned.  Y [M][N] is written in the
  * original channel order.  When the output has too few tiles to fill the GPU, K is split
  * across workgroups whose partial outputs a second kernel adds in split order; no atomics

@@ -204,7 +204,7 @@ def alloc_wq(N: int, K: int, mask: int, device="cuda", want_perm=True, want_err=
               fmt=torch.empty(N, dtype=u8, device=device),
               codes=torch.empty((N, K * cb // 8), dtype=u8, device=device),
               scale=torch.empty(N, dtype=f32, device=device),
-              zero=torch.empty(N, dtype=i32, device=device),
+              zero=torch.empty(N, dtype=torch.float32, device=device),
               nf4_absmax=torch.empty((N, K // 64), dtype=f32, device=device) if nf4 else None,
               e8m0=torch.empty((N, K // 32), dtype=u8, device=device) if mx else None,
               perm=torch.empty(N, dtype=i32, device=device) if want_perm else None,

@@ -26,6 +26,17 @@ CHAM_DEV float clampf(float x, float lo, float hi) { return fminf(fmaxf(x, lo), 
 // Every floating group scale is floored at the smallest normal number (finite reciprocal).
 CHAM_DEV float floor_scale(float s) { return s < FLT_MIN ? FLT_MIN : s; }
 
+// ScaleZP of the INT-asym formats (App. A.7; App. A.11: L + 1 evenly spaced levels from min
+// to max): s = (hi - lo)/L, z = round(-lo/s) with no clamp, so a one-sided range keeps its
+// own end points and z lies outside [0, L].  A constant group (hi == lo) takes s = |lo|
+// (1 if lo = 0), z = -sign(lo): every element is reconstructed exactly.
+CHAM_DEV void int_asym_scale_zp(float lo, float hi, float L, float* s, float* z) {
+    const float d = hi - lo;
+    const float sc = d == 0.0f ? (lo != 0.0f ? fabsf(lo) : 1.0f) : floor_scale(d / L);
+    *s = sc;
+    *z = rne(-lo / sc);
+}
+
 // floor(log2(a)) for finite a > 0, from the binary32 fields (subnormals included).
 CHAM_DEV int floor_log2(float a) {
     uint32_t u = __float_as_uint(a) & 0x7fffffffu;

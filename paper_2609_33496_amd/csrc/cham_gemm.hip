@@ -56,7 +56,7 @@ constexpr int kBufferFlags = 0x00020000;  // buffer descriptor word 3: 32-bit da
 
 // ------------------------------------------------------------------------------------
 // pre-pass for MX activation formats: codes -> half precision relative to the row's
-// largest block exponent (exact), the row scale 2^eref separately
+// largest block exponent (exact for blocks within 2^28 of it), the row scale separately
 // ------------------------------------------------------------------------------------
 struct PrepArgs {
     const uint8_t* xc;
@@ -80,7 +80,9 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
     __syncthreads();
     if ((threadIdx.x & 63) == 0) atomicMax(&sh_e, mx_e);
     __syncthreads();
-    const int eref = sh_e - 127;
+    // the row's largest block lands at [2^14, 2^15): blocks down to 2^-28 of it stay normal
+    // in half precision (values are below 2 times 2^(block exponent - eref))
+    const int eref = sh_e - 127 - 14;
     const uint8_t* row = p.xc + (int64_t)m * K;
     _Float16* out = p.Xh + (int64_t)m * K;
     for (int g = threadIdx.x; g < K / 8; g += blockDim.x) {
@@ -156,8 +158,8 @@ CHAM_DEV half8 decode_bytes_table(const Table& t, uint32_t w0, uint32_t w1) {
     return r.h;
 }
 
-// 8-bit integer codes: value = ((c ^ x) - zoff) * factor, through 1024 + c in half
-// precision; x, -(1024 + zoff) and the factor come from the table slot.
+// 8-bit integer codes: value = fma((1024 + (c ^ x)) + a, f, b) in half precision, 1024 + c
+// formed by placing c in the mantissa; x, a, f and b come from the table slot.
 CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
     w0 ^= t.lo[0];
     w1 ^= t.lo[0];
@@ -166,11 +168,12 @@ CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
     r.u[1] = __builtin_amdgcn_perm(0x64646464u, w0, 0x04030402u);
     r.u[2] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04010400u);
     r.u[3] = __builtin_amdgcn_perm(0x64646464u, w1, 0x04030402u);
-    const half2v off = __builtin_bit_cast(half2v, t.lo[1]), fac = __builtin_bit_cast(half2v, t.lo[2]);
+    const half2v off = __builtin_bit_cast(half2v, t.lo[1]), fac = __builtin_bit_cast(half2v, t.lo[2]),
+                 off2 = __builtin_bit_cast(half2v, t.lo[3]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         half2v v = __builtin_bit_cast(half2v, r.u[i]);
-        v = (v + off) * fac;
+        v = __builtin_elementwise_fma(v + off, fac, off2);
         r.u[i] = __builtin_bit_cast(uint32_t, v);
     }
     return r.h;
@@ -183,7 +186,7 @@ CHAM_DEV half8 decode_bytes_int(const Table& t, uint32_t w0, uint32_t w1) {
 struct RecArgs {
     const uint8_t* wfmt;
     const float* wscale;
-    const int32_t* wzero;
+    const float* wzero;
     const float* wnf4;
     const uint8_t* we8;
     const uint8_t* wc;
@@ -191,7 +194,8 @@ struct RecArgs {
     int N, K, code_bits;
     int kchunk;  // k-steps per workgroup
     ColPrep* cols;
-    uint4* rec;  // [K/64][N][2][pieces]
+    float* colsum;  // [N] sum over k of the dequantized weights
+    uint4* rec;     // [K/64][N][2][pieces]
 };
 
 // Workgroup b handles 32 channels (block b % nblk) and the k-steps of chunk b / nblk.
@@ -212,10 +216,62 @@ constexpr int kRecPrefetch = 3;
 constexpr int kRecBatchMax = 16;
 struct RecBatch {
     int nl, ng;
-    int wg_end[kRecBatchMax];  // workgroups of layers 0..i
+    int cs_end[kRecBatchMax];  // column-sum workgroups of layers 0..i
+    int wg_end[kRecBatchMax];  // record workgroups of layers 0..i
     RecArgs r[kRecBatchMax];
     GroupArgs g[kRecBatchMax];
 };
+
+// Dequantized weight of code u in format f (App. A.11, as the quantizers define it).
+CHAM_DEV float dequant_code(int f, uint32_t u, float s, float z, float nfa, int e8) {
+    const int q8 = (int)(int8_t)(uint8_t)u, q4 = (int)(u << 28) >> 28;
+    switch (f) {
+    case CHAM_W_INT8_SYM: return (float)q8 * s;
+    case CHAM_W_INT4_SYM: return (float)q4 * s;
+    case CHAM_W_INT8_ASYM:
+    case CHAM_W_INT4_ASYM: return ((float)u - z) * s;
+    case CHAM_W_FP4: return e2m1_decode(u) * s;
+    case CHAM_W_NF4: return nf4_level(u) * nfa;
+    case CHAM_W_MXINT8: return ldexpf((float)q8, e8 - 127 - 6);
+    case CHAM_W_MXINT4: return ldexpf((float)q4, e8 - 127 - 2);
+    default: return ldexpf(e2m1_decode(u), e8 - 127);  // MXFP4
+    }
+}
+
+// Column sum of channel n (one wavefront): lane l adds elements 8(l + 64 j) .. + 7 in order
+// in binary64, then the lanes are added by a fixed tree, so the sum is the same every run.
+CHAM_DEV void colsum_channel(const RecArgs& a, int n) {
+    const int lane = threadIdx.x & 63;
+    const int K = a.K;
+    const int f = a.wfmt[n];
+    double acc = 0.0;
+    if (f < CHAM_W_NFMT && ((a.mask >> f) & 1u)) {
+        const float s = a.wscale[n], z = a.wzero[n];
+        for (int k0 = 8 * lane; k0 < K; k0 += 512) {
+            uint32_t w0, w1;
+            if (a.code_bits == 4) {
+                const uint32_t w = *reinterpret_cast<const uint32_t*>(a.wc + (int64_t)n * (K / 2) + k0 / 2);
+                w0 = (w & 0x0F0F0F0Fu);  // even k of the 8, one per byte
+                w1 = (w >> 4) & 0x0F0F0F0Fu;
+            } else {
+                const uint2 w = *reinterpret_cast<const uint2*>(a.wc + (int64_t)n * K + k0);
+                w0 = w.x;
+                w1 = w.y;
+            }
+            const float nfa = f == CHAM_W_NF4 ? a.wnf4[(int64_t)n * (K / 64) + k0 / 64] : 0.0f;
+            const int e8 = is_mx(f) ? (int)a.we8[(int64_t)n * (K / 32) + k0 / 32] : 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                // 4-bit layout: k0 + j is byte j/2 of the word, even j low nibble
+                const uint32_t u = a.code_bits == 4 ? (((j & 1) ? w1 : w0) >> (8 * (j >> 1))) & 0xFFu
+                                                    : ((j < 4 ? w0 : w1) >> (8 * (j & 3))) & 0xFFu;
+                acc += (double)dequant_code(f, u, s, z, nfa, e8);
+            }
+        }
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) a.colsum[n] = (float)acc;
+}
 
 __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     __shared__ ColPrep cp[kRecChannels];
@@ -223,7 +279,16 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
         group_channels<256>(B.g[blockIdx.x], nullptr);
         return;
     }
-    const int rb = (int)blockIdx.x - B.ng;  // record workgroup index
+    const int cb_all = (int)blockIdx.x - B.ng;
+    if (cb_all < B.cs_end[B.nl - 1]) {  // column sums: four channels per workgroup
+        int li = 0;
+        while (li + 1 < B.nl && cb_all >= B.cs_end[li]) ++li;
+        const RecArgs& a = B.r[li];
+        const int n = 4 * (cb_all - (li ? B.cs_end[li - 1] : 0)) + (threadIdx.x >> 6);
+        if (n < a.N) colsum_channel(a, n);
+        return;
+    }
+    const int rb = cb_all - B.cs_end[B.nl - 1];  // record workgroup index
     int li = 0;
     while (li + 1 < B.nl && rb >= B.wg_end[li]) ++li;
     const RecArgs& a = B.r[li];
@@ -291,13 +356,19 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
         ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
         if (ok) {
             c.fmt = f;
-            c.zero = (float)a.wzero[nn];
+            c.zero = a.wzero[nn];
             if (f == CHAM_W_NF4) {
-                c.eref = floor_log2(floor_scale(mxf));
+                // levels (|v| <= 1) times the block absmax over 2^eref stay below 2^15, and a
+                // block 2^-28 below the largest is still a normal half-precision number
+                c.eref = floor_log2(floor_scale(mxf)) - 14;
                 c.colscale = ldexpf(1.0f, c.eref);
             } else if (is_mx(f)) {
-                c.eref = mxe - 127 - mx_F(f);
+                // element magnitudes up to 127 (MXINT8) times 2^8 stay below 2^15
+                c.eref = mxe - 127 - mx_F(f) - 8;
                 c.colscale = ldexpf(1.0f, c.eref);
+            } else if (f == CHAM_W_INT8_ASYM || f == CHAM_W_INT4_ASYM) {
+                c.eref = int_asym_eref(c.zero, f == CHAM_W_INT8_ASYM ? 255.0f : 15.0f);
+                c.colscale = ldexpf(a.wscale[nn], c.eref);
             } else {
                 c.colscale = a.wscale[nn];
             }
@@ -340,6 +411,7 @@ struct GemmArgs {
     const float* xs;         // per-tensor activation scale (device scalar)
     const float* xz;         // per-tensor activation zero point (device scalar)
     const ColPrep* cols;     // [N]
+    const float* colsum;     // [N] sum over k of the dequantized weights
     const uint4* rec;        // [K/64][N][2][pieces]
     float* Y;
     int M, N, K;
@@ -408,10 +480,16 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     const int nsteps = K / BK - kb < a.kchunk ? K / BK - kb : a.kchunk;
 
     if (t < BM) Rs[t] = AF == kAF16 ? a.rowscale[t < rows ? m0 + t : m0] : *a.xs;
+    // INT8-asym: the codes are decoded as (1024 + c) - (1024 + z1) with z1 the zero point
+    // clamped to [-1024, 1024] (exact in half precision); the rest z - z1 (an integer, exact
+    // in binary32) is taken out in the epilogue as -(z - z1) s times the channel's weight sum
     half2v negz = {(_Float16)0.0f, (_Float16)0.0f};
+    float zc = 0.0f;
     if (AF == kAInt8) {
-        const _Float16 nz = (_Float16)(-(1024.0f + *a.xz));
+        const float za = *a.xz, z1 = clampf(za, -1024.0f, 1024.0f);
+        const _Float16 nz = (_Float16)(-(1024.0f + z1));
         negz = half2v{nz, nz};
+        zc = split == 0 ? -((za - z1) * *a.xs) : 0.0f;
     }
 
     // ---- activation tile: global -> registers two k-steps ahead -> LDS, 16-byte loads
@@ -491,13 +569,14 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     // per-channel parameters of the lane's TN channels: 8-bit code layout decoded
     // arithmetically, epilogue factor (loaded here, off the tail of the kernel)
     bool int8[TN];
-    float cs[TN];
+    float cs[TN], zcs[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int n = n0 + nl + 32 * j;
         const ColPrep cp = n < N ? a.cols[n] : ColPrep{CHAM_W_NFMT, 0, 0.0f, 0.0f};
         int8[j] = CODE_BITS == 8 && is_8bit(cp.fmt);
         cs[j] = cp.colscale;
+        zcs[j] = (AF == kAInt8 && zc != 0.0f && n < N) ? zc * a.colsum[n] : 0.0f;
     }
     auto decode = [&](const Rec& r, int j, int s) __attribute__((always_inline)) -> half8 {
         if (CODE_BITS == 4) {
@@ -622,23 +701,26 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
         for (int j = 0; j < TN; ++j) {
             const int n = n0 + nl + 32 * j;
             float* base = out + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
+            // (acc rs) cs, plus the zero-point correction of INT8-asym activations
+            auto outv = [&](int r) __attribute__((always_inline)) {
+                const float v = (acc[i][j][r] * rs[r]) * cs[j];
+                return AF == kAInt8 ? v + zcs[j] : v;
+            };
             if (full && a.splits > 1) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = (acc[i][j][r] * rs[r]) * cs[j];
+                for (int r = 0; r < 16; ++r) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = outv(r);
             } else if (full) {
                 // the output is not read again here: non-temporal stores keep the L2 for the
                 // operand tiles other workgroups still read (partials, read back by the
                 // reduction, take ordinary stores)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    __builtin_nontemporal_store((acc[i][j][r] * rs[r]) * cs[j],
-                                                &base[(int64_t)(8 * (r >> 2) + (r & 3)) * N]);
+                    __builtin_nontemporal_store(outv(r), &base[(int64_t)(8 * (r >> 2) + (r & 3)) * N]);
             } else if (n < N) {
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int ml = 32 * i + 8 * (r >> 2) + 4 * h + (r & 3);
-                    if (ml < rows) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = (acc[i][j][r] * rs[r]) * cs[j];
+                    if (ml < rows) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = outv(r);
                 }
             }
         }
@@ -823,14 +905,31 @@ int64_t record_bytes(int64_t N, int64_t K) { return N * (K / BK) * 2 * 64; }
 
 using namespace cham;
 
+// The packed layout: ColPrep[N], the column sums [N], then the records.
 extern "C" size_t cham_packed_bytes(int64_t N, int64_t K) {
     if (N < 1 || K < 1) return 0;
-    return align256((size_t)N * sizeof(ColPrep)) + (size_t)record_bytes(N, K);
+    return align256((size_t)N * sizeof(ColPrep)) + align256((size_t)N * 4) + (size_t)record_bytes(N, K);
 }
 
-// Record pre-pass arguments of one searched weight writing into cols / rec (device), and
-// the workgroups it takes.
-static RecArgs record_args(const cham_wq* wq, ColPrep* cols, uint4* rec, int* wgs) {
+struct Layout {
+    ColPrep* cols;
+    float* colsum;
+    uint4* rec;
+};
+static Layout layout_at(void* p, int64_t N) {
+    char* c = (char*)p;
+    Layout l;
+    l.cols = (ColPrep*)c;
+    c += align256((size_t)N * sizeof(ColPrep));
+    l.colsum = (float*)c;
+    c += align256((size_t)N * 4);
+    l.rec = (uint4*)c;
+    return l;
+}
+
+// Record pre-pass arguments of one searched weight writing into the layout L (device),
+// and the workgroups it takes.
+static RecArgs record_args(const cham_wq* wq, const Layout& L, int* wgs) {
     const uint32_t mask = wq->palette_mask;
     const int N = (int)wq->N, K = (int)wq->K;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
@@ -843,17 +942,20 @@ static RecArgs record_args(const cham_wq* wq, ColPrep* cols, uint4* rec, int* wg
     *wgs = nblk * ((nst + rchunk - 1) / rchunk);
     // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
     return RecArgs{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
-                   mask, N, K, wq->code_bits, rchunk, cols, rec};
+                   mask, N, K, wq->code_bits, rchunk, L.cols, L.colsum, L.rec};
 }
 
-static void launch_records(const cham_wq* wq, ColPrep* cols, uint4* rec, hipStream_t s) {
+static int colsum_wgs(int64_t N) { return (int)((N + 3) / 4); }
+
+static void launch_records(const cham_wq* wq, const Layout& L, hipStream_t s) {
     RecBatch B;
     B.nl = 1;
     B.ng = 0;
     int wgs = 0;
-    B.r[0] = record_args(wq, cols, rec, &wgs);
+    B.r[0] = record_args(wq, L, &wgs);
+    B.cs_end[0] = colsum_wgs(wq->N);
     B.wg_end[0] = wgs;
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)wgs), dim3(256), 0, s, B);
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(wgs + B.cs_end[0])), dim3(256), 0, s, B);
 }
 
 // Writes the packed layout of n searched weights (called by the search entry points, which
@@ -864,25 +966,26 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
         RecBatch B;
         B.nl = std::min(kRecBatchMax, n - i0);
         B.ng = 0;
-        int total = 0;
+        int total = 0, cs = 0;
         for (int j = 0; j < B.nl; ++j) {
             const cham_wq* wq = wqs[i0 + j];
-            char* p = (char*)wq->packed;
             int wgs = 0;
-            B.r[j] = record_args(wq, (ColPrep*)p, (uint4*)(p + align256((size_t)wq->N * sizeof(ColPrep))), &wgs);
+            B.r[j] = record_args(wq, layout_at(wq->packed, wq->N), &wgs);
             total += wgs;
             B.wg_end[j] = total;
+            cs += colsum_wgs(wq->N);
+            B.cs_end[j] = cs;
             if (wq->perm || wq->group_off) B.g[B.ng++] = GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off};
         }
-        hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + B.ng)), dim3(256), 0, s, B);
+        hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + cs + B.ng)), dim3(256), 0, s, B);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;
 }
 
 size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    return align256((size_t)M * (size_t)K * 2) + align256((size_t)M * 4) + align256((size_t)N * sizeof(ColPrep)) +
-           align256((size_t)record_bytes(N, K)) + split_bytes(M, N, K);
+    return align256((size_t)M * (size_t)K * 2) + align256((size_t)M * 4) + align256(cham_packed_bytes(N, K)) +
+           split_bytes(M, N, K);
 }
 
 extern "C" int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bits, int32_t* out, int32_t out_len) {
@@ -939,15 +1042,10 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     w += align256((size_t)M * (size_t)K * 2);
     float* rowscale = (float*)w;
     w += align256((size_t)M * 4);
-    ColPrep* cols = (ColPrep*)w;
-    w += align256((size_t)N * sizeof(ColPrep));
-    uint4* rec = (uint4*)w;
-    w += align256((size_t)record_bytes(N, K));
+    // the search's packed layout replaces the pre-pass
+    const Layout lay = layout_at(wq->packed ? wq->packed : (void*)w, N);
+    w += align256(cham_packed_bytes(N, K));
     float* part = (float*)w;
-    if (wq->packed) {  // the search's packed layout replaces the pre-pass
-        cols = (ColPrep*)wq->packed;
-        rec = (uint4*)((char*)wq->packed + align256((size_t)N * sizeof(ColPrep)));
-    }
 
     if (amx) {
         PrepArgs p{xq->codes, xq->e8m0, xq->fmt, M, K, code_bits == 4, Xh, rowscale};
@@ -955,7 +1053,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
 
-    if (!wq->packed) launch_records(wq, cols, rec, s);
+    if (!wq->packed) launch_records(wq, lay, s);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;
@@ -964,8 +1062,9 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     a.xc = xq->codes;
     a.xs = xq->scale;
     a.xz = xq->zero;
-    a.cols = cols;
-    a.rec = rec;
+    a.cols = lay.cols;
+    a.colsum = lay.colsum;
+    a.rec = lay.rec;
     a.Y = Y;
     a.M = M;
     a.N = N;

@@ -54,9 +54,7 @@ __global__ __launch_bounds__(kQThreads) void minmax_partial_kernel(const float* 
 // ScaleZP (App. A.7) for the per-tensor formats.
 CHAM_DEV void scale_zp(int fmt, float lo, float hi, float* s, float* z) {
     if (fmt == CHAM_A_INT8_ASYM) {
-        float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
-        *s = floor_scale((h0 - l0) / 255.0f);
-        *z = clampf(rne(-l0 / *s), 0.0f, 255.0f);
+        int_asym_scale_zp(lo, hi, 255.0f, s, z);
     } else if (fmt == CHAM_A_FP8_E4M3) {
         *s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
         *z = 0.0f;

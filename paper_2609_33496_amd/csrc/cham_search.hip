@@ -31,7 +31,7 @@ struct SearchArgs {
     uint8_t* fmt;
     uint8_t* codes;
     float* scale;
-    int32_t* zero;
+    float* zero;
     float* nf4a;
     uint8_t* e8;
     double* err;
@@ -212,12 +212,22 @@ CHAM_DEV float chunk_err(const float (&w)[4], const RowParams& p, float blk32, f
         const float s = F == CHAM_W_INT8_ASYM ? p.s_as8 : p.s_as4;
         const float z = F == CHAM_W_INT8_ASYM ? p.z_as8 : p.z_as4;
         const float L = F == CHAM_W_INT8_ASYM ? 255.0f : 15.0f;
+        if (fabsf(z) <= 0x1p23f) {  // wavefront-uniform (one channel per wavefront)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            // clamp(round(w r) + z, 0, L) - z == clamp(round(w r), -z, L - z) on these integers
-            const float u = __builtin_amdgcn_fmed3f(rne(w[j] * r), -z, L - z);
-            const float d = w[j] - u * s;
-            e = __builtin_fmaf(d, d, e);
+            for (int j = 0; j < 4; ++j) {
+                // clamp(round(w r) + z, 0, L) - z == clamp(round(w r), -z, L - z): with |z| <= 2^23
+                // every integer here is exact in binary32
+                const float u = __builtin_amdgcn_fmed3f(rne(w[j] * r), -z, L - z);
+                const float d = w[j] - u * s;
+                e = __builtin_fmaf(d, d, e);
+            }
+        } else {  // a zero point beyond 2^23: the sums round, so each step as the format states it
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float q = __builtin_amdgcn_fmed3f(rne(w[j] * r) + z, 0.0f, L);
+                const float d = w[j] - (q - z) * s;
+                e = __builtin_fmaf(d, d, e);
+            }
         }
     } else if (F == CHAM_W_INT8_SYM || F == CHAM_W_INT4_SYM) {
         const float r = F == CHAM_W_INT8_SYM ? p.r_sym8 : p.r_sym4;
@@ -404,13 +414,10 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     RowParams p;
     p.s_sym8 = floor_scale(amax / 127.0f); p.r_sym8 = 1.0f / p.s_sym8;
     p.s_sym4 = floor_scale(amax / 7.0f);   p.r_sym4 = 1.0f / p.s_sym4;
-    {
-        float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
-        p.s_as8 = floor_scale((h0 - l0) / 255.0f); p.r_as8 = 1.0f / p.s_as8;
-        p.z_as8 = clampf(rne(-l0 / p.s_as8), 0.0f, 255.0f);
-        p.s_as4 = floor_scale((h0 - l0) / 15.0f);  p.r_as4 = 1.0f / p.s_as4;
-        p.z_as4 = clampf(rne(-l0 / p.s_as4), 0.0f, 15.0f);
-    }
+    int_asym_scale_zp(lo, hi, 255.0f, &p.s_as8, &p.z_as8);
+    p.r_as8 = 1.0f / p.s_as8;
+    int_asym_scale_zp(lo, hi, 15.0f, &p.s_as4, &p.z_as4);
+    p.r_as4 = 1.0f / p.s_as4;
     p.s_fp4 = floor_scale(amax / 6.0f); p.r_fp4 = 1.0f / p.s_fp4;
 
     // ---- binary32 error sums of every enabled format, one fused pass
@@ -517,12 +524,11 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     const int f = best;
     if (lane == 0 && part == 0) {
         a.fmt[n] = (uint8_t)f;
-        float s = 0.0f;
-        int32_t z = 0;
+        float s = 0.0f, z = 0.0f;
         if (f == CHAM_W_INT8_SYM) s = p.s_sym8;
         else if (f == CHAM_W_INT4_SYM) s = p.s_sym4;
-        else if (f == CHAM_W_INT8_ASYM) { s = p.s_as8; z = (int32_t)p.z_as8; }
-        else if (f == CHAM_W_INT4_ASYM) { s = p.s_as4; z = (int32_t)p.z_as4; }
+        else if (f == CHAM_W_INT8_ASYM) { s = p.s_as8; z = p.z_as8; }
+        else if (f == CHAM_W_INT4_ASYM) { s = p.s_as4; z = p.z_as4; }
         else if (f == CHAM_W_FP4) s = p.s_fp4;
         a.scale[n] = s;
         a.zero[n] = z;

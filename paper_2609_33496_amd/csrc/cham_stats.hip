@@ -251,9 +251,7 @@ __global__ __launch_bounds__(kLutThreads) void lut_kernel(LutArgs a) {
         if (n != 0.0) {
             const float lo = a.lohi[2 * i], hi = a.lohi[2 * i + 1];
             if (f == CHAM_A_INT8_ASYM) {
-                float l0 = fminf(lo, 0.0f), h0 = fmaxf(hi, 0.0f);
-                s = floor_scale((h0 - l0) / 255.0f);
-                z = clampf(rne(-l0 / s), 0.0f, 255.0f);
+                int_asym_scale_zp(lo, hi, 255.0f, &s, &z);
             } else if (f == CHAM_A_FP8_E4M3) {
                 s = floor_scale(fmaxf(fabsf(lo), fabsf(hi)) / 448.0f);
             } else if (f == CHAM_A_FP8_E5M2) {
