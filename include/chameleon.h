@@ -222,12 +222,14 @@ int32_t cham_bucket(int32_t t, int32_t T, int32_t B);
  * 3. activation quantization (Alg. 2 static / Alg. 3 dynamic)
  * ------------------------------------------------------------------------------------- */
 typedef struct cham_aq {
-    int64_t M, K;     /* X is [M][K]                                                         */
-    int32_t fmt;      /* activation format used (filled in by the quantize call)              */
-    uint8_t* codes;   /* [M][K] INT8-asym unsigned q, FP8 / MXFP8 codes, MXINT8 two's compl.  */
-    uint8_t* e8m0;    /* [M][K/32] biased block exponents (MX formats; may be NULL otherwise) */
-    float* scale;     /* [1] the scale s used (1 for MX formats)                              */
-    float* zero;      /* [1] the zero point z used (0 unless INT8-asym)                       */
+    int64_t M, K;      /* X is [M][K]                                                        */
+    int32_t fmt;       /* activation format used (filled in by the quantize call)             */
+    int32_t nsamples;  /* S >= 1 samples of M/S consecutive rows each (M % S == 0), e.g. the
+                          two halves of a CFG-doubled batch; each has its own (s, z)          */
+    uint8_t* codes;    /* [M][K] INT8-asym unsigned q, FP8 / MXFP8 codes, MXINT8 two's compl. */
+    uint8_t* e8m0;     /* [M][K/32] biased block exponents (MX formats; may be NULL otherwise)*/
+    float* scale;      /* [S] the scale s of each sample (1 for MX formats)                   */
+    float* zero;       /* [S] the zero point z of each sample (0 unless INT8-asym)            */
 } cham_aq;
 
 /* Quantize X [M][K] (device, finite binary32, 16-byte aligned; out->codes 4-byte aligned)
@@ -238,9 +240,11 @@ typedef struct cham_aq {
  *   MXFP8      per 32-block E = floor(log2 amax) (the paper's exponent: values in (-2, 2)),
  *              e = E4M3(x / 2^E)
  *   MXINT8     per 32-block E = floor(log2 amax), k = clamp(round(x 2^(6-E)), +-127)
- * Static (dynamic = 0): s = *s_dev, z = *z_dev (device pointers, e.g. LUT entries).
- * Dynamic (dynamic = 1): (s, z) = ScaleZP(fmt, min X, max X) of this tensor; s_dev/z_dev
- * are ignored.  The (s, z) used are written to out->scale / out->zero.  ws: CHAM_OP_QUANT_ACT
+ * Static (dynamic = 0): s = *s_dev, z = *z_dev (device pointers, e.g. LUT entries), the same
+ * for every sample.  Dynamic (dynamic = 1, Alg. 3's per-sample, per-forward micro-scaling):
+ * each of the out->nsamples samples takes (s, z) = ScaleZP(fmt, min, max) of its own rows
+ * (one sample = per-tensor); s_dev/z_dev are ignored.  The (s, z) used are written to
+ * out->scale[S] / out->zero[S].  1 <= nsamples <= 1024.  ws: CHAM_OP_QUANT_ACT
  * bytes.  Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE (K % 32 for MX), CHAM_EWORKSPACE,
  * CHAM_EHIP. */
 int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev,

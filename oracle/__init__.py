@@ -224,6 +224,30 @@ def quantize_act_dynamic(X: np.ndarray, fmt: int, want_xhat: bool = False):
     return codes, e8, xh, s, z
 
 
+def quantize_act_per_sample(X: np.ndarray, fmt: int, nsamples: int, want_xhat: bool = False):
+    """Alg. 3 with per-sample micro-scaling (Sec. 4.6 (ii)): X [M, K] holds nsamples samples of
+    M / nsamples consecutive rows; each sample's (s, z) is ScaleZP of its own min / max, and its
+    rows are quantized with them.  Returns (codes, e8m0, xhat or None, s [S], z [S])."""
+    X = _f32(X)
+    M, K = X.shape
+    if nsamples < 1 or M % nsamples:
+        raise ValueError("oracle: nsamples must divide M")
+    rows = M // nsamples
+    codes = np.zeros((M, K), np.uint8)
+    e8 = np.zeros((M, K // 32), np.uint8)
+    xh = np.zeros((M, K), np.float32) if want_xhat else None
+    s_all = np.zeros(nsamples, np.float32)
+    z_all = np.zeros(nsamples, np.float32)
+    for b in range(nsamples):
+        sl = slice(b * rows, (b + 1) * rows)
+        c, e, h, s, z = quantize_act_dynamic(X[sl], fmt, want_xhat)
+        codes[sl], e8[sl] = c, e
+        if want_xhat:
+            xh[sl] = h
+        s_all[b], z_all[b] = s, z
+    return codes, e8, xh, s_all, z_all
+
+
 def dequant_act(codes: np.ndarray, e8: np.ndarray, fmt: int, s=1.0, z=0.0) -> np.ndarray:
     codes = np.ascontiguousarray(codes, np.uint8)
     M, K = codes.shape

@@ -59,8 +59,8 @@ class _LUT(ctypes.Structure):
 
 
 class _AQ(ctypes.Structure):
-    _fields_ = [("M", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int32), ("codes", _P),
-                ("e8m0", _P), ("scale", _P), ("zero", _P)]
+    _fields_ = [("M", ctypes.c_int64), ("K", ctypes.c_int64), ("fmt", ctypes.c_int32), ("nsamples", ctypes.c_int32),
+                ("codes", _P), ("e8m0", _P), ("scale", _P), ("zero", _P)]
 
 
 _lib = None
@@ -386,26 +386,31 @@ class AQ:
     fmt: int
     codes: torch.Tensor              # [M, K] u8
     e8m0: Optional[torch.Tensor]     # [M, K/32] u8
-    scale: torch.Tensor              # [1] f32
-    zero: torch.Tensor               # [1] f32
+    scale: torch.Tensor              # [nsamples] f32
+    zero: torch.Tensor               # [nsamples] f32
+    nsamples: int = 1                # samples of M / nsamples consecutive rows
 
     def struct(self):
-        return _AQ(self.M, self.K, self.fmt, _ptr(self.codes), _ptr(self.e8m0), _ptr(self.scale), _ptr(self.zero))
+        return _AQ(self.M, self.K, self.fmt, self.nsamples, _ptr(self.codes), _ptr(self.e8m0), _ptr(self.scale),
+                   _ptr(self.zero))
 
 
-def alloc_aq(M: int, K: int, device="cuda", with_e8m0=True) -> AQ:
+def alloc_aq(M: int, K: int, device="cuda", with_e8m0=True, nsamples: int = 1) -> AQ:
     return AQ(M, K, -1, torch.empty((M, K), dtype=torch.uint8, device=device),
               torch.empty((M, K // 32), dtype=torch.uint8, device=device) if with_e8m0 else None,
-              torch.empty(1, dtype=torch.float32, device=device), torch.empty(1, dtype=torch.float32, device=device))
+              torch.empty(nsamples, dtype=torch.float32, device=device),
+              torch.empty(nsamples, dtype=torch.float32, device=device), nsamples)
 
 
 def quantize_act(X: torch.Tensor, fmt: int, dynamic: bool = True, s: Optional[torch.Tensor] = None,
-                 z: Optional[torch.Tensor] = None, out: Optional[AQ] = None, ws=None, stream=None) -> AQ:
-    """Quantize X [M, K]; static mode reads the scale/zero from device tensors s, z."""
+                 z: Optional[torch.Tensor] = None, out: Optional[AQ] = None, ws=None, stream=None,
+                 nsamples: int = 1) -> AQ:
+    """Quantize X [M, K]; static mode reads the scale/zero from device tensors s, z; dynamic
+    mode takes each of the nsamples row blocks' own range (per-sample scaling)."""
     _dev_tensor(X, torch.float32, "X")
     M, K = X.shape
     if out is None:
-        out = alloc_aq(M, K, X.device)
+        out = alloc_aq(M, K, X.device, nsamples=nsamples)
     ws, nb = _workspace(OP_QUANT_ACT, M, 0, K, X.device, ws)
     a = out.struct()
     _check(lib().cham_quantize_act(_ptr(X), fmt, int(dynamic), _ptr(s), _ptr(z), ctypes.byref(a), _ptr(ws), nb,
@@ -415,13 +420,13 @@ def quantize_act(X: torch.Tensor, fmt: int, dynamic: bool = True, s: Optional[to
 
 
 def quantize_act_lut(X: torch.Tensor, lut: LUT, layer: int, t: int, dynamic: bool = False,
-                     out: Optional[AQ] = None, ws=None, stream=None) -> AQ:
+                     out: Optional[AQ] = None, ws=None, stream=None, nsamples: int = 1) -> AQ:
     _dev_tensor(X, torch.float32, "X")
     if lut.F_host is None:
         lut.mirror()
     M, K = X.shape
     if out is None:
-        out = alloc_aq(M, K, X.device)
+        out = alloc_aq(M, K, X.device, nsamples=nsamples)
     ws, nb = _workspace(OP_QUANT_ACT, M, 0, K, X.device, ws)
     a, l = out.struct(), lut.struct()
     _check(lib().cham_quantize_act_lut(_ptr(X), ctypes.byref(l), ctypes.c_void_p(lut.F_host.data_ptr()), layer, t,

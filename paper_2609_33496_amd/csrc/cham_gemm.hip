@@ -408,8 +408,9 @@ struct GemmArgs {
     const _Float16* Xh;      // [M][K] (column order as above), MX activation formats
     const float* rowscale;   // [M], MX activation formats
     const uint8_t* xc;       // [M][K] activation codes, per-tensor formats
-    const float* xs;         // per-tensor activation scale (device scalar)
-    const float* xz;         // per-tensor activation zero point (device scalar)
+    const float* xs;         // activation scale per sample [M / rps] (per-tensor formats)
+    const float* xz;         // activation zero point per sample
+    int rps;                 // rows per sample
     const ColPrep* cols;     // [N]
     const float* colsum;     // [N] sum over k of the dequantized weights
     const uint4* rec;        // [K/64][N][2][pieces]
@@ -465,7 +466,8 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     constexpr int AQ = AF == kAF16 ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
     constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
     __shared__ uint4 lds[2][A_CH];
-    __shared__ float Rs[BM];
+    __shared__ __align__(16) float Rs[BM];
+    __shared__ __align__(16) float Rc[AF == kAInt8 ? BM : 4];
 
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
@@ -479,17 +481,35 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     const int kb = split * a.kchunk;
     const int nsteps = K / BK - kb < a.kchunk ? K / BK - kb : a.kchunk;
 
-    if (t < BM) Rs[t] = AF == kAF16 ? a.rowscale[t < rows ? m0 + t : m0] : *a.xs;
-    // INT8-asym: the codes are decoded as (1024 + c) - (1024 + z1) with z1 the zero point
+    // per-row activation scale (the row's sample's s; MX: the pre-pass's row scale).
+    // INT8-asym: codes are decoded as (1024 + c) - (1024 + z1) with z1 the sample's zero point
     // clamped to [-1024, 1024] (exact in half precision); the rest z - z1 (an integer, exact
     // in binary32) is taken out in the epilogue as -(z - z1) s times the channel's weight sum
-    half2v negz = {(_Float16)0.0f, (_Float16)0.0f};
-    float zc = 0.0f;
-    if (AF == kAInt8) {
-        const float za = *a.xz, z1 = clampf(za, -1024.0f, 1024.0f);
-        const _Float16 nz = (_Float16)(-(1024.0f + z1));
-        negz = half2v{nz, nz};
-        zc = split == 0 ? -((za - z1) * *a.xs) : 0.0f;
+    // (split 0 only).
+    if (t < BM) {
+        const int m = t < rows ? m0 + t : m0;
+        if (AF == kAF16) {
+            Rs[t] = a.rowscale[m];
+        } else {
+            Rs[t] = a.xs[m / a.rps];
+            if (AF == kAInt8) {
+                const float za = a.xz[m / a.rps], z1 = clampf(za, -1024.0f, 1024.0f);
+                Rc[t] = split == 0 ? -((za - z1) * a.xs[m / a.rps]) : 0.0f;
+            }
+        }
+    }
+    // the staging rows of this thread (row q >> 2 of load q = 256 i + t): their -(1024 + z1)
+    constexpr int AQ0 = AF == kAF16 ? 1 : (TM + 1) / 2;
+    half2v negz[AQ0];
+#pragma unroll
+    for (int i = 0; i < AQ0; ++i) {
+        negz[i] = half2v{(_Float16)0.0f, (_Float16)0.0f};
+        if (AF == kAInt8) {
+            const int r = (i * 256 + t) >> 2;
+            const int m = r < rows ? m0 + r : m0;
+            const _Float16 nz = (_Float16)(-(1024.0f + clampf(a.xz[m / a.rps], -1024.0f, 1024.0f)));
+            negz[i] = half2v{nz, nz};
+        }
     }
 
     // ---- activation tile: global -> registers two k-steps ahead -> LDS, 16-byte loads
@@ -528,8 +548,8 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
                 const int q = i * 256 + t;
                 if (q < BM * 4) {
                     const int r = q >> 2, c = 2 * (q & 3), sw = (r >> 1) & 7;
-                    lds[buf][r * 8 + (c ^ sw)] = decode_act8<AF>(S.v[i].x, S.v[i].y, perm4, negz);
-                    lds[buf][r * 8 + ((c + 1) ^ sw)] = decode_act8<AF>(S.v[i].z, S.v[i].w, perm4, negz);
+                    lds[buf][r * 8 + (c ^ sw)] = decode_act8<AF>(S.v[i].x, S.v[i].y, perm4, negz[i]);
+                    lds[buf][r * 8 + ((c + 1) ^ sw)] = decode_act8<AF>(S.v[i].z, S.v[i].w, perm4, negz[i]);
                 }
             }
         }
@@ -569,14 +589,14 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     // per-channel parameters of the lane's TN channels: 8-bit code layout decoded
     // arithmetically, epilogue factor (loaded here, off the tail of the kernel)
     bool int8[TN];
-    float cs[TN], zcs[TN];
+    float cs[TN], csum[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         const int n = n0 + nl + 32 * j;
         const ColPrep cp = n < N ? a.cols[n] : ColPrep{CHAM_W_NFMT, 0, 0.0f, 0.0f};
         int8[j] = CODE_BITS == 8 && is_8bit(cp.fmt);
         cs[j] = cp.colscale;
-        zcs[j] = (AF == kAInt8 && zc != 0.0f && n < N) ? zc * a.colsum[n] : 0.0f;
+        csum[j] = (AF == kAInt8 && n < N) ? a.colsum[n] : 0.0f;
     }
     auto decode = [&](const Rec& r, int j, int s) __attribute__((always_inline)) -> half8 {
         if (CODE_BITS == 4) {
@@ -691,11 +711,15 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     float* const out = a.splits > 1 ? a.part + (int64_t)split * a.M * N : a.Y;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
-        float rs[16];
+        float rs[16], rc[16];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const float4 v = *reinterpret_cast<const float4*>(&Rs[32 * i + 8 * q + 4 * h]);
             rs[4 * q] = v.x; rs[4 * q + 1] = v.y; rs[4 * q + 2] = v.z; rs[4 * q + 3] = v.w;
+            if (AF == kAInt8) {
+                const float4 c = *reinterpret_cast<const float4*>(&Rc[32 * i + 8 * q + 4 * h]);
+                rc[4 * q] = c.x; rc[4 * q + 1] = c.y; rc[4 * q + 2] = c.z; rc[4 * q + 3] = c.w;
+            }
         }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
@@ -704,7 +728,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
             // (acc rs) cs, plus the zero-point correction of INT8-asym activations
             auto outv = [&](int r) __attribute__((always_inline)) {
                 const float v = (acc[i][j][r] * rs[r]) * cs[j];
-                return AF == kAInt8 ? v + zcs[j] : v;
+                return AF == kAInt8 ? v + rc[r] * csum[j] : v;
             };
             if (full && a.splits > 1) {
 #pragma unroll
@@ -1011,6 +1035,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     if (!wq->fmt || !wq->codes || !wq->scale || !wq->zero) return CHAM_EINVAL;
     if (xq->M < 1 || wq->N < 1 || xq->K < 1 || xq->K != wq->K) return CHAM_EINVAL;
     if (xq->fmt < 0 || xq->fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
+    if (xq->nsamples < 1 || xq->M % xq->nsamples != 0) return CHAM_EINVAL;
     const uint32_t mask = wq->palette_mask;
     if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
     const int code_bits = (mask & 0x7u) ? 8 : 4;
@@ -1062,6 +1087,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
     a.xc = xq->codes;
     a.xs = xq->scale;
     a.xz = xq->zero;
+    a.rps = M / xq->nsamples;
     a.cols = lay.cols;
     a.colsum = lay.colsum;
     a.rec = lay.rec;

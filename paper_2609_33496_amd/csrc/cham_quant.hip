@@ -7,6 +7,8 @@
 // shuffle reduction and one lane writes the E8M0 byte.  Dynamic mode first reduces
 // min/max into per-workgroup partials (workspace); the quantize kernel folds them (min
 // and max are exact, so the result does not depend on the order).
+#include <algorithm>
+
 #include "cham_device.h"
 
 namespace cham {
@@ -16,16 +18,19 @@ constexpr int kQThreads = 256;
 constexpr int kQMaxBlocks = 1024;
 constexpr int kQLoads = 4;  // float4 loads in flight per thread
 
+// Per-sample launches: the grid is nbs workgroups per sample, sample-major; workgroup
+// j = blockIdx.x % nbs of sample blockIdx.x / nbs strides over that sample's float4s.
 // float4 index of load u of the thread's run starting at i0 (workgroup-strided)
 CHAM_DEV int64_t qidx(int64_t i0, int u) { return i0 + (int64_t)u * kQThreads; }
-CHAM_DEV int64_t qfirst() { return (int64_t)blockIdx.x * kQThreads * kQLoads + threadIdx.x; }
-CHAM_DEV int64_t qstep() { return (int64_t)gridDim.x * kQThreads * kQLoads; }
+CHAM_DEV int64_t qfirst(int nbs) { return (int64_t)(blockIdx.x % nbs) * kQThreads * kQLoads + threadIdx.x; }
+CHAM_DEV int64_t qstep(int nbs) { return (int64_t)nbs * kQThreads * kQLoads; }
 
-__global__ __launch_bounds__(kQThreads) void minmax_partial_kernel(const float* X, int64_t n, float2* part) {
+// n: elements per sample (a multiple of 4)
+__global__ __launch_bounds__(kQThreads) void minmax_partial_kernel(const float* X, int64_t n, int nbs, float2* part) {
     float lo = INFINITY, hi = -INFINITY;
     const int64_t nq = n >> 2;
-    const float4* X4 = reinterpret_cast<const float4*>(X);
-    for (int64_t i0 = qfirst(); i0 < nq; i0 += qstep()) {
+    const float4* X4 = reinterpret_cast<const float4*>(X) + (int64_t)(blockIdx.x / nbs) * nq;
+    for (int64_t i0 = qfirst(nbs); i0 < nq; i0 += qstep(nbs)) {
         float4 t[kQLoads];
 #pragma unroll
         for (int u = 0; u < kQLoads; ++u) {
@@ -69,26 +74,27 @@ CHAM_DEV void scale_zp(int fmt, float lo, float hi, float* s, float* z) {
 
 struct QArgs {
     const float* X;
-    int64_t n;          // M*K, multiple of 4
+    int64_t n;          // elements per sample (M/S * K), multiple of 4
+    int nbs;            // workgroups per sample
     int fmt;
     const float* s_dev;  // static
     const float* z_dev;
-    const float2* part;  // dynamic partials (or NULL)
-    int nparts;
+    const float2* part;  // dynamic: nbs partials per sample (or NULL)
     uint8_t* codes;
-    float* scale_out;
+    float* scale_out;    // [S]
     float* zero_out;
 };
 
 template <int FMT>
 __global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
     __shared__ float sh_s, sh_z;
+    const int sample = (int)blockIdx.x / a.nbs;
     if (threadIdx.x < kWave) {
         float s, z;
         if (a.part) {
             float lo = INFINITY, hi = -INFINITY;
-            for (int i = threadIdx.x; i < a.nparts; i += kWave) {
-                float2 p = a.part[i];
+            for (int i = threadIdx.x; i < a.nbs; i += kWave) {
+                float2 p = a.part[(int64_t)sample * a.nbs + i];
                 lo = fminf(lo, p.x);
                 hi = fmaxf(hi, p.y);
             }
@@ -102,16 +108,16 @@ __global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
         if (threadIdx.x == 0) {
             sh_s = s;
             sh_z = z;
-            if (blockIdx.x == 0) { *a.scale_out = s; *a.zero_out = z; }
+            if ((int)blockIdx.x % a.nbs == 0) { a.scale_out[sample] = s; a.zero_out[sample] = z; }
         }
     }
     __syncthreads();
     const float s = sh_s, z = sh_z;
     const float r = 1.0f / s;
     const int64_t nq = a.n >> 2;
-    const float4* X4 = reinterpret_cast<const float4*>(a.X);
-    uint32_t* C4 = reinterpret_cast<uint32_t*>(a.codes);
-    for (int64_t i0 = qfirst(); i0 < nq; i0 += qstep()) {
+    const float4* X4 = reinterpret_cast<const float4*>(a.X) + (int64_t)sample * nq;
+    uint32_t* C4 = reinterpret_cast<uint32_t*>(a.codes) + (int64_t)sample * nq;
+    for (int64_t i0 = qfirst(a.nbs); i0 < nq; i0 += qstep(a.nbs)) {
         float4 t[kQLoads];
 #pragma unroll
         for (int u = 0; u < kQLoads; ++u) {
@@ -144,15 +150,17 @@ __global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
 // 8-lane groups stay aligned because the stride is a multiple of 64.
 template <int FMT>
 __global__ __launch_bounds__(kQThreads) void quant_mx_kernel(const float* X, int64_t n, uint8_t* codes, uint8_t* e8,
-                                                             float* scale_out, float* zero_out) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) { *scale_out = 1.0f; *zero_out = 0.0f; }
+                                                             float* scale_out, float* zero_out, int nsamples) {
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < nsamples; i += kQThreads) { scale_out[i] = 1.0f; zero_out[i] = 0.0f; }
+    const int nbs = gridDim.x;  // the block exponents need no per-sample scale: one range
     const int64_t nq = n >> 2;  // multiple of 8
     const float4* X4 = reinterpret_cast<const float4*>(X);
     uint32_t* C4 = reinterpret_cast<uint32_t*>(codes);
     // the same trip count for every lane: the 8-lane reductions run with whole wavefronts
-    const int64_t iters = (nq + qstep() - 1) / qstep();
+    const int64_t iters = (nq + qstep(nbs) - 1) / qstep(nbs);
     for (int64_t it = 0; it < iters; ++it) {
-        const int64_t i0 = qfirst() + it * qstep();
+        const int64_t i0 = qfirst(nbs) + it * qstep(nbs);
         float4 t[kQLoads];
 #pragma unroll
         for (int u = 0; u < kQLoads; ++u) {
@@ -198,59 +206,78 @@ int qblocks(int64_t nq) {
 
 using namespace cham;
 
-size_t cham_quant_workspace_bytes(int64_t n) { return sizeof(float2) * (size_t)qblocks(n >> 2); }
+// dynamic scales: at most kQMaxBlocks min/max partials in all (float2 each)
+size_t cham_quant_workspace_bytes(int64_t n) { return n > 0 ? sizeof(float2) * (size_t)kQMaxBlocks : 0; }
 
-extern "C" int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
-                                 cham_aq* out, void* ws, size_t ws_bytes, void* stream) {
+// Checks the arguments of a quantize call (no launch).
+static int quant_check(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
+                       const cham_aq* out) {
     if (!X || !out || !out->codes || !out->scale || !out->zero) return CHAM_EINVAL;
     if (out->M < 1 || out->K < 1) return CHAM_EINVAL;
+    if (out->nsamples < 1 || out->nsamples > kQMaxBlocks || out->M % out->nsamples != 0) return CHAM_EINVAL;
     if (fmt < 0 || fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
     if (out->K % 32 != 0) return CHAM_ESHAPE;
     if (((uintptr_t)X & 15u) != 0 || ((uintptr_t)out->codes & 3u) != 0) return CHAM_EINVAL;
     const bool mx = fmt == CHAM_A_MXFP8_E4M3 || fmt == CHAM_A_MXINT8;
     if (mx && !out->e8m0) return CHAM_EINVAL;
     if (!mx && !dynamic && (!s_dev || !z_dev)) return CHAM_EINVAL;
+    return CHAM_OK;
+}
+
+// The launches of a checked quantize call; part: kQMaxBlocks float2 of device scratch
+// (used when dynamic).
+static int quant_launch(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
+                        cham_aq* out, float2* part, hipStream_t s) {
     const int64_t n = out->M * out->K;
-    hipStream_t s = (hipStream_t)stream;
+    const int S = out->nsamples;
     out->fmt = fmt;
-    const int nb = qblocks(n >> 2);
-    if (mx) {
+    if (fmt == CHAM_A_MXFP8_E4M3 || fmt == CHAM_A_MXINT8) {
+        const int nb = qblocks(n >> 2);
         if (fmt == CHAM_A_MXFP8_E4M3)
             hipLaunchKernelGGL(quant_mx_kernel<CHAM_A_MXFP8_E4M3>, dim3(nb), dim3(kQThreads), 0, s, X, n, out->codes,
-                               out->e8m0, out->scale, out->zero);
+                               out->e8m0, out->scale, out->zero, S);
         else
             hipLaunchKernelGGL(quant_mx_kernel<CHAM_A_MXINT8>, dim3(nb), dim3(kQThreads), 0, s, X, n, out->codes,
-                               out->e8m0, out->scale, out->zero);
+                               out->e8m0, out->scale, out->zero, S);
         CHAM_CHECK_LAUNCH();
         return CHAM_OK;
     }
+    const int64_t ns = n / S;  // elements per sample, a multiple of 32
+    const int nbs = std::max(1, std::min(qblocks(ns >> 2), kQMaxBlocks / S));
     QArgs a;
     a.X = X;
-    a.n = n;
+    a.n = ns;
+    a.nbs = nbs;
     a.fmt = fmt;
     a.s_dev = s_dev;
     a.z_dev = z_dev;
     a.part = nullptr;
-    a.nparts = 0;
     a.codes = out->codes;
     a.scale_out = out->scale;
     a.zero_out = out->zero;
+    const dim3 grid((unsigned)(nbs * S));
     if (dynamic) {
-        if (!ws || ws_bytes < sizeof(float2) * (size_t)nb) return CHAM_EWORKSPACE;
-        float2* part = (float2*)ws;
-        hipLaunchKernelGGL(minmax_partial_kernel, dim3(nb), dim3(kQThreads), 0, s, X, n, part);
+        hipLaunchKernelGGL(minmax_partial_kernel, grid, dim3(kQThreads), 0, s, X, ns, nbs, part);
         CHAM_CHECK_LAUNCH();
         a.part = part;
-        a.nparts = nb;
     }
     if (fmt == CHAM_A_INT8_ASYM)
-        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_INT8_ASYM>, dim3(nb), dim3(kQThreads), 0, s, a);
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_INT8_ASYM>, grid, dim3(kQThreads), 0, s, a);
     else if (fmt == CHAM_A_FP8_E4M3)
-        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E4M3>, dim3(nb), dim3(kQThreads), 0, s, a);
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E4M3>, grid, dim3(kQThreads), 0, s, a);
     else
-        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E5M2>, dim3(nb), dim3(kQThreads), 0, s, a);
+        hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E5M2>, grid, dim3(kQThreads), 0, s, a);
     CHAM_CHECK_LAUNCH();
     return CHAM_OK;
+}
+
+extern "C" int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
+                                 cham_aq* out, void* ws, size_t ws_bytes, void* stream) {
+    const int rc = quant_check(X, fmt, dynamic, s_dev, z_dev, out);
+    if (rc != CHAM_OK) return rc;
+    const bool mx = fmt == CHAM_A_MXFP8_E4M3 || fmt == CHAM_A_MXINT8;
+    if (dynamic && !mx && (!ws || ws_bytes < cham_quant_workspace_bytes(out->M * out->K))) return CHAM_EWORKSPACE;
+    return quant_launch(X, fmt, dynamic, s_dev, z_dev, out, (float2*)ws, (hipStream_t)stream);
 }
 
 extern "C" int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_host, int32_t layer,

@@ -98,16 +98,19 @@ def test_other_argument_errors():
     assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk_bad, 2, ctypes.byref(st), P(256), 1 << 30, None) == cham.EINVAL
     assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk, 0, ctypes.byref(st), P(256), 1 << 30, None) == cham.EINVAL
     assert L.cham_act_stats_accumulate_batch(xs, ne, ly, bk, 2, ctypes.byref(st), P(256), 64, None) == cham.EWORKSPACE
-    aq = cham._AQ(4, 64, 0, P(16), P(16), P(16), P(16))
+    aq = cham._AQ(4, 64, 0, 1, P(16), P(16), P(16), P(16))
     assert L.cham_quantize_act(P(16), 7, 1, None, None, ctypes.byref(aq), P(256), 1 << 20, None) == cham.EFORMAT
-    aq48 = cham._AQ(4, 48, 0, P(16), P(16), P(16), P(16))
+    aq48 = cham._AQ(4, 48, 0, 1, P(16), P(16), P(16), P(16))
     assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aq48), P(256), 1 << 20, None) == cham.ESHAPE
     assert L.cham_quantize_act(P(16), 1, 0, None, None, ctypes.byref(aq), None, 0, None) == cham.EINVAL
     assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aq), None, 0, None) == cham.EWORKSPACE
+    for ns in (0, 3, 1025):  # samples: at least one, dividing M, at most 1024
+        aqs = cham._AQ(4 if ns != 1025 else 2050, 64, 0, ns, P(16), P(16), P(16), P(16))
+        assert L.cham_quantize_act(P(16), 1, 1, None, None, ctypes.byref(aqs), P(256), 1 << 20, None) == cham.EINVAL
     w = _wq(code_bits=4)
-    aqk = cham._AQ(4, 128, 1, P(16), P(16), P(16), P(16))  # K = 128 vs wq K = 64
+    aqk = cham._AQ(4, 128, 1, 1, P(16), P(16), P(16), P(16))  # K = 128 vs wq K = 64
     assert L.cham_mixed_linear(ctypes.byref(aqk), ctypes.byref(w), P(16), None, 0, None) == cham.EINVAL  # K mismatch
-    aqf = cham._AQ(4, 64, 9, P(16), P(16), P(16), P(16))
+    aqf = cham._AQ(4, 64, 9, 1, P(16), P(16), P(16), P(16))
     assert L.cham_mixed_linear(ctypes.byref(aqf), ctypes.byref(w), P(16), None, 0, None) == cham.EFORMAT
     w8 = _wq(code_bits=4, palette_mask=cham.MASK_W8)
     assert L.cham_mixed_linear(ctypes.byref(aq), ctypes.byref(w8), P(16), None, 0, None) == cham.EFORMAT

@@ -365,3 +365,47 @@ def test_act_dequant_inverts_codes():
         c2, e82, xh2 = oracle.quantize_act(xh, fmt, s, z, want_xhat=True)
         if fmt != oracle.A_MXFP8:
             assert np.array_equal(xh2, xh), fmt
+
+
+# ---------------------------------------------------------------------------------------
+# per-sample dynamic scaling (Alg. 3: lo, hi = min, max per sample and forward; Sec. 4.6 (ii))
+# ---------------------------------------------------------------------------------------
+def test_per_sample_scaling_hand_computed():
+    """Two samples whose ranges give exact scales: INT8-asym [-128, 127] -> s = 1, z = 128 and
+    [2, 257] -> s = 1, z = -2; E4M3 amax 448 -> s = 1 and amax 896 -> s = 2."""
+    K = 64
+    X = np.zeros((4, K), np.float32)
+    X[0:2] = np.linspace(-128, 127, 2 * K).reshape(2, K)
+    X[2:4] = np.linspace(2, 257, 2 * K).reshape(2, K)
+    codes, _, xh, s, z = oracle.quantize_act_per_sample(X, oracle.A_INT8_ASYM, 2, want_xhat=True)
+    assert list(s) == [1.0, 1.0] and list(z) == [128.0, -2.0]
+    assert codes[0, 0] == 0 and codes[1, -1] == 255 and codes[2, 0] == 0 and codes[3, -1] == 255
+    assert xh[0, 0] == -128 and xh[1, -1] == 127 and xh[2, 0] == 2 and xh[3, -1] == 257
+    Y = np.zeros((4, K), np.float32)
+    Y[0:2, 0], Y[0:2, 1] = 448.0, -3.0
+    Y[2:4, 0], Y[2:4, 1] = -896.0, 3.0
+    codes, _, _, s, z = oracle.quantize_act_per_sample(Y, oracle.A_FP8_E4M3, 2)
+    assert list(s) == [1.0, 2.0] and list(z) == [0.0, 0.0]
+    assert codes[0, 0] == 0x7E and codes[2, 0] == 0xFE       # +-448: the largest finite code
+    assert codes[0, 1] == 0xC4 and codes[2, 1] == 0x3C       # -3 at s = 1; 3/2 = 1.5 at s = 2
+
+
+def test_per_sample_scaling_properties():
+    """One sample is the per-tensor path; samples are independent (reordering the samples
+    reorders scales and codes and changes nothing else); MX formats carry no scale."""
+    g = np.random.default_rng(30)
+    X = np.concatenate([g.normal(0, 1, (6, 96)), 40 + 5 * g.standard_t(3, (6, 96)),
+                        -0.01 * g.random((6, 96))]).astype(np.float32)
+    for fmt in range(5):
+        c1, e1, h1, s1, z1 = oracle.quantize_act_per_sample(X, fmt, 1, want_xhat=True)
+        c0, e0, h0, s0, z0 = oracle.quantize_act_dynamic(X, fmt, want_xhat=True)
+        assert np.array_equal(c1, c0) and np.array_equal(h1, h0) and s1[0] == s0 and z1[0] == z0
+        c, e, h, s, z = oracle.quantize_act_per_sample(X, fmt, 3, want_xhat=True)
+        Xp = np.concatenate([X[12:18], X[0:6], X[6:12]])
+        cp, ep, hp, sp, zp = oracle.quantize_act_per_sample(Xp, fmt, 3, want_xhat=True)
+        assert np.array_equal(cp, np.concatenate([c[12:18], c[0:6], c[6:12]]))
+        assert list(sp) == [s[2], s[0], s[1]] and list(zp) == [z[2], z[0], z[1]]
+        if fmt >= oracle.A_MXFP8:
+            assert np.all(s == 1) and np.all(z == 0) and np.array_equal(c, c0)
+        else:
+            assert len(set(s.tolist())) == 3  # three different ranges, three scales
