@@ -250,6 +250,18 @@ typedef struct cham_aq {
 int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev,
                       const float* z_dev, cham_aq* out, void* ws, size_t ws_bytes, void* stream);
 
+/* cham_quantize_act without a workspace argument, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and errors as cham_quantize_act; it calls no
+ * allocating routine.  The dynamic min/max partials live in an 8 KB array of device memory
+ * that the library holds on each GPU it runs on until the process ends; it is large enough
+ * for every size this call accepts (the launch caps its partials at 1024).  All calls on one
+ * GPU share that array: calls that overlap on one GPU (different streams, other threads)
+ * race and must be ordered by the caller.  Errors: as cham_quantize_act (without
+ * CHAM_EWORKSPACE); CHAM_EHIP also if the array's address cannot be obtained. */
+int cham_quantize_act_noalloc(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev,
+                              const float* z_dev, cham_aq* out, void* stream);
+
 /* The per-step runtime lookup of Alg. 2 / Alg. 3: b = cham_bucket(t, lut->T, lut->B), the
  * format is F_host[layer*B + b] (a host mirror of lut->F, copied once after calibration, so
  * no device synchronization is needed per step), and the scale/zero are read on the device

@@ -93,6 +93,7 @@ def lib():
     L.cham_quantize_act.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P, sz, _P]
     L.cham_quantize_act_lut.argtypes = [_P, ctypes.POINTER(_LUT), _P, i32, i32, i32, ctypes.POINTER(_AQ), _P, sz,
                                         _P]
+    L.cham_quantize_act_noalloc.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P]
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
     L.cham_workspace_bytes.restype = sz
@@ -101,7 +102,8 @@ def lib():
     L.cham_linear_plan.argtypes = [i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32), i32]
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
-                 "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_mixed_linear",
+                 "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_quantize_act_noalloc",
+                 "cham_mixed_linear",
                  "cham_linear_plan"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -415,6 +417,17 @@ def quantize_act(X: torch.Tensor, fmt: int, dynamic: bool = True, s: Optional[to
     a = out.struct()
     _check(lib().cham_quantize_act(_ptr(X), fmt, int(dynamic), _ptr(s), _ptr(z), ctypes.byref(a), _ptr(ws), nb,
                                    _stream(stream)), "quantize_act")
+    out.fmt = a.fmt
+    return out
+
+
+def quantize_act_noalloc(X: torch.Tensor, fmt: int, dynamic: bool, s: Optional[torch.Tensor], z: Optional[torch.Tensor],
+                         out: AQ, stream=None) -> AQ:
+    """cham_quantize_act_noalloc: the caller passes the output buffers; no workspace."""
+    _dev_tensor(X, torch.float32, "X")
+    a = out.struct()
+    _check(lib().cham_quantize_act_noalloc(_ptr(X), fmt, int(dynamic), _ptr(s), _ptr(z), ctypes.byref(a),
+                                           _stream(stream)), "quantize_act_noalloc")
     out.fmt = a.fmt
     return out
 

@@ -8,6 +8,7 @@
 // min/max into per-workgroup partials (workspace); the quantize kernel folds them (min
 // and max are exact, so the result does not depend on the order).
 #include <algorithm>
+#include <atomic>
 
 #include "cham_device.h"
 
@@ -269,6 +270,36 @@ static int quant_launch(const float* X, int32_t fmt, int32_t dynamic, const floa
         hipLaunchKernelGGL(quant_tensor_kernel<CHAM_A_FP8_E5M2>, grid, dim3(kQThreads), 0, s, a);
     CHAM_CHECK_LAUNCH();
     return CHAM_OK;
+}
+
+// ---- allocation-free variant: the dynamic min/max partials go to a file-scope device array
+// (kQMaxBlocks float2 = 8 KB on every device the library runs on, held until the process
+// ends), addressed through hipGetSymbolAddress once per device.
+static __device__ __align__(256) float2 scratch[kQMaxBlocks];
+
+// Device address of this device's copy of scratch (queried on the first call on each
+// device, with that device current; concurrent first calls store the same address).
+static float2* scratch_ptr() {
+    static std::atomic<void*> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    void* p = cached[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        cached[dev].store(p, std::memory_order_release);
+    }
+    return (float2*)p;
+}
+
+extern "C" int cham_quantize_act_noalloc(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev,
+                                         const float* z_dev, cham_aq* out, void* stream) {
+    const int rc = quant_check(X, fmt, dynamic, s_dev, z_dev, out);
+    if (rc != CHAM_OK) return rc;
+    float2* part = scratch_ptr();
+    if (!part) return CHAM_EHIP;
+    // every call needs at most kQMaxBlocks partials (the launch caps its workgroups), so no
+    // size exceeds the array
+    return quant_launch(X, fmt, dynamic, s_dev, z_dev, out, part, (hipStream_t)stream);
 }
 
 extern "C" int cham_quantize_act(const float* X, int32_t fmt, int32_t dynamic, const float* s_dev, const float* z_dev,
