@@ -1,28 +1,28 @@
 """Benchmark of the whole Chameleon quantized-linear hot path on one MI355X.
 
-Workload: the SDXL-like 1280-wide transformer-block linear set at 1024 px with CFG batch 2 --
-M = 2048 tokens through QKV 1280->3840, out-proj 1280->1280, GEGLU 1280->10240 and FF-out
-5120->1280.  Weights are W4 with per-channel formats (heterogeneous synthetic rows);
-activations are A8 in the format a lookup table built for B = 4 timestep buckets from
-kurtosis and SNR (scaled-linear schedule 0.00085 -> 0.012, T = 1000) assigns.
+Workload: the multi-step SDXL-like sweep -- the 70-block linear stack (10 transformer blocks
+at width 640 on 4096 latent tokens, 60 at width 1280 on 1024 tokens, each block QKV d->3d,
+out-proj d->d, GEGLU d->8d and FF-out 4d->d: 280 linears, 1.64 G weights) at CFG batch 2
+(M = 8192 / 2048 rows), W4 per-channel weight formats, A8 activation formats from a lookup
+table over B = 10 timestep buckets (scaled-linear schedule 0.00085 -> 0.012, T = 1000).
 
-One step = one pass of every step of the path over one batch, all inputs resident in HBM:
-  select_weight_formats_batch (the 4 layers, one call, also writing each layer's packed GEMM
-  layout) -> act_stats_accumulate_batch (the 4 layer inputs, one call) ->
-  build_act_lut -> quantize_act_lut (4) -> mixed_linear (4).
-The weight side and the activation side are independent until the GEMMs: the search runs on
-a second stream (default priority) while the statistics, LUT and quantization run on the
-launch stream, which waits for the search before the GEMMs; the next step's search waits
-for this step's GEMMs (they read the packed weights it rewrites).
+One step = one pass of every step of the path over one batch (one sampler step), all inputs
+resident in HBM:
+  select_weight_formats_batch (the 280 layers, writing each layer's packed GEMM layout) ->
+  act_stats_accumulate_batch (the 280 layer inputs, into the step's bucket) ->
+  build_act_lut (280 x 10) -> quantize_act_lut (280, static LUT scales) -> mixed_linear (280).
+The weight side runs on a second stream (default priority) beside the statistics, LUT and
+quantization on the launch stream, which waits for it before the GEMMs; the next step's
+search waits for this step's GEMMs (they read the packed weights it rewrites).
 
-Printed: one JSON line.  `value` is mixed_linear TFLOP/s over the whole step time (GEMM
-flops / step time; the search, statistics, LUT and quantization count against it).  The
-`roofline` object is for the dominant kernel (the mixed-format GEMM), timed with HIP events
-on the launch stream over the timed steps; the weight search's own HBM rate is reported
-beside it.  `roofline.per_layer` breaks the GEMM time down by layer, from untimed steps run
-after the timed ones with an event between the calls (--layer-steps; each such event adds a
-launch gap, so the timed steps carry none).  `cpu_baseline` times the CPU oracle on a
-bounded sample of the same step.
+Printed: one JSON line.  `value` = the step's GEMM flops / step time (everything else in the
+step counts against it).  `roofline` is for the dominant kernel, the mixed-format GEMM: its
+280 calls timed with HIP events on the launch stream inside the timed steps; per layer kind
+(width x linear) from untimed steps with an event between calls.  Beside it: the weight
+search of the whole stack timed as its own call (no packing; §8(d) bytes), the packing pass
+by difference, the PixArt-like 28-block search at W4 and W8, the single-step (batch 1)
+stack's quantize + GEMM pass with one fixed A8 format per layer, and `cpu_baseline`: the CPU
+oracle on a bounded sample of the step, single-threaded and on all host cores.
 """
 from __future__ import annotations
 
@@ -30,6 +30,7 @@ import argparse
 import ctypes
 import json
 import os
+import platform
 import sys
 import time
 
@@ -41,33 +42,28 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 F16_PEAK_TFLOPS = 2500.0   # dense f16/bf16 MFMA
 T_SCHED = 1000
-B_BUCKETS = 4
-M_TOKENS = 2048
-D = 1280
+B_BUCKETS = 10
+ROWS = {640: 8192, 1280: 2048}   # CFG batch 2 x (4096 | 1024) tokens
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
-    p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--t", type=int, default=375, help="timestep of the benchmarked batch")
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--t", type=int, default=379, help="timestep of the benchmarked sampler step (999 - 20 i)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--no-dense-reference", action="store_true",
-                   help="skip timing the library's dense f16 GEMM on the same shapes (a point of comparison)")
-    p.add_argument("--cpu-budget-s", type=float, default=15.0)
-    p.add_argument("--no-w8", action="store_true", help="skip the W8 x A8 GEMM timing after the benchmark")
-    p.add_argument("--layer-steps", type=int, default=10,
+    p.add_argument("--cpu-budget-s", type=float, default=12.0, help="seconds of oracle work per baseline run")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the C3 search, the single-step stack and the dense f16 comparison")
+    p.add_argument("--layer-steps", type=int, default=2,
                    help="untimed steps after the timed ones for the per-layer GEMM breakdown (0: none)")
-    p.add_argument("--calib-copy-mib", type=int, default=0,
-                   help="before timing, copy a buffer of this many MiB once (a kernel of known HBM traffic "
-                        "for scaling hardware byte counters)")
     return p.parse_args()
 
 
 def committed_traffic():
-    """HBM bytes per mixed_linear call from the committed rocprofv3 counter summary, or None
-    when the GEMM source has changed since those counters were taken."""
+    """HBM bytes of one step's mixed_linear calls from the committed rocprofv3 counter
+    summary, or None when the GEMM source has changed since those counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "mixed_linear_hbm_traffic.md")
     src = os.path.join(ROOT, "paper_2609_33496_amd", "csrc", "cham_gemm.hip")
@@ -75,24 +71,28 @@ def committed_traffic():
         return None
     vals = {}
     for line in open(path):
-        if ":" in line and line.split(":")[0].strip() in ("traffic_bytes_per_call", "gemm_source_sha256_16"):
+        if ":" in line and line.split(":")[0].strip() in ("traffic_bytes_per_step", "gemm_source_sha256_16"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip()
     sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if vals.get("gemm_source_sha256_16") != sha or "traffic_bytes_per_call" not in vals:
+    if vals.get("gemm_source_sha256_16") != sha or "traffic_bytes_per_step" not in vals:
         return None
-    return int(vals["traffic_bytes_per_call"])
+    return int(vals["traffic_bytes_per_step"])
 
 
-def search_bytes_per_weight(K: int) -> float:
-    """Algorithmic bytes of the W4 search call per weight: 4 B read + 0.5 B codes + the
-    block metadata written for every channel (NF4 absmax 4 B / 64, E8M0 1 B / 32) + 14 B per
-    channel (format, scale, zero, perm, amortized over K); then the packed GEMM layout: the
-    codes and block metadata read back (0.5 + 4/64 + 1/32 B), 48 B of record per 32 weights
-    (1.5 B) and 16 B of channel parameters per channel."""
-    search = 4.0 + 0.5 + 4.0 / 64 + 1.0 / 32 + 14.0 / K
-    pack = 0.5 + 4.0 / 64 + 1.0 / 32 + 1.5 + 16.0 / K
-    return search + pack
+def search_bytes(N: int, K: int, bits: int = 4) -> float:
+    """Algorithmic bytes of the weight search of one layer (§8(d)): 4 B read per weight, the
+    codes (bits / 8 B), the chosen format's block metadata for every channel (NF4 absmax 4 B /
+    64, E8M0 1 B / 32 at W4; E8M0 at W8) and 13 B per channel (format, scale, zero, perm)."""
+    meta = (4.0 / 64 + 1.0 / 32) if bits == 4 else 1.0 / 32
+    return N * K * (4.0 + bits / 8.0 + meta) + 13.0 * N
+
+
+def pack_bytes(N: int, K: int) -> float:
+    """Algorithmic bytes of the packing pass: codes and block metadata read (once for the
+    records, once for the column sums), 48 B of record per 32 weights written, 20 B per
+    channel."""
+    return N * K * (2 * (0.5 + 4.0 / 64 + 1.0 / 32) + 1.5) + 20.0 * N
 
 
 def main():
@@ -114,92 +114,78 @@ def main():
     S = ctypes.c_void_p(stream.cuda_stream)
     side = torch.cuda.Stream(device=dev)  # the weight search of each step (default priority)
     S_side = ctypes.c_void_p(side.cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
 
-    layers = synth.sdxl_block_layers(D)
-    # ---- inputs (synthetic, resident in HBM before timing)
-    Ws, Xs = [], []
-    for li, (name, K, N) in enumerate(layers):
-        W, _ = synth.hetero_weights(100 + li, N, K)
-        Ws.append(torch.from_numpy(W).to(dev))
-        Xs.append(torch.from_numpy(synth.diffusion_acts(0, li, args.t, M_TOKENS, K)).to(dev))
-    # the search also writes each layer's GEMM-ready layout (decode tables), which
-    # mixed_linear then reads instead of deriving it again on every call
-    wqs = [cham.alloc_wq(N, K, cham.MASK_W4, dev, want_perm=True, want_packed=True) for (_, K, N) in layers]
-    aqs = [cham.alloc_aq(M_TOKENS, K, dev) for (_, K, N) in layers]
-    Ys = [torch.empty((M_TOKENS, N), dtype=torch.float32, device=dev) for (_, K, N) in layers]
-    stats = cham.alloc_stats(len(layers), B_BUCKETS, dev)
+    layers = synth.sdxl_stack_layers()
+    nl = len(layers)
+    Ms = [ROWS[d] for (_, _, _, d) in layers]
+    print(f"bench: building the {nl}-layer stack inputs on the GPU", file=sys.stderr, flush=True)
+    # ---- inputs (synthetic, drawn on the GPU, resident in HBM before timing)
+    Ws = [synth.hetero_weights_dev(1000 + li, N, K, dev) for li, (_, K, N, _) in enumerate(layers)]
+    Xs = [synth.diffusion_acts_dev(0, li, args.t, M, K, dev) for li, ((_, K, _, _), M) in enumerate(zip(layers, Ms))]
+    wqs = [cham.alloc_wq(N, K, cham.MASK_W4, dev, want_perm=True, want_packed=True) for (_, K, N, _) in layers]
+    aqs = [cham.alloc_aq(M, K, dev) for (_, K, _, _), M in zip(layers, Ms)]
+    Ys = [torch.empty((M, N), dtype=torch.float32, device=dev) for (_, _, N, _), M in zip(layers, Ms)]
+    # one workspace per call kind, sized for the largest layer (the calls run in order)
+    ws_lin = torch.empty(max(cham.workspace_bytes(cham.OP_LINEAR, M, N, K) for (_, K, N, _), M in zip(layers, Ms)),
+                         dtype=torch.uint8, device=dev)
+    ws_q = torch.empty(max(cham.workspace_bytes(cham.OP_QUANT_ACT, M, 0, K) for (_, K, _, _), M in zip(layers, Ms)),
+                       dtype=torch.uint8, device=dev)
+    # calibration pre-pass (setup, untimed): one batch of 256 rows per (layer, bucket) at the
+    # bucket's middle timestep
+    stats = cham.alloc_stats(nl, B_BUCKETS, dev)
     cham.act_stats_reset(stats)
-    # calibration pre-pass: two batches per bucket at the bucket's timesteps (setup, untimed)
     for b in range(B_BUCKETS):
-        for i in range(2):
-            t = b * T_SCHED // B_BUCKETS + (2 * i + 1) * T_SCHED // (4 * B_BUCKETS)
-            for li, (_, K, _) in enumerate(layers):
-                x = torch.from_numpy(synth.diffusion_acts(1, li, t, 512, K)).to(dev)
-                cham.act_stats_accumulate(x, li, b, stats)
+        t = b * T_SCHED // B_BUCKETS + T_SCHED // (2 * B_BUCKETS)
+        cal = [synth.diffusion_acts_dev(1, li, t, 256, K, dev) for li, (_, K, _, _) in enumerate(layers)]
+        cham.act_stats_accumulate_batch(cal, list(range(nl)), [b] * nl, stats)
+        del cal
     sched = cham.Schedule(T=T_SCHED)
     lut = cham.build_act_lut(stats, sched, want_kappa=True)
     lut.mirror()
     bucket = cham.bucket(args.t, T_SCHED, B_BUCKETS)
-    if args.calib_copy_mib > 0:
-        src = torch.ones(args.calib_copy_mib << 18, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
 
-    # prepared C structs and workspaces (the step issues raw C-ABI calls)
-    ws_q = [torch.empty(max(cham.workspace_bytes(cham.OP_QUANT_ACT, M_TOKENS, 0, X.shape[1]), 256),
-                        dtype=torch.uint8, device=dev) for X in Xs]
-    ws_lin = [torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=dev)
-              for (_, K, N) in layers]
+    # prepared C structs (the step issues raw C-ABI calls)
     wq_s = [w.struct() for w in wqs]
-    sbatch = cham.SearchBatch(Ws, wqs)  # the block's four layers searched in one call
-    # the four layer inputs' statistics in one call (as one calibration forward pass gives them)
-    tbatch = cham.StatsBatch(Xs, list(range(len(layers))), [bucket] * len(layers), stats)
-    st_s = stats.struct()
-    sc_s = sched.struct()
-    lut_s = lut.struct()
+    sbatch = cham.SearchBatch(Ws, wqs)
+    tbatch = cham.StatsBatch(Xs, list(range(nl)), [bucket] * nl, stats)
+    st_s, sc_s, lut_s = stats.struct(), sched.struct(), lut.struct()
     aq_s = [a.struct() for a in aqs]
     Fh = ctypes.c_void_p(lut.F_host.data_ptr())
-    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
-
     ev = {k: [] for k in ("search", "gemm", "layer")}
-    prev_end = [None]  # event: the previous step's GEMMs are done (or the timing start)
+    prev_end = [None]
 
     def step(record=False, per_layer_events=False):
-        e0 = e1 = None
-        # weight side, on the second stream: after the previous step's GEMMs
         if prev_end[0] is not None:
             side.wait_event(prev_end[0])
         if record:
             e0 = torch.cuda.Event(enable_timing=True)
             e0.record(side)
-        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, len(layers), S_side)
+        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, nl, S_side)
         assert rc == 0, rc
         searched = torch.cuda.Event(enable_timing=record)
         searched.record(side)
         if record:
             ev["search"].append((e0, searched))
-        # activation side, on the launch stream
-        rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, len(layers),
+        rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, nl,
                                                ctypes.byref(st_s), P(tbatch.ws), tbatch.ws_bytes, S)
         assert rc == 0, rc
         rc = L.cham_build_act_lut(ctypes.byref(st_s), ctypes.byref(sc_s), None, ctypes.byref(lut_s), None, S)
         assert rc == 0, rc
-        for li in range(len(layers)):
+        for li in range(nl):
             rc = L.cham_quantize_act_lut(P(Xs[li]), ctypes.byref(lut_s), Fh, li, args.t, 0, ctypes.byref(aq_s[li]),
-                                         P(ws_q[li]), ws_q[li].numel(), S)
+                                         P(ws_q), ws_q.numel(), S)
             assert rc == 0, rc
         stream.wait_event(searched)
         if record:
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
         marks = [e2] if record else []
-        for li in range(len(layers)):
-            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin[li]),
-                                     ws_lin[li].numel(), S)
+        for li in range(nl):
+            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
+                                     ws_lin.numel(), S)
             assert rc == 0, rc
-            if per_layer_events and li + 1 < len(layers):
+            if per_layer_events and li + 1 < nl:
                 marks.append(torch.cuda.Event(enable_timing=True))
                 marks[-1].record(stream)
         end = torch.cuda.Event(enable_timing=record)
@@ -211,46 +197,65 @@ def main():
         elif record:
             ev["gemm"].append((e2, end))
 
+    print("bench: warmup", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
-    prev_end[0] = t0  # the first timed search starts after the timing start
+    prev_end[0] = t0
     for _ in range(args.steps):
         step(record=True)
     t1.record(stream)
     torch.cuda.synchronize()
-    ms_total = t0.elapsed_time(t1)
-    ms_step = ms_total / args.steps
-    ms_search = float(np.mean([a.elapsed_time(b) for a, b in ev["search"]]))
+    print("bench: timed steps done", file=sys.stderr, flush=True)
+    ms_step = t0.elapsed_time(t1) / args.steps
+    ms_search_step = float(np.mean([a.elapsed_time(b) for a, b in ev["search"]]))
     ms_gemm = float(np.mean([a.elapsed_time(b) for a, b in ev["gemm"]]))
-    # per-layer breakdown from extra steps after the timed region: an event between calls
-    # adds a launch gap (≈ 2–3 µs each), so the timed steps carry only the two around the GEMMs
     for _ in range(args.layer_steps):
         step(record=True, per_layer_events=True)
     torch.cuda.synchronize()
-    # per layer: HIP-event time of its call (launch gap to the previous call included), and
-    # its roofline time max(flops / f16 MFMA peak, algorithmic bytes / HBM peak), the bytes
-    # being activation codes, 4-bit weight codes and the binary32 output
-    per_layer = {}
-    for li, (name, K, N) in enumerate(layers if args.layer_steps > 0 else []):
-        us = float(np.mean([a.elapsed_time(b) for a, b in (st[li] for st in ev["layer"])])) * 1e3
-        fl = 2.0 * M_TOKENS * N * K
-        by = M_TOKENS * K + N * K / 2 + 4.0 * M_TOKENS * N
-        t_roof = max(fl / (F16_PEAK_TFLOPS * 1e6), by / (HBM_PEAK_GBPS * 1e3))
-        per_layer[name] = {"us": round(us, 2), "tflops": round(fl / us / 1e6, 1), "t_roof_us": round(t_roof, 2),
-                           "frac_t_roof": round(t_roof / us, 4)}
 
-    flops = sum(2.0 * M_TOKENS * N * K for (_, K, N) in layers)
-    sbytes = sum(N * K * search_bytes_per_weight(K) for (_, K, N) in layers)
-    gemm_tflops = flops / (ms_gemm * 1e-3) / 1e12
-    value = flops / (ms_step * 1e-3) / 1e12
-    search_gbps = sbytes / (ms_search * 1e-3) / 1e9
+    flops = [2.0 * M * N * K for (_, K, N, _), M in zip(layers, Ms)]
+    per_kind = {}
+    if args.layer_steps > 0:
+        us = np.mean([[a.elapsed_time(b) * 1e3 for a, b in st] for st in ev["layer"]], axis=0)
+        for li, ((name, K, N, d), M) in enumerate(zip(layers, Ms)):
+            kind = name.split(".")[0] + "." + name.split(".")[-1]
+            by = M * K + N * K / 2 + 4.0 * M * N
+            t_roof = max(flops[li] / (F16_PEAK_TFLOPS * 1e6), by / (HBM_PEAK_GBPS * 1e3))
+            k = per_kind.setdefault(kind, {"calls": 0, "us": 0.0, "t_roof_us": 0.0, "fl": 0.0, "shape": f"{M}x{N}x{K}"})
+            k["calls"] += 1
+            k["us"] += float(us[li])
+            k["t_roof_us"] += t_roof
+            k["fl"] += flops[li]
+        for k in per_kind.values():
+            k["tflops"] = round(k.pop("fl") / (k["us"] * 1e-6) / 1e12, 1)
+            k["frac_t_roof"] = round(k["t_roof_us"] / k["us"], 4)
+            k["us_per_call"] = round(k["us"] / k["calls"], 2)
+            k["us"] = round(k["us"], 1)
+            k["t_roof_us"] = round(k["t_roof_us"], 1)
 
-    fmts = [int(lut.F_host[li * B_BUCKETS + bucket]) for li in range(len(layers))]
+    total_flops = sum(flops)
+    gemm_tflops = total_flops / (ms_gemm * 1e-3) / 1e12
+    value = total_flops / (ms_step * 1e-3) / 1e12
+
+    # ---- the weight search of the whole stack as its own call (no packing), then with packing
+    print("bench: search timing", file=sys.stderr, flush=True)
+    wq_np = [cham.alloc_wq(N, K, cham.MASK_W4, dev, want_perm=True) for (_, K, N, _) in layers]
+    nb_search = cham.SearchBatch(Ws, wq_np)
+    ms_search = time_calls(lambda: nb_search.run(stream), stream)
+    ms_search_pack = time_calls(lambda: sbatch.run(stream), stream)
+    sb = sum(search_bytes(N, K) for (_, K, N, _) in layers)
+    pb = sum(pack_bytes(N, K) for (_, K, N, _) in layers)
+    nweights = sum(N * K for (_, K, N, _) in layers)
+    search_gbps = sb / (ms_search * 1e-3) / 1e9
+    del wq_np, nb_search
+
+    fmts = [int(lut.F_host[li * B_BUCKETS + bucket]) for li in range(nl)]
     hist = np.bincount(torch.cat([w.fmt for w in wqs]).cpu().numpy(), minlength=9)
+    afh = np.bincount(np.array(fmts), minlength=5)
     out = {
         "metric": "mixed_linear TFLOP/s + weight-search GB/s (frac of MI355X peak), 1 GPU",
         "value": round(value, 3),
@@ -263,48 +268,157 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16-mfma(fp32 acc); w4 codes, a8 codes",
-        "data": "synthetic (seeded hetero W4 rows; diffusion-mixture activations)",
-        "config": {"workload": "SDXL-like 1280-wide block linears, M=2048 (1024 tokens x CFG 2), W4 per-channel, "
-                               "A8 LUT B=4 scaled-linear T=1000",
-                   "layers": [f"{n} {k}->{nn}" for (n, k, nn) in layers], "timestep": args.t, "bucket": bucket,
-                   "act_formats": [cham.A_NAMES[f] for f in fmts],
+        "data": "synthetic (seeded hetero W4 rows; diffusion-mixture activations; drawn on the GPU)",
+        "config": {"workload": "SDXL-like 70-block linear stack (10 blocks d=640 at M=8192, 60 blocks d=1280 at "
+                               "M=2048; CFG batch 2), one sampler step of the 50-step sweep, W4 per-channel, A8 LUT "
+                               "B=10 scaled-linear T=1000",
+                   "linears": nl, "weights": nweights, "gemm_tflop_per_step": round(total_flops / 1e12, 3),
+                   "timestep": args.t, "bucket": bucket,
+                   "act_format_hist": {cham.A_NAMES[i]: int(afh[i]) for i in range(5) if afh[i]},
                    "weight_format_hist": {cham.W_NAMES[i]: int(hist[i]) for i in range(9) if hist[i]}},
         "gemm_tflops": round(gemm_tflops, 3),
         "gemm_ms": round(ms_gemm, 4),
-        "search_GBps": round(search_gbps, 2),
-        "search_frac_hbm": round(search_gbps / HBM_PEAK_GBPS, 4),
-        "search_ms": round(ms_search, 4),
+        "search": {"ms": round(ms_search, 4), "GBps": round(search_gbps, 1),
+                   "frac_hbm": round(search_gbps / HBM_PEAK_GBPS, 4), "bytes": int(sb), "weights": nweights,
+                   "what": "select_weight_formats_batch over the 280 layers without packing, HIP events over 3 "
+                           "calls; bytes per §8(d): 4 B read + 0.5 B codes + block metadata per weight, 13 B per "
+                           "channel"},
+        "pack": {"ms": round(ms_search_pack - ms_search, 4),
+                 "GBps": round(pb / max(ms_search_pack - ms_search, 1e-6) / 1e6, 1), "bytes": int(pb),
+                 "what": "the same call writing each layer's packed GEMM layout, minus the search alone"},
+        "search_in_step_ms": round(ms_search_step, 4),
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4),
                      "traffic": committed_traffic(),
-                     "per_layer": {"layers": per_layer,
-                                   "what": f"{args.layer_steps} untimed steps after the timed ones with an event between "
-                                           "the GEMM calls (each adds a launch gap of about 2-3 us); t_roof = max("
-                                           "2MNK / f16 MFMA peak, (MK + NK/2 + 4MN) bytes / HBM peak)"},
-                     "kernel": "mixed_linear (gemm_kernel, k-split reduce_kernel; the weights' decode layout comes packed from the search); achieved = 2MNK summed over the "
-                               "4 calls / their HIP-event time; traffic = HBM bytes per call"},
+                     "per_layer": {"kinds": per_kind,
+                                   "what": f"{args.layer_steps} untimed steps with an event between the GEMM calls "
+                                           "(each adds a launch gap of about 2-3 us); t_roof = max(2MNK / f16 MFMA "
+                                           "peak, (MK + NK/2 + 4MN) bytes / HBM peak), summed per kind"},
+                     "kernel": "mixed_linear (gemm_kernel, k-split reduce_kernel; packed weights from the search); "
+                               "achieved = 2MNK summed over the step's 280 calls / their HIP-event time on the launch "
+                               "stream; traffic = HBM bytes of those 280 calls"},
     }
-    if not args.no_dense_reference:
-        out["dense_f16_reference"] = dense_reference(layers, stream)
-    if not args.no_w8:
-        for a, st_c in zip(aqs, aq_s):
-            a.fmt = st_c.fmt  # the format the step's quantize calls wrote into the C structs
-        out["w8a8_linear"] = w8_linear(cham, layers, Ws, aqs, stream)
+    if not args.no_extras:
+        print("bench: single-step stack, PixArt-like search, dense comparison", file=sys.stderr, flush=True)
+        out["single_step_stack"] = single_step_stack(cham, L, layers, Ms, Xs, wqs, stream, S)
+        out["pixart_search"] = pixart_search(cham, synth, stream, dev)
+        out["dense_f16_reference"] = dense_reference(layers, Ms, stream)
+    del Ys
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers, Ws, Xs, fmts, args.cpu_budget_s)
+        print("bench: CPU baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(layers, Ms, Ws, Xs, fmts, bucket, args.cpu_budget_s, total_flops)
     print(json.dumps(out), flush=True)
 
 
-def dense_reference(layers, stream, reps=20):
+def time_calls(fn, stream, reps=3):
+    """Mean HIP-event time (ms) of fn() over reps calls after one warm call."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def single_step_stack(cham, L, layers, Ms, Xs, wqs, stream, S):
+    """The single-step (SDXL-Turbo-like) case on the same stack: batch 1 (M = 4096 / 1024
+    rows: the first CFG half of each input), one fixed A8 format per layer from a B = 1 LUT
+    routed by kurtosis alone (statistics at t = 999); quantize + GEMM over the 280 layers."""
+    import torch
+    from paper_2609_33496_amd import synth
+    nl = len(layers)
+    dev = Xs[0].device
+    st = cham.alloc_stats(nl, 1, dev)
+    cham.act_stats_reset(st)
+    cal = [synth.diffusion_acts_dev(2, li, 999, 256, K, dev) for li, (_, K, _, _) in enumerate(layers)]
+    cham.act_stats_accumulate_batch(cal, list(range(nl)), [0] * nl, st)
+    del cal
+    lut = cham.build_act_lut(st, cham.Schedule(snr_gate_on=0)).mirror()
+    X1 = [X[: M // 2] for X, M in zip(Xs, Ms)]
+    aqs = [cham.alloc_aq(M // 2, K, dev, with_e8m0=True) for (_, K, _, _), M in zip(layers, Ms)]
+    Ys = [torch.empty((M // 2, N), dtype=torch.float32, device=dev) for (_, _, N, _), M in zip(layers, Ms)]
+    ws_lin = torch.empty(max(cham.workspace_bytes(cham.OP_LINEAR, M // 2, N, K) for (_, K, N, _), M in zip(layers, Ms)),
+                         dtype=torch.uint8, device=dev)
+    ws_q = torch.empty(1 << 16, dtype=torch.uint8, device=dev)
+    lut_s = lut.struct()
+    Fh = ctypes.c_void_p(lut.F_host.data_ptr())
+    aq_s = [a.struct() for a in aqs]
+    wq_s = [w.struct() for w in wqs]
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    marks = {}
+
+    def run(record=False):
+        for li in range(nl):
+            assert L.cham_quantize_act_lut(P(X1[li]), ctypes.byref(lut_s), Fh, li, 999, 0, ctypes.byref(aq_s[li]),
+                                           P(ws_q), ws_q.numel(), S) == 0
+        if record:
+            marks["g0"] = torch.cuda.Event(enable_timing=True)
+            marks["g0"].record(stream)
+        for li in range(nl):
+            assert L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
+                                       ws_lin.numel(), S) == 0
+        if record:
+            marks["g1"] = torch.cuda.Event(enable_timing=True)
+            marks["g1"].record(stream)
+
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    run(record=True)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    fl = sum(2.0 * (M // 2) * N * K for (_, K, N, _), M in zip(layers, Ms))
+    ms = e0.elapsed_time(e1)
+    ms_g = marks["g0"].elapsed_time(marks["g1"])
+    fh = np.bincount(lut.F_host.numpy(), minlength=5)
+    return {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1), "gemm_ms": round(ms_g, 4),
+            "gemm_tflops": round(fl / (ms_g * 1e-3) / 1e12, 1),
+            "act_format_hist": {cham.A_NAMES[i]: int(fh[i]) for i in range(5) if fh[i]},
+            "what": "280 x (quantize_act_lut + mixed_linear) at batch 1 (M = 4096 / 1024), fixed per-layer A8 "
+                    "formats (B = 1, kurtosis-only LUT at t = 999), weights packed by the step's search"}
+
+
+def pixart_search(cham, synth, stream, dev):
+    """The weight-format search over 28 PixArt-like DiT blocks (QKV, proj, fc1, fc2,
+    cross-attention KV: 578 M weights) at W4 and at W8 {INT8-sym, INT8-asym, MXINT8}, one
+    batched call each, no packing."""
+    blocks = [(name, K, N) for _ in range(28) for (name, K, N, _) in synth.pixart_block_layers()]
+    Ws = [synth.hetero_weights_dev(3000 + i, N, K, dev) for i, (_, K, N) in enumerate(blocks)]
+    res = {}
+    for mask, tag, bits in ((cham.MASK_W4, "w4", 4), (cham.MASK_W8, "w8", 8)):
+        outs = [cham.alloc_wq(N, K, mask, dev, want_perm=True) for (_, K, N) in blocks]
+        sb = cham.SearchBatch(Ws, outs)
+        ms = time_calls(lambda: sb.run(stream), stream)
+        by = sum(search_bytes(N, K, bits) for (_, K, N) in blocks)
+        gbps = by / (ms * 1e-3) / 1e9
+        hist = np.bincount(np.concatenate([o.fmt.cpu().numpy() for o in outs]), minlength=9)
+        res[tag] = {"ms": round(ms, 4), "GBps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4),
+                    "format_hist": {cham.W_NAMES[i]: int(hist[i]) for i in range(9) if hist[i]}}
+        del outs, sb
+    res["weights"] = sum(N * K for (_, K, N) in blocks)
+    res["what"] = "28 blocks x 5 linears in one batched call per palette, HIP events over 3 calls, §8(d) bytes"
+    return res
+
+
+def dense_reference(layers, Ms, stream, reps=10):
     """For comparison only (not part of the path): the library's dense f16 GEMM (torch.matmul,
-    f16 inputs and output, no per-channel decode) on the same shapes, timed after the
-    benchmark with HIP events; TFLOP/s per layer."""
+    f16 inputs and output, no per-channel decode) on the stack's eight distinct shapes,
+    weighted by their count in the stack; TFLOP/s per shape and over the step."""
     import torch
     g = torch.Generator(device="cuda").manual_seed(0)
-    res = {}
-    for (name, K, N) in layers:
-        a = torch.randn(M_TOKENS, K, dtype=torch.float16, device="cuda", generator=g)
-        b = torch.randn(K, N, dtype=torch.float16, device="cuda", generator=g)  # contiguous [K, N]
+    shapes = {}
+    for (name, K, N, d), M in zip(layers, Ms):
+        shapes.setdefault((M, N, K), 0)
+        shapes[(M, N, K)] += 1
+    res, tot_ms, tot_fl = {}, 0.0, 0.0
+    for (M, N, K), cnt in shapes.items():
+        a = torch.randn(M, K, dtype=torch.float16, device="cuda", generator=g)
+        b = torch.randn(K, N, dtype=torch.float16, device="cuda", generator=g)
         for _ in range(3):
             torch.matmul(a, b)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -314,90 +428,117 @@ def dense_reference(layers, stream, reps=20):
         e1.record(stream)
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / reps
-        res[name] = round(2.0 * M_TOKENS * N * K / (ms * 1e-3) / 1e12, 1)
-    return {"tflops": res, "unit": "TFLOP/s",
+        res[f"{M}x{N}x{K}"] = round(2.0 * M * N * K / (ms * 1e-3) / 1e12, 1)
+        tot_ms += ms * cnt
+        tot_fl += 2.0 * M * N * K * cnt
+    return {"tflops": res, "step_tflops": round(tot_fl / (tot_ms * 1e-3) / 1e12, 1), "unit": "TFLOP/s",
             "what": "torch.matmul f16 x f16 -> f16 (library GEMM), same M, N, K; no decode, 2-byte output"}
 
 
-def w8_linear(cham, layers, Ws, aqs, stream, reps=20):
-    """The same four GEMMs with W8 weights (INT8-sym, INT8-asym, MXINT8 per channel: the
-    8-bit palette) against the step's A8 activation codes, after the benchmark: each call
-    timed with HIP events over `reps` calls; TFLOP/s per layer and over the four."""
-    import torch
-    res, tot_ms, tot_fl = {}, 0.0, 0.0
-    for (name, K, N), W, aq in zip(layers, Ws, aqs):
-        wq = cham.select_weight_formats(W, cham.MASK_W8, want_packed=True)
-        Y = torch.empty((M_TOKENS, N), dtype=torch.float32, device=W.device)
-        ws = torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M_TOKENS, N, K), dtype=torch.uint8, device=W.device)
-        for _ in range(3):
-            cham.mixed_linear(aq, wq, Y=Y, ws=ws)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            cham.mixed_linear(aq, wq, Y=Y, ws=ws)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / reps
-        fl = 2.0 * M_TOKENS * N * K
-        res[name] = round(fl / (ms * 1e-3) / 1e12, 1)
-        tot_ms += ms
-        tot_fl += fl
-    return {"tflops": res, "all_tflops": round(tot_fl / (tot_ms * 1e-3) / 1e12, 1), "unit": "TFLOP/s",
-            "what": "mixed_linear with W8 per-channel weights (8-bit palette), the step's A8 codes; each call "
-                    "timed alone after the benchmark"}
+# ---------------------------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the step
+# ---------------------------------------------------------------------------------------------
+def _oracle_chunk(job):
+    """One unit of oracle work (run in a worker process or inline): returns seconds spent."""
+    import oracle
+    kind, arrs, p = job
+    t = time.perf_counter()
+    if kind == "search":
+        oracle.select_weight_formats(arrs[0], oracle.MASK_W4, want_err=False, want_perm=False)
+    elif kind == "stats":
+        st = oracle.Stats(1, 1)
+        st.accumulate(arrs[0], 0, 0)
+    elif kind == "quant":
+        oracle.quantize_act(arrs[0], p["fmt"], p["s"], p["z"], want_xhat=True)
+    elif kind == "pairs":
+        oracle.linear_pairs(arrs[0], arrs[1], p["mm"], p["nn"])
+    return time.perf_counter() - t
 
 
-def cpu_baseline(layers, Ws, Xs, act_fmts, budget_s):
-    """The CPU oracle (single-threaded C) on a bounded sample of the same step, scaled to
-    the step's GEMM-flop throughput: per layer, output channels are searched, activation
-    rows quantized and single outputs computed, each in chunks until its share of the
-    budget is spent; the per-layer times are extrapolated to the full sizes."""
+def cpu_baseline(layers, Ms, Ws, Xs, act_fmts, bucket, budget_s, total_flops):
+    """The CPU oracle (plain C, scalar, the same code the tests check against) on a bounded
+    sample of the step, single-threaded and on all host cores (one process per core, each
+    running the oracle on its own chunk): for one layer of each of the stack's eight kinds,
+    output channels searched, activation rows accumulated into the moments and quantized,
+    and single outputs computed; the LUT build over 280 x 10 in full.  Per-kind times are
+    extrapolated to the kind's layers at full size and summed to a step time, reported as
+    the step's GEMM-flop rate."""
+    import multiprocessing as mp
+
     import oracle
 
-    def until(share, total, chunk, fn):  # run fn(first, count) in chunks for `share` seconds
-        done, t0 = 0, time.perf_counter()
-        while done < total and (done == 0 or time.perf_counter() - t0 < share):
-            n = min(chunk, total - done)
-            fn(done, n)
-            done += n
-        return done, time.perf_counter() - t0
-
-    per_layer = budget_s / len(layers)
-    total_s = 0.0
-    flops = 0.0
-    samples = []
-    for li, (name, K, N) in enumerate(layers):
-        W = Ws[li].cpu().numpy()
-        X = Xs[li].cpu().numpy()
-        M = X.shape[0]
-        first = {}
-
-        def search(a, n):
-            wq = oracle.select_weight_formats(W[a:a + n], oracle.MASK_W4, want_err=False, want_perm=False)
-            first.setdefault("wq", wq)
-        nrows, ts = until(0.4 * per_layer, N, 32, search)
-        t = time.perf_counter()
+    kinds = {}
+    for li, ((name, K, N, d), M) in enumerate(zip(layers, Ms)):
+        kinds.setdefault(name.split(".")[0] + "." + name.split(".")[-1], []).append(li)
+    # the sample: per kind, chunks of work cut from the first layer of the kind
+    jobs, scale = [], []
+    for kind, lis in kinds.items():
+        li = lis[0]
+        _, K, N, _ = layers[li]
+        M = Ms[li]
+        W = Ws[li][:256].cpu().numpy()
+        X = Xs[li][:256].cpu().numpy()
         lo, hi = oracle.minmax(X)
         s, z = oracle.scale_zp(act_fmts[li], lo, hi)
-        t_mm = time.perf_counter() - t
-
-        def quant(a, n):
-            xh = oracle.quantize_act(X[a:a + n], act_fmts[li], s, z, want_xhat=True)[2]
-            first.setdefault("xh", xh)
-        mrows, tq = until(0.2 * per_layer, M, 64, quant)
-        Wh = oracle.dequant_weights(first["wq"], K)
-        xh = first["xh"]
+        wq = oracle.select_weight_formats(W[:64], oracle.MASK_W4, want_err=False, want_perm=False)
+        Wh = oracle.dequant_weights(wq, K)
+        xh = oracle.quantize_act(X[:64], act_fmts[li], s, z, want_xhat=True)[2]
         g = np.random.default_rng(li)
+        n = len(lis)
+        for c in range(4):
+            jobs.append(("search", [W[64 * c:64 * c + 64]], {}))
+            scale.append(n * N / 64.0)
+            jobs.append(("stats", [X[64 * c:64 * c + 64]], {}))
+            scale.append(n * M / 64.0)
+            jobs.append(("quant", [X[64 * c:64 * c + 64]], {"fmt": act_fmts[li], "s": s, "z": z}))
+            scale.append(n * M / 64.0)
+            mm, nn = g.integers(0, 64, 2048), g.integers(0, 64, 2048)
+            jobs.append(("pairs", [xh, Wh], {"mm": mm, "nn": nn}))
+            scale.append(n * M * N / 2048.0)
+    # the LUT over 280 x 10 from the accumulated moments (its cost in full, on one core)
+    ost = oracle.Stats(len(layers), B_BUCKETS)
+    t = time.perf_counter()
+    oracle.build_lut(ost)
+    t_lut = time.perf_counter() - t
 
-        def pairs(a, n):
-            oracle.linear_pairs(xh, Wh, g.integers(0, xh.shape[0], n), g.integers(0, Wh.shape[0], n))
-        npairs, tg = until(0.4 * per_layer, M * N, 4096, pairs)
-        total_s += ts * N / nrows + t_mm + tq * M / mrows + tg * (M * N) / npairs
-        flops += 2.0 * M * N * K
-        samples.append(f"{name}: {nrows}/{N} channels searched, {mrows}/{M} rows quantized, {npairs} outputs")
-    return {"value": round(flops / total_s / 1e12, 9), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
-            "sample": "; ".join(samples) + f"; each part run for its share of {budget_s:.0f} s of CPU time, "
-                      "per-layer times extrapolated to full size (stats/LUT omitted)"}
+    def run(pool):
+        done, secs, t0 = np.zeros(len(jobs)), np.zeros(len(jobs)), time.perf_counter()
+        rounds = 0
+        while rounds == 0 or time.perf_counter() - t0 < budget_s:
+            res = pool.map(_oracle_chunk, jobs) if pool else [_oracle_chunk(j) for j in jobs]
+            secs += np.array(res)
+            done += 1
+            rounds += 1
+        wall = time.perf_counter() - t0
+        cpu = float(np.sum(secs))
+        est = float(np.sum(secs / done * np.array(scale)))  # single-core seconds for the full step
+        return est, wall, cpu, rounds
+
+    est1, wall1, _, r1 = run(None)
+    step1 = est1 + t_lut
+    ncores = min(16, os.cpu_count() or 1)
+    with mp.get_context("spawn").Pool(ncores) as pool:  # fresh interpreters: no GPU state
+        estn, walln, cpun, rn = run(pool)
+    # all cores: the same per-chunk costs spread over ncores workers, at the parallel efficiency
+    # the pool achieved (CPU-seconds of work per wall second / cores)
+    eff = min(1.0, cpun / (walln * ncores))
+    stepn = estn / (ncores * eff) + t_lut
+    cpu_model = platform.processor() or "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(total_flops / stepn / 1e12, 9), "unit": "TFLOP/s", "cores": ncores, "kind": "oracle",
+            "value_1core": round(total_flops / step1 / 1e12, 9), "step_s_1core": round(step1, 1),
+            "step_s_all_cores": round(stepn, 1), "parallel_efficiency": round(eff, 3),
+            "nproc": os.cpu_count(), "cpu_model": cpu_model,
+            "sample": f"one layer of each of the 8 kinds: 256 channels searched, 256 rows accumulated into the "
+                      f"moments and quantized, 8192 single outputs per kind, repeated for {budget_s:.0f} s "
+                      f"({r1} rounds on 1 core, {rn} on {ncores}); times extrapolated to the kind's layers at full "
+                      f"size; LUT 280 x 10 in full"}
 
 
 if __name__ == "__main__":

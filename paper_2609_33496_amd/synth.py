@@ -118,3 +118,81 @@ def pixart_block_layers(d: int = 1152):
     4096-wide text encoder.  Returns [(name, K, N, M_tokens)]."""
     return [("qkv", d, 3 * d, 8192), ("proj", d, d, 8192), ("fc1", d, 4 * d, 8192),
             ("fc2", 4 * d, d, 8192), ("cross_kv", 4096, d, 240)]
+
+
+# --------------------------------------------------------------------------------------------
+# the same recipes drawn on the GPU (torch, seeded per array), for the benchmark's full-size
+# stacks (1.64 G weights, 1.5 G activations) where drawing on the host would take minutes.
+# Only normal and uniform draws: Laplace by inverting its CDF, Student-t with integral nu as
+# a normal over the root of a chi-square built from nu squared normals.
+# --------------------------------------------------------------------------------------------
+def _gen(device, *key: int):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(rng(*key).integers(0, 2 ** 62)))
+    return g
+
+
+def _student_t_dev(nu: int, shape, g, device):
+    import torch
+    z = torch.randn(shape, generator=g, device=device)
+    chi = torch.zeros(shape, device=device)
+    for _ in range(nu):
+        chi += torch.randn(shape, generator=g, device=device) ** 2
+    return z / torch.sqrt(chi / nu)
+
+
+def hetero_weights_dev(seed: int, N: int, K: int, device="cuda"):
+    """hetero_weights' families and proportions, drawn on `device` (float32 [N, K])."""
+    import torch
+    g = _gen(device, seed, 12)
+    fam = torch.multinomial(torch.tensor(FAMILY_P, device=device), N, replacement=True, generator=g)
+    W = torch.empty((N, K), dtype=torch.float32, device=device)
+    for f, name in enumerate(FAMILIES):
+        rows = torch.nonzero(fam == f).flatten()
+        if rows.numel() == 0:
+            continue
+        shape = (rows.numel(), K)
+        if name == "gauss":
+            v = torch.randn(shape, generator=g, device=device)
+        elif name == "laplace":
+            u = torch.rand(shape, generator=g, device=device) - 0.5
+            v = -torch.sign(u) * torch.log1p(-2.0 * u.abs()) / np.sqrt(2.0)
+        elif name == "uniform":
+            v = (torch.rand(shape, generator=g, device=device) * 2.0 - 1.0) * np.sqrt(3.0)
+        elif name == "t3":
+            v = _student_t_dev(3, shape, g, device) / np.sqrt(3.0)
+        elif name == "outlier":
+            v = torch.randn(shape, generator=g, device=device)
+            v = torch.where(torch.rand(shape, generator=g, device=device) < 0.005, v * 10.0, v)
+        else:  # blockvar
+            v = torch.randn(shape, generator=g, device=device)
+            nb = K // 32
+            sc = torch.exp(torch.randn((rows.numel(), nb), generator=g, device=device))
+            v[:, :nb * 32] *= torch.repeat_interleave(sc, 32, dim=1)
+        W[rows] = v
+    W *= 0.02 * torch.exp(0.5 * torch.randn((N, 1), generator=g, device=device))
+    return W
+
+
+def diffusion_acts_dev(seed: int, layer: int, t: int, M: int, K: int, device="cuda", step: int = 0):
+    """diffusion_acts' mixture at timestep t, drawn on `device` (float32 [M, K])."""
+    import torch
+    a = float(alphas_cumprod()[t])
+    g = _gen(device, seed, 14, layer, t, step)
+    means = torch.tensor([-1.5, -0.5, 0.5, 1.5], device=device)
+    comp = torch.randint(0, 4, (M, K), generator=g, device=device)
+    gmm = means[comp] + 0.1 * torch.randn((M, K), generator=g, device=device)
+    noise = layer_lambda(seed, layer) * _student_t_dev(3, (M, K), g, device)
+    return (np.sqrt(a) * gmm + np.sqrt(1.0 - a) * noise).to(torch.float32)
+
+
+def sdxl_stack_layers():
+    """The 70-block SDXL-like linear stack: 10 blocks at width 640 then 60 at width 1280, each
+    with the block linear set.  Returns [(name, K, N, width)] in order (280 linears)."""
+    out = []
+    for d, nblk in ((640, 10), (1280, 60)):
+        for b in range(nblk):
+            for name, K, N in sdxl_block_layers(d):
+                out.append((f"d{d}.{name}", K, N, d))
+    return out
