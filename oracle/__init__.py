@@ -88,6 +88,11 @@ def _load():
     lib.orc_route.restype = i32
     lib.orc_build_lut.argtypes = [i32, i32, P, P, i32, f64, f64, i32, f64, f64, f64, f64, i32, P, P, P,
                                   P, P]
+    lib.orc_select_group_formats.argtypes = [P, i64, i64, u32, u32, P, P, P, P, P, P, P, P]
+    lib.orc_select_group_formats.restype = i32
+    lib.orc_dequant_grouped.argtypes = [i64, i64, i32, i32, i32, P, P, P, P, P]
+    lib.orc_dequant_grouped.restype = i32
+    lib.orc_gq_row.argtypes = [i32, i32, P, i64, P, P, P, P, P]
     lib.orc_linear.argtypes = [i64, i64, i64, P, P, P, P]
     lib.orc_linear_pairs.argtypes = [i64, i64, P, P, P, P, P, P]
     if not lib.orc_rounding_ok():
@@ -182,6 +187,58 @@ def dequant_weights(wq: dict, K: int) -> np.ndarray:
                                      _p(np.ascontiguousarray(wq["e8m0"])), _p(Wh))
     if rc != 0:
         raise ValueError("oracle: K too large")
+    return Wh
+
+
+# ---------------------------------------------------------------------------------------------
+# DiT joint (group size, format) search (Sec. 4.6 (i))
+# ---------------------------------------------------------------------------------------------
+GROUP_SIZES = (32, 64, 128, 192, 288)
+GMASK_ALL = 0x1F
+MASK_DIT_W4 = (1 << W_INT4_ASYM) | (1 << W_NF4) | (1 << W_FP4)      # the DiT fork's 4-bit set
+MASK_DIT_W8 = MASK_W8                                                 # {INT8-sym, INT8-asym, MXINT8}
+
+
+def gq_row(fmt: int, g: int, w: np.ndarray):
+    """Round trip one row in groups of g: (codes, w_hat, group scales, group zeros, e8m0)."""
+    w = _f32(w)
+    K = w.shape[0]
+    codes = np.zeros(K, np.uint8)
+    wh = np.zeros(K, np.float32)
+    gs = np.zeros(K // 32, np.float32)
+    gz = np.zeros(K // 32, np.float32)
+    e8 = np.zeros(K // 32, np.uint8)
+    _load().orc_gq_row(fmt, g, _p(w), K, _p(codes), _p(wh), _p(gs), _p(gz), _p(e8))
+    return codes, wh, gs, gz, e8
+
+
+def select_group_formats(W: np.ndarray, mask: int, energy: np.ndarray, gmask: int = GMASK_ALL):
+    """Per-layer (g, f) search with input-aware error weights energy[K].  Returns a dict:
+    g, fmt_id, err [45] (tuple t = group index * 9 + format; -1 not evaluated), fmt [N],
+    codes, gscale / gzero [N, K/32], e8m0 [N, K/32], code_bits."""
+    W = _f32(W)
+    N, K = W.shape
+    e = _f32(energy)
+    cb = code_bits(mask)
+    out = dict(choice=np.zeros(2, np.int32), err=np.zeros(45, np.float64), fmt=np.zeros(N, np.uint8),
+               codes=np.zeros((N, K * cb // 8), np.uint8), gscale=np.zeros((N, K // 32), np.float32),
+               gzero=np.zeros((N, K // 32), np.float32), e8m0=np.zeros((N, K // 32), np.uint8))
+    rc = _load().orc_select_group_formats(_p(W), N, K, mask, gmask, _p(e), _p(out["choice"]), _p(out["err"]),
+                                          _p(out["fmt"]), _p(out["codes"]), _p(out["gscale"]), _p(out["gzero"]),
+                                          _p(out["e8m0"]))
+    if rc != 0:
+        raise ValueError("oracle: bad arguments to the group search")
+    out["g"], out["fmt_id"], out["code_bits"] = int(out["choice"][0]), int(out["choice"][1]), cb
+    return out
+
+
+def dequant_grouped(gq: dict, K: int) -> np.ndarray:
+    N = gq["fmt"].shape[0]
+    Wh = np.zeros((N, K), np.float32)
+    rc = _load().orc_dequant_grouped(N, K, gq["code_bits"], gq["g"], gq["fmt_id"], _p(np.ascontiguousarray(gq["codes"])),
+                                     _p(gq["gscale"]), _p(gq["gzero"]), _p(gq["e8m0"]), _p(Wh))
+    if rc != 0:
+        raise ValueError("oracle: bad grouped weight")
     return Wh
 
 

@@ -683,3 +683,144 @@ void orc_linear_pairs(int64_t K, int64_t npairs, const int64_t* mm, const int64_
         Babs[p] = ab;
     }
 }
+
+/* ------------------------------------------------------------------------- */
+/* DiT joint (group size, format) weight search (Sec. 4.6 (i), Fig. dit caption;  */
+/* App. A.11).  For every tuple (g, f) of the group sizes G = {32, 64, 128, 192,   */
+/* 288} and the enabled formats, every output row is quantized in groups of g      */
+/* consecutive input channels (the last group holds K mod g when g does not divide */
+/* K; READING), each group with its own scale as the format's per-channel           */
+/* quantizer defines it (INT-sym/asym ScaleZP on the group's range, FP4 amax/6, NF4 */
+/* the group absmax); MX formats carry their own 32-element blocks and are         */
+/* evaluated at g = 32 only.  The input-aware error of a tuple is                   */
+/* sum_n sum_k e_k (w - w^)^2 with e_k = E[x_k^2] (the SQNR of the paper weights     */
+/* each input channel's squared error by its activation energy; the signal term is */
+/* common to all tuples, so the argmax SQNR is this argmin).  Ties go to the lowest  */
+/* tuple index t = gi * 9 + f (group sizes in the listed order, formats in palette  */
+/* order; READING).                                                                 */
+/* ------------------------------------------------------------------------- */
+static const int GROUP_SIZES[5] = { 32, 64, 128, 192, 288 };
+
+static int is_mx_fmt(int f) { return f == W_MXINT8 || f == W_MXINT4 || f == W_MXFP4; }
+
+/* Round trip one row in groups of g with format f; scale / zero per group into gs / gz
+ * (index j of group j; NF4: the group absmax), e8 per 32-block for MX formats. */
+static void gq_row(int f, int g, const float* w, int64_t K, uint8_t* code, float* wh, float* gs,
+                   float* gz, uint8_t* e8) {
+    nf4_build();
+    for (int64_t b = 0; b < K / 32; ++b) { gs[b] = 0.0f; gz[b] = 0.0f; if (e8) e8[b] = 0; }
+    if (is_mx_fmt(f)) {  /* its own 32-blocks */
+        float s;
+        float z;
+        wq_row(f, w, K, code, wh, &s, &z, NULL, e8);
+        return;
+    }
+    for (int64_t j = 0; j * g < K; ++j) {
+        const int64_t k0 = j * g, n = (k0 + g <= K) ? g : K - k0;
+        float s = 0.0f;
+        float z = 0.0f;
+        switch (f) {
+        case W_INT8_SYM: q_int_sym(w + k0, n, 127, 8, code + k0, wh + k0, &s); break;
+        case W_INT4_SYM: q_int_sym(w + k0, n, 7, 4, code + k0, wh + k0, &s); break;
+        case W_INT8_ASYM: q_int_asym(w + k0, n, 255, code + k0, wh + k0, &s, &z); break;
+        case W_INT4_ASYM: q_int_asym(w + k0, n, 15, code + k0, wh + k0, &s, &z); break;
+        case W_FP4: q_fp4(w + k0, n, code + k0, wh + k0, &s); break;
+        case W_NF4: q_nf4_block(w + k0, n, code + k0, wh + k0, &s); break;
+        }
+        gs[j] = s;
+        gz[j] = z;
+    }
+}
+
+/* The search over a layer W [N][K] (K % 32 == 0, K <= 65536).  mask: formats; gmask: group
+ * sizes (bit i enables GROUP_SIZES[i]); energy [K] (binary32).  Outputs: choice[2] = {g, f},
+ * err[45] = the layer error of each tuple (-1 when not evaluated), fmt [N] (= f), codes
+ * ([N][K/2] when every enabled format is 4-bit, else [N][K]), gscale / gzero [N][K/32]
+ * (group j at j, 0 past the last group), e8 [N][K/32] (MX; may be NULL).
+ * Returns 0, or -1 on a bad argument. */
+int orc_select_group_formats(const float* W, int64_t N, int64_t K, uint32_t mask, uint32_t gmask,
+                             const float* energy, int32_t* choice, double* err, uint8_t* fmt,
+                             uint8_t* codes, float* gscale, float* gzero, uint8_t* e8) {
+    if (N < 1 || K <= 0 || K % 32 || K > (1 << 16) || mask == 0 || (mask & ~0x1FFu) || gmask == 0 ||
+        (gmask & ~0x1Fu))
+        return -1;
+    static float wh[1 << 16], gs[1 << 11], gz[1 << 11];
+    static uint8_t cb[1 << 16], eb[1 << 11];
+    int code_bits = 4;
+    for (int f = 0; f < W_NFMT; ++f)
+        if (((mask >> f) & 1u) && wfmt_bits(f) == 8) code_bits = 8;
+    for (int t = 0; t < 45; ++t) err[t] = -1.0;
+    int best = -1;
+    for (int gi = 0; gi < 5; ++gi) {
+        if (!((gmask >> gi) & 1u)) continue;
+        for (int f = 0; f < W_NFMT; ++f) {
+            if (!((mask >> f) & 1u)) continue;
+            if (is_mx_fmt(f) && GROUP_SIZES[gi] != 32) continue;
+            double e = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                gq_row(f, GROUP_SIZES[gi], W + n * K, K, cb, wh, gs, gz, eb);
+                for (int64_t k = 0; k < K; ++k) {
+                    float d = W[n * K + k] - wh[k];
+                    e += (double)energy[k] * ((double)d * (double)d);
+                }
+            }
+            const int t = gi * 9 + f;
+            err[t] = e;
+            if (best < 0 || e < err[best]) best = t;
+        }
+    }
+    if (best < 0) return -1;  /* only MX formats enabled without g = 32 */
+    const int g = GROUP_SIZES[best / 9], f = best % 9;
+    choice[0] = g;
+    choice[1] = f;
+    for (int64_t n = 0; n < N; ++n) {
+        gq_row(f, g, W + n * K, K, cb, wh, gs, gz, eb);
+        fmt[n] = (uint8_t)f;
+        for (int64_t b = 0; b < K / 32; ++b) {
+            gscale[n * (K / 32) + b] = gs[b];
+            gzero[n * (K / 32) + b] = gz[b];
+            if (e8) e8[n * (K / 32) + b] = is_mx_fmt(f) ? eb[b] : 0;
+        }
+        if (code_bits == 4) {
+            for (int64_t k = 0; k < K; k += 2)
+                codes[n * (K / 2) + k / 2] = (uint8_t)((cb[k] & 15u) | ((cb[k + 1] & 15u) << 4));
+        } else {
+            memcpy(codes + n * K, cb, (size_t)K);
+        }
+    }
+    return 0;
+}
+
+/* Decode a grouped weight (as emitted above) to binary32. */
+int orc_dequant_grouped(int64_t N, int64_t K, int code_bits, int g, int f, const uint8_t* codes,
+                        const float* gscale, const float* gzero, const uint8_t* e8, float* Wh) {
+    nf4_build();
+    if (K % 32 || K > (1 << 16)) return -1;
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t k = 0; k < K; ++k) {
+            unsigned u = code_bits == 4 ? ((codes[n * (K / 2) + k / 2] >> (4 * (k & 1))) & 15u)
+                                        : codes[n * K + k];
+            const float s = gscale[n * (K / 32) + k / g], z = gzero[n * (K / 32) + k / g];
+            float v = 0.0f;
+            switch (f) {
+            case W_INT8_SYM: v = (float)(int8_t)u * s; break;
+            case W_INT4_SYM: v = (float)((int)(u << 28) >> 28) * s; break;
+            case W_INT8_ASYM:
+            case W_INT4_ASYM: v = ((float)u - z) * s; break;
+            case W_FP4: v = (float)mf_decode(&MF_E2M1, u) * s; break;
+            case W_NF4: v = NF4[u & 15u] * s; break;
+            case W_MXINT8: v = ldexpf((float)(int8_t)u, (int)e8[n * (K / 32) + k / 32] - 127 - 6); break;
+            case W_MXINT4: v = ldexpf((float)((int)(u << 28) >> 28), (int)e8[n * (K / 32) + k / 32] - 127 - 2); break;
+            case W_MXFP4: v = ldexpf((float)mf_decode(&MF_E2M1, u), (int)e8[n * (K / 32) + k / 32] - 127); break;
+            }
+            Wh[n * K + k] = v;
+        }
+    }
+    return 0;
+}
+
+/* Round trip one row in groups (diagnostics and pins). */
+void orc_gq_row(int f, int g, const float* w, int64_t K, uint8_t* codes, float* wh, float* gs,
+                float* gz, uint8_t* e8) {
+    gq_row(f, g, w, K, codes, wh, gs, gz, e8);
+}
