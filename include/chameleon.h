@@ -154,6 +154,59 @@ size_t cham_packed_bytes(int64_t N, int64_t K);
 int cham_select_weight_formats_batch(const float* const* W, cham_wq* wq, int32_t nlayers, void* stream);
 
 /* ---------------------------------------------------------------------------------------
+ * 1b. DiT joint (group size, format) weight search (Sec. 4.6 (i))
+ *
+ * For one linear layer W [N][K], every tuple (g, f) of the enabled group sizes g (groups of
+ * g consecutive input channels along K; the last group holds K mod g when g does not divide
+ * K) and enabled formats f is evaluated: each group is quantized with its own parameters as
+ * the format's per-channel quantizer above defines them (INT-sym / INT-asym on the group's
+ * range, FP4 amax/6, NF4 the group absmax), and the layer's input-aware error
+ * sum_n sum_k energy[k] (w - w^)^2 (energy[k] = E[x_k^2], the activation energy of input
+ * channel k) is formed in binary64.  The tuple with the smallest error (= the largest
+ * input-aware SQNR) is chosen, ties to the lowest index t = group index * 9 + format; MX
+ * formats use their own 32-blocks and are evaluated at g = 32 only.  The choice stays on
+ * the device (choice[]), so no synchronization is needed before the GEMM.
+ * ------------------------------------------------------------------------------------- */
+#define CHAM_NGROUPS 5          /* group sizes 32, 64, 128, 192, 288 (bit i of group_mask)  */
+#define CHAM_GMASK_ALL 0x1Fu
+/* The DiT fork's 4-bit search set {INT4-asym, NF4, FP4}; at 8 bits F_w^(8). */
+#define CHAM_MASK_DIT_W4 0x070u
+
+typedef struct cham_gwq {
+    int64_t N, K;           /* W is [N][K]; K % 32 == 0, K <= 8192                           */
+    uint32_t palette_mask;  /* formats searched (bit f = format f)                            */
+    uint32_t group_mask;    /* group sizes searched (bit i = the i-th size); nonzero          */
+    int32_t code_bits;      /* 4 if every enabled format is 4-bit, else 8 (set by the search) */
+    int32_t* choice;        /* [2] device: the chosen group size and format id                */
+    uint8_t* fmt;           /* [N]      the chosen format id in every entry                   */
+    uint8_t* codes;         /* [N][K/2] (4-bit) or [N][K] (8-bit), as in cham_wq              */
+    float* gscale;          /* [N][K/32] per group j (at index j): INT scale, FP4 scale or NF4
+                               absmax; 0 past the last group and for MX formats               */
+    float* gzero;           /* [N][K/32] per group: INT-asym zero point (integral), else 0    */
+    uint8_t* e8m0;          /* [N][K/32] MX block exponents (0 unless an MX format is chosen);
+                               may be NULL iff no MX format is enabled                        */
+    double* err;            /* [45]     layer error of tuple t (-1 if not evaluated); NULL = skip */
+    void* packed;           /* cham_packed_bytes(N, K) bytes, 256-byte aligned: the GEMM
+                               layout, written by the search when non-NULL (4-bit palettes and
+                               K % 64 == 0 only); NULL = skip                                  */
+} cham_gwq;
+
+/* Search W [N][K] (device, binary32, finite, 16-byte aligned) with error weights energy[K]
+ * (device, binary32, 16-byte aligned) and fill *gq.  ws: CHAM_OP_GSELECT bytes (the
+ * per-channel errors).  Errors: CHAM_EINVAL (NULL or misaligned buffer, N < 1), CHAM_EFORMAT
+ * (masks; only MX formats without g = 32), CHAM_ESHAPE (K, or packing with 8-bit codes),
+ * CHAM_EWORKSPACE, CHAM_EHIP. */
+int cham_select_group_formats(const float* W, const float* energy, cham_gwq* gq, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* Calibration pre-pass of the search's weights: colsq[k] += sum_m X[m][k]^2 over X [M][K]
+ * (device binary32; colsq device binary64 [K]), summed in a fixed order (bitwise
+ * reproducible); E[x_k^2] = colsq[k] / rows.  ws: CHAM_OP_COLSQ bytes.
+ * Errors: CHAM_EINVAL, CHAM_EWORKSPACE, CHAM_EHIP. */
+int cham_act_colsq_accumulate(const float* X, int64_t M, int64_t K, double* colsq, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* ---------------------------------------------------------------------------------------
  * 2. calibration statistics (Sec. 4.4; Alg. 1) and the LUT (Sec. 4.3; Alg. 1)
  * ------------------------------------------------------------------------------------- */
 typedef struct cham_act_stats {
@@ -296,6 +349,14 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
 int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* The same linear layer with group-scaled weights from cham_select_group_formats (the DiT
+ * path, Sec. 4.6 (i)): each 32-element half of a 64-wide k-step lies in one group (every
+ * group size is a multiple of 32), whose scale and zero point build its decode table;
+ * accuracy as above.  4-bit palettes only (gq->code_bits == 4; the 8-bit group-scaled
+ * decode is not built: CHAM_EFORMAT).  ws: CHAM_OP_LINEAR bytes. */
+int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, float* Y, void* ws, size_t ws_bytes,
+                              void* stream);
+
 /* The launch plan cham_mixed_linear takes for M x N x K with 4- or 8-bit weight codes
  * (diagnostics; host only, launches nothing).  out (host, out_len >= 10 int32) receives
  * {launches (1 or 2), k-splits, then per launch: first row, end row, tile rows, tile
@@ -311,6 +372,8 @@ int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bits, int32_t
 #define CHAM_OP_STATS 1
 #define CHAM_OP_QUANT_ACT 2
 #define CHAM_OP_LINEAR 3
+#define CHAM_OP_GSELECT 4   /* cham_select_group_formats: N output channels              */
+#define CHAM_OP_COLSQ 5     /* cham_act_colsq_accumulate: K input channels               */
 /* Bytes of workspace op needs at these sizes (M rows of X -- numel for CHAM_OP_STATS --,
  * N output channels, K inner size).  0 means no workspace. */
 size_t cham_workspace_bytes(int32_t op, int64_t M, int64_t N, int64_t K);

@@ -31,7 +31,10 @@ MASK_W8 = 0x007
 A_INT8_ASYM, A_FP8_E4M3, A_FP8_E5M2, A_MXFP8, A_MXINT8 = range(5)
 A_NAMES = ["INT8-asym", "FP8-E4M3", "FP8-E5M2", "MXFP8-E4M3", "MXINT8"]
 # workspace ops
-OP_SELECT, OP_STATS, OP_QUANT_ACT, OP_LINEAR = range(4)
+OP_SELECT, OP_STATS, OP_QUANT_ACT, OP_LINEAR, OP_GSELECT, OP_COLSQ = range(6)
+GROUP_SIZES = (32, 64, 128, 192, 288)
+GMASK_ALL = 0x1F
+MASK_DIT_W4 = 0x070  # {INT4-asym, NF4, FP4}
 SCHED_SCALED_LINEAR, SCHED_LINEAR = 0, 1
 
 _P = ctypes.c_void_p
@@ -56,6 +59,12 @@ class _Sched(ctypes.Structure):
 class _LUT(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int32), ("B", ctypes.c_int32), ("T", ctypes.c_int32), ("F", _P), ("S", _P),
                 ("Z", _P)]
+
+
+class _GWQ(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("K", ctypes.c_int64), ("palette_mask", ctypes.c_uint32),
+                ("group_mask", ctypes.c_uint32), ("code_bits", ctypes.c_int32), ("choice", _P), ("fmt", _P),
+                ("codes", _P), ("gscale", _P), ("gzero", _P), ("e8m0", _P), ("err", _P), ("packed", _P)]
 
 
 class _AQ(ctypes.Structure):
@@ -95,6 +104,9 @@ def lib():
                                         _P]
     L.cham_quantize_act_noalloc.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P]
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
+    L.cham_mixed_linear_grouped.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_GWQ), _P, _P, sz, _P]
+    L.cham_select_group_formats.argtypes = [_P, _P, ctypes.POINTER(_GWQ), _P, sz, _P]
+    L.cham_act_colsq_accumulate.argtypes = [_P, i64, i64, _P, _P, sz, _P]
     L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
     L.cham_workspace_bytes.restype = sz
     L.cham_packed_bytes.argtypes = [i64, i64]
@@ -103,7 +115,8 @@ def lib():
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_quantize_act_noalloc",
-                 "cham_mixed_linear",
+                 "cham_mixed_linear", "cham_mixed_linear_grouped", "cham_select_group_formats",
+                 "cham_act_colsq_accumulate",
                  "cham_linear_plan"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -447,6 +460,82 @@ def quantize_act_lut(X: torch.Tensor, lut: LUT, layer: int, t: int, dynamic: boo
            "quantize_act_lut")
     out.fmt = a.fmt
     return out
+
+
+# -------------------------------------------------------------------------------------------
+# DiT joint (group size, format) search (Sec. 4.6 (i))
+# -------------------------------------------------------------------------------------------
+@dataclass
+class GWQ:
+    """Group-scaled weights of one format (device tensors, see cham_gwq)."""
+    N: int
+    K: int
+    mask: int
+    gmask: int
+    code_bits: int
+    choice: torch.Tensor             # [2] i32: group size, format
+    fmt: torch.Tensor
+    codes: torch.Tensor
+    gscale: torch.Tensor             # [N, K/32]
+    gzero: torch.Tensor              # [N, K/32]
+    e8m0: Optional[torch.Tensor]
+    err: Optional[torch.Tensor]      # [45] f64
+    packed: Optional[torch.Tensor] = None
+
+    def struct(self) -> _GWQ:
+        return _GWQ(self.N, self.K, self.mask, self.gmask, self.code_bits, _ptr(self.choice), _ptr(self.fmt),
+                    _ptr(self.codes), _ptr(self.gscale), _ptr(self.gzero), _ptr(self.e8m0), _ptr(self.err),
+                    _ptr(self.packed))
+
+
+def alloc_gwq(N: int, K: int, mask: int, gmask: int = GMASK_ALL, device="cuda", want_err=True,
+              want_packed=False) -> GWQ:
+    cb = code_bits(mask)
+    mx = bool(mask & ((1 << W_MXINT8) | (1 << W_MXINT4) | (1 << W_MXFP4)))
+    f32 = torch.float32
+    return GWQ(N, K, mask, gmask, cb, torch.zeros(2, dtype=torch.int32, device=device),
+               torch.empty(N, dtype=torch.uint8, device=device),
+               torch.empty((N, K * cb // 8), dtype=torch.uint8, device=device),
+               torch.empty((N, K // 32), dtype=f32, device=device), torch.empty((N, K // 32), dtype=f32, device=device),
+               torch.empty((N, K // 32), dtype=torch.uint8, device=device) if mx else None,
+               torch.empty(45, dtype=torch.float64, device=device) if want_err else None,
+               torch.empty(packed_bytes(N, K), dtype=torch.uint8, device=device) if want_packed else None)
+
+
+def select_group_formats(W: torch.Tensor, energy: torch.Tensor, mask: int = MASK_DIT_W4, gmask: int = GMASK_ALL,
+                         out: Optional[GWQ] = None, want_packed=False, ws=None, stream=None) -> GWQ:
+    _dev_tensor(W, torch.float32, "W")
+    _dev_tensor(energy, torch.float32, "energy")
+    N, K = W.shape
+    if out is None:
+        out = alloc_gwq(N, K, mask, gmask, W.device, want_packed=want_packed)
+    ws, nb = _workspace(OP_GSELECT, 0, N, K, W.device, ws)
+    g = out.struct()
+    _check(lib().cham_select_group_formats(_ptr(W), _ptr(energy), ctypes.byref(g), _ptr(ws), nb, _stream(stream)),
+           "select_group_formats")
+    out.code_bits = g.code_bits
+    return out
+
+
+def act_colsq_accumulate(X: torch.Tensor, colsq: torch.Tensor, ws=None, stream=None):
+    """colsq[k] += sum_m X[m, k]^2 (binary64, fixed order)."""
+    _dev_tensor(X, torch.float32, "X")
+    _dev_tensor(colsq, torch.float64, "colsq")
+    M, K = X.shape
+    ws, nb = _workspace(OP_COLSQ, M, 0, K, X.device, ws)
+    _check(lib().cham_act_colsq_accumulate(_ptr(X), M, K, _ptr(colsq), _ptr(ws), nb, _stream(stream)),
+           "act_colsq_accumulate")
+
+
+def mixed_linear_grouped(xq: "AQ", gq: GWQ, Y: Optional[torch.Tensor] = None, ws=None, stream=None) -> torch.Tensor:
+    if Y is None:
+        Y = torch.empty((xq.M, gq.N), dtype=torch.float32, device=xq.codes.device)
+    _dev_tensor(Y, torch.float32, "Y")
+    ws, nb = _workspace(OP_LINEAR, xq.M, gq.N, gq.K, Y.device, ws)
+    a, g = xq.struct(), gq.struct()
+    _check(lib().cham_mixed_linear_grouped(ctypes.byref(a), ctypes.byref(g), _ptr(Y), _ptr(ws), nb, _stream(stream)),
+           "mixed_linear_grouped")
+    return Y
 
 
 # -------------------------------------------------------------------------------------------

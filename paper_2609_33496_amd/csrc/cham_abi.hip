@@ -5,6 +5,8 @@
 size_t cham_stats_workspace_bytes(int64_t numel);
 size_t cham_quant_workspace_bytes(int64_t n);
 size_t cham_linear_workspace_bytes(int64_t M, int64_t N, int64_t K);
+size_t cham_gselect_workspace_bytes(int64_t N);
+size_t cham_colsq_workspace_bytes(int64_t K);
 
 extern "C" const char* cham_status_string(int status) {
     switch (status) {
@@ -27,6 +29,8 @@ extern "C" size_t cham_workspace_bytes(int32_t op, int64_t M, int64_t N, int64_t
     case CHAM_OP_STATS: return M > 0 ? cham_stats_workspace_bytes(M) : 0;
     case CHAM_OP_QUANT_ACT: return (M > 0 && K > 0) ? cham_quant_workspace_bytes(M * K) : 0;
     case CHAM_OP_LINEAR: return (M > 0 && N > 0 && K > 0) ? cham_linear_workspace_bytes(M, N, K) : 0;
+    case CHAM_OP_GSELECT: return cham_gselect_workspace_bytes(N);
+    case CHAM_OP_COLSQ: return cham_colsq_workspace_bytes(K);
     default: return 0;
     }
 }

@@ -196,6 +196,11 @@ struct RecArgs {
     ColPrep* cols;
     float* colsum;  // [N] sum over k of the dequantized weights
     uint4* rec;     // [K/64][N][2][pieces]
+    // group-scaled weights (the DiT search): the chosen group size on the device (NULL: the
+    // per-channel formats above), per-group scale / NF4 absmax and zero point [N][K/32]
+    const int32_t* gsel;
+    const float* gscale;
+    const float* gzero;
 };
 
 // Workgroup b handles 32 channels (block b % nblk) and the k-steps of chunk b / nblk.
@@ -246,8 +251,17 @@ CHAM_DEV void colsum_channel(const RecArgs& a, int n) {
     const int f = a.wfmt[n];
     double acc = 0.0;
     if (f < CHAM_W_NFMT && ((a.mask >> f) & 1u)) {
-        const float s = a.wscale[n], z = a.wzero[n];
+        const int gsz = a.gsel ? *a.gsel : 0;
+        float s = a.gsel ? 0.0f : a.wscale[n], z = a.gsel ? 0.0f : a.wzero[n];
         for (int k0 = 8 * lane; k0 < K; k0 += 512) {
+            float nfa = 0.0f;
+            if (gsz) {  // the 8 elements lie in one group (group sizes are multiples of 32)
+                s = a.gscale[(int64_t)n * (K / 32) + k0 / gsz];
+                z = a.gzero[(int64_t)n * (K / 32) + k0 / gsz];
+                nfa = s;
+            } else if (f == CHAM_W_NF4) {
+                nfa = a.wnf4[(int64_t)n * (K / 64) + k0 / 64];
+            }
             uint32_t w0, w1;
             if (a.code_bits == 4) {
                 const uint32_t w = *reinterpret_cast<const uint32_t*>(a.wc + (int64_t)n * (K / 2) + k0 / 2);
@@ -258,7 +272,6 @@ CHAM_DEV void colsum_channel(const RecArgs& a, int n) {
                 w0 = w.x;
                 w1 = w.y;
             }
-            const float nfa = f == CHAM_W_NF4 ? a.wnf4[(int64_t)n * (K / 64) + k0 / 64] : 0.0f;
             const int e8 = is_mx(f) ? (int)a.we8[(int64_t)n * (K / 32) + k0 / 32] : 0;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -305,12 +318,22 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     const int n = n0 + ((t & 63) >> 1), h = t & 1;
     const bool live = n < a.N;
     const int kb = kc * a.kchunk + (t >> 6), ke = min(nst, (kc + 1) * a.kchunk);
-    auto load_rec = [&](int k, uint4 (&code)[2], float& nfa, int& e8) __attribute__((always_inline)) {
+    const int gsz = a.gsel ? *a.gsel : 0;  // group size of group-scaled weights, else 0
+    // block parameters of a record: NF4 absmax (or the group's scale / absmax) in nfa, the
+    // group's zero point in gz, the MX exponent in e8
+    auto load_rec = [&](int k, uint4 (&code)[2], float& nfa, float& gz, int& e8) __attribute__((always_inline)) {
         const uint4* src = reinterpret_cast<const uint4*>(a.wc + n * cstride + (int64_t)k * (16 * a.code_bits / 2) +
                                                           (int64_t)h * 16 * cw);
         code[0] = src[0];
         code[1] = cw > 1 ? src[1] : make_uint4(0u, 0u, 0u, 0u);
-        nfa = a.wnf4 ? a.wnf4[(int64_t)n * (K / 64) + k] : 0.0f;
+        if (gsz) {
+            const int64_t j = (int64_t)n * (K / 32) + (64 * k + 32 * h) / gsz;
+            nfa = a.gscale[j];
+            gz = a.gzero[j];
+        } else {
+            nfa = a.wnf4 ? a.wnf4[(int64_t)n * (K / 64) + k] : 0.0f;
+            gz = 0.0f;
+        }
         e8 = a.we8 ? (int)a.we8[(int64_t)n * (K / 32) + 2 * k + h] : 0;
     };
     auto store_rec = [&](int k, const uint4 (&code)[2], const Table& tb) __attribute__((always_inline)) {
@@ -321,11 +344,11 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
         dst[cw + 1] = make_uint4(tb.hi[0], tb.hi[1], tb.hi[2], tb.hi[3]);
     };
     uint4 pc[kRecPrefetch][2];
-    float pn[kRecPrefetch];
+    float pn[kRecPrefetch], pz[kRecPrefetch];
     int pe[kRecPrefetch];
 #pragma unroll
     for (int i = 0; i < kRecPrefetch; ++i)
-        if (live && kb + 4 * i < ke) load_rec(kb + 4 * i, pc[i], pn[i], pe[i]);
+        if (live && kb + 4 * i < ke) load_rec(kb + 4 * i, pc[i], pn[i], pz[i], pe[i]);
 
     {
         const int ch = t >> 3, sub = t & 7;
@@ -346,7 +369,25 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
 #pragma unroll 4
             for (int b = sub; b < K / 32; b += 8) mxe = max(mxe, (int)r[b]);
         }
-        if (!(ok && f == CHAM_W_NF4)) mxf = 0.0f;
+        if (gsz && nn < a.N && ok && !is_mx(f)) {
+            // group-scaled: the largest decoded magnitude over the channel's groups
+            const int G = (K + gsz - 1) / gsz;
+            const float* gs = a.gscale + (int64_t)nn * (K / 32);
+            const float* gzr = a.gzero + (int64_t)nn * (K / 32);
+            for (int j = sub; j < G; j += 8) {
+                float m = gs[j];  // NF4: the group absmax
+                if (f == CHAM_W_FP4) m = 6.0f * gs[j];
+                else if (f == CHAM_W_INT4_SYM) m = 7.0f * gs[j];
+                else if (f == CHAM_W_INT8_SYM) m = 127.0f * gs[j];
+                else if (f == CHAM_W_INT4_ASYM || f == CHAM_W_INT8_ASYM) {
+                    const float L = f == CHAM_W_INT4_ASYM ? 15.0f : 255.0f;
+                    m = fmaxf(fabsf(gzr[j]), fabsf(L - gzr[j])) * gs[j];
+                }
+                mxf = fmaxf(mxf, m);
+            }
+        } else if (!(ok && f == CHAM_W_NF4)) {
+            mxf = 0.0f;
+        }
         if (!(ok && is_mx(f))) mxe = 0;
 #pragma unroll
         for (int o = 1; o < 8; o <<= 1) {
@@ -354,7 +395,12 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
             mxe = max(mxe, __shfl_xor(mxe, o, kWave));
         }
         ColPrep c{CHAM_W_NFMT, 0, 0.0f, 0.0f};
-        if (ok) {
+        if (ok && gsz && !is_mx(f)) {
+            // group-scaled: every table is relative to the channel's largest decoded magnitude
+            c.fmt = f;
+            c.eref = floor_log2(floor_scale(mxf)) - 14;
+            c.colscale = ldexpf(1.0f, c.eref);
+        } else if (ok) {
             c.fmt = f;
             c.zero = a.wzero[nn];
             if (f == CHAM_W_NF4) {
@@ -381,15 +427,18 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     __syncthreads();
     if (!live) return;
     const ColPrep c = cp[(t & 63) >> 1];
+    auto table = [&](float nfa, float gz, int e8) __attribute__((always_inline)) {
+        return gsz && !is_mx(c.fmt) ? group_table(c, nfa, gz) : record_table(c, nfa, e8);
+    };
 #pragma unroll
     for (int i = 0; i < kRecPrefetch; ++i)
-        if (kb + 4 * i < ke) store_rec(kb + 4 * i, pc[i], record_table(c, pn[i], pe[i]));
+        if (kb + 4 * i < ke) store_rec(kb + 4 * i, pc[i], table(pn[i], pz[i], pe[i]));
     for (int k = kb + 4 * kRecPrefetch; k < ke; k += 4) {
         uint4 code[2];
-        float nfa;
+        float nfa, gz;
         int e8;
-        load_rec(k, code, nfa, e8);
-        store_rec(k, code, record_table(c, nfa, e8));
+        load_rec(k, code, nfa, gz, e8);
+        store_rec(k, code, table(nfa, gz, e8));
     }
 }
 
@@ -951,11 +1000,39 @@ static Layout layout_at(void* p, int64_t N) {
     return l;
 }
 
+// One searched weight as the record pre-pass and the GEMM see it: per-channel formats
+// (cham_wq) or group-scaled weights of one format (cham_gwq).
+struct WView {
+    int64_t N, K;
+    uint32_t mask;
+    int code_bits;
+    const uint8_t* fmt;
+    const float* scale;
+    const float* zero;
+    const float* nf4;
+    const uint8_t* e8;
+    const uint8_t* codes;
+    void* packed;
+    const int32_t* gsel;
+    const float* gscale;
+    const float* gzero;
+};
+
+static WView view_of(const cham_wq* wq) {
+    return WView{wq->N, wq->K, wq->palette_mask, wq->code_bits, wq->fmt, wq->scale, wq->zero, wq->nf4_absmax,
+                 wq->e8m0, wq->codes, wq->packed, nullptr, nullptr, nullptr};
+}
+
+static WView view_of(const cham_gwq* gq) {
+    return WView{gq->N, gq->K, gq->palette_mask, gq->code_bits, gq->fmt, nullptr, nullptr, nullptr,
+                 gq->e8m0, gq->codes, gq->packed, gq->choice, gq->gscale, gq->gzero};
+}
+
 // Record pre-pass arguments of one searched weight writing into the layout L (device),
 // and the workgroups it takes.
-static RecArgs record_args(const cham_wq* wq, const Layout& L, int* wgs) {
-    const uint32_t mask = wq->palette_mask;
-    const int N = (int)wq->N, K = (int)wq->K;
+static RecArgs record_args(const WView& v, const Layout& L, int* wgs) {
+    const uint32_t mask = v.mask;
+    const int N = (int)v.N, K = (int)v.K;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
     // about one workgroup per CU per layer (all of a batch resident at once), at least 4
@@ -965,19 +1042,19 @@ static RecArgs record_args(const cham_wq* wq, const Layout& L, int* wgs) {
     const int rchunk = (nst + nkc - 1) / nkc;
     *wgs = nblk * ((nst + rchunk - 1) / rchunk);
     // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
-    return RecArgs{wq->fmt, wq->scale, wq->zero, nf4 ? wq->nf4_absmax : nullptr, wmx ? wq->e8m0 : nullptr, wq->codes,
-                   mask, N, K, wq->code_bits, rchunk, L.cols, L.colsum, L.rec};
+    return RecArgs{v.fmt, v.scale, v.zero, nf4 && !v.gsel ? v.nf4 : nullptr, wmx ? v.e8 : nullptr, v.codes,
+                   mask, N, K, v.code_bits, rchunk, L.cols, L.colsum, L.rec, v.gsel, v.gscale, v.gzero};
 }
 
 static int colsum_wgs(int64_t N) { return (int)((N + 3) / 4); }
 
-static void launch_records(const cham_wq* wq, const Layout& L, hipStream_t s) {
+static void launch_records(const WView& v, const Layout& L, hipStream_t s) {
     RecBatch B;
     B.nl = 1;
     B.ng = 0;
     int wgs = 0;
-    B.r[0] = record_args(wq, L, &wgs);
-    B.cs_end[0] = colsum_wgs(wq->N);
+    B.r[0] = record_args(v, L, &wgs);
+    B.cs_end[0] = colsum_wgs(v.N);
     B.wg_end[0] = wgs;
     hipLaunchKernelGGL(record_kernel, dim3((unsigned)(wgs + B.cs_end[0])), dim3(256), 0, s, B);
 }
@@ -994,7 +1071,7 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
         for (int j = 0; j < B.nl; ++j) {
             const cham_wq* wq = wqs[i0 + j];
             int wgs = 0;
-            B.r[j] = record_args(wq, layout_at(wq->packed, wq->N), &wgs);
+            B.r[j] = record_args(view_of(wq), layout_at(wq->packed, wq->N), &wgs);
             total += wgs;
             B.wg_end[j] = total;
             cs += colsum_wgs(wq->N);
@@ -1004,6 +1081,14 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
         hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + cs + B.ng)), dim3(256), 0, s, B);
         CHAM_CHECK_LAUNCH();
     }
+    return CHAM_OK;
+}
+
+// The packed layout of a group-scaled weight (called by the grouped search after its
+// launches, which have checked the arguments).
+int cham_pack_grouped(const cham_gwq* gq, hipStream_t s) {
+    launch_records(view_of(gq), layout_at(gq->packed, gq->N), s);
+    CHAM_CHECK_LAUNCH();
     return CHAM_OK;
 }
 
@@ -1029,17 +1114,20 @@ extern "C" int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bi
     return CHAM_OK;
 }
 
-extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
-                                 void* stream) {
-    if (!xq || !wq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
-    if (!wq->fmt || !wq->codes || !wq->scale || !wq->zero) return CHAM_EINVAL;
+static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* ws, size_t ws_bytes, void* stream) {
+    const WView* wq = &v;
+    if (!xq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
+    if (!wq->fmt || !wq->codes) return CHAM_EINVAL;
+    if (!wq->gsel && (!wq->scale || !wq->zero)) return CHAM_EINVAL;
+    if (wq->gsel && (!wq->gscale || !wq->gzero)) return CHAM_EINVAL;
     if (xq->M < 1 || wq->N < 1 || xq->K < 1 || xq->K != wq->K) return CHAM_EINVAL;
     if (xq->fmt < 0 || xq->fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
     if (xq->nsamples < 1 || xq->M % xq->nsamples != 0) return CHAM_EINVAL;
-    const uint32_t mask = wq->palette_mask;
+    const uint32_t mask = wq->mask;
     if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
     const int code_bits = (mask & 0x7u) ? 8 : 4;
     if (wq->code_bits != code_bits) return CHAM_EFORMAT;
+    if (wq->gsel && code_bits != 4) return CHAM_EFORMAT;  // the 8-bit group-scaled decode is not built
     if (xq->K % 64 != 0) return CHAM_ESHAPE;
     // 32-bit buffer offsets: a 256-row activation tile and the weight records stay below
     // 2^31 bytes
@@ -1048,7 +1136,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
-    if ((nf4 && !wq->nf4_absmax) || (wmx && !wq->e8m0)) return CHAM_EINVAL;
+    if ((nf4 && !wq->gsel && !wq->nf4) || (wmx && !wq->e8)) return CHAM_EINVAL;
     const bool amx = xq->fmt == CHAM_A_MXFP8_E4M3 || xq->fmt == CHAM_A_MXINT8;
     if (amx && !xq->e8m0) return CHAM_EINVAL;
     if (((uintptr_t)xq->codes & 15u) || ((uintptr_t)wq->codes & 15u) || ((uintptr_t)wq->packed & 255u))
@@ -1078,7 +1166,7 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
 
-    if (!wq->packed) launch_records(wq, lay, s);
+    if (!wq->packed) launch_records(v, lay, s);
     CHAM_CHECK_LAUNCH();
 
     GemmArgs a;
@@ -1115,4 +1203,16 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;
+}
+
+extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
+                                 void* stream) {
+    if (!wq) return CHAM_EINVAL;
+    return mixed_linear_impl(xq, view_of(wq), Y, ws, ws_bytes, stream);
+}
+
+extern "C" int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, float* Y, void* ws, size_t ws_bytes,
+                                         void* stream) {
+    if (!gq || !gq->choice) return CHAM_EINVAL;
+    return mixed_linear_impl(xq, view_of(gq), Y, ws, ws_bytes, stream);
 }

@@ -133,6 +133,20 @@ CHAM_DEV Table record_table(const ColPrep& c, float nf4a, int e8) {
     return tb;
 }
 
+// Table of a half k-step of a group-scaled 4-bit weight (the DiT search): the base values
+// of the channel's format times the group's scale (NF4: absmax) over 2^eref; INT-asym with
+// the group's zero point.
+CHAM_DEV Table group_table(const ColPrep& c, float gscale, float gzero) {
+    const float factor = ldexpf(gscale, -c.eref);
+    switch (c.fmt) {
+    case CHAM_W_NF4: return table_fmt<CHAM_W_NF4>(0.0f, factor);
+    case CHAM_W_FP4: return table_fmt<CHAM_W_FP4>(0.0f, factor);
+    case CHAM_W_INT4_ASYM: return table_fmt<CHAM_W_INT4_ASYM>(gzero, factor);
+    case CHAM_W_INT4_SYM: return table_fmt<CHAM_W_INT4_SYM>(0.0f, factor);
+    default: return Table{{0u, 0u, 0u, 0u}, {0u, 0u, 0u, 0u}};
+    }
+}
+
 }  // namespace cham
 
 #endif  // CHAM_RECORDS_H_
