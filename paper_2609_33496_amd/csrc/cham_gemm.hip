@@ -48,6 +48,10 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
+#ifndef CHAM_GEMM_SCHED
+#define CHAM_GEMM_SCHED 0
+#endif
+
 constexpr int BK = 64;
 constexpr int kThreads = 256;
 // TN = 32-channel MFMA blocks per wavefront: a tile is 128 TN channels wide (four wavefronts)
@@ -194,7 +198,8 @@ struct RecArgs {
     int N, K, code_bits;
     int kchunk;  // k-steps per workgroup
     ColPrep* cols;
-    float* colsum;  // [N] sum over k of the dequantized weights
+    float* colsum;  // [k-chunks][N] per workgroup chunk of k-steps: the sum of the channel's
+                    // decoded weights (the GEMM adds the chunks in order)
     uint4* rec;     // [K/64][N][2][pieces]
     // group-scaled weights (the DiT search): the chosen group size on the device (NULL: the
     // per-channel formats above), per-group scale / NF4 absmax and zero point [N][K/32]
@@ -221,70 +226,10 @@ constexpr int kRecPrefetch = 3;
 constexpr int kRecBatchMax = 16;
 struct RecBatch {
     int nl, ng;
-    int cs_end[kRecBatchMax];  // column-sum workgroups of layers 0..i
     int wg_end[kRecBatchMax];  // record workgroups of layers 0..i
     RecArgs r[kRecBatchMax];
     GroupArgs g[kRecBatchMax];
 };
-
-// Dequantized weight of code u in format f (App. A.11, as the quantizers define it).
-CHAM_DEV float dequant_code(int f, uint32_t u, float s, float z, float nfa, int e8) {
-    const int q8 = (int)(int8_t)(uint8_t)u, q4 = (int)(u << 28) >> 28;
-    switch (f) {
-    case CHAM_W_INT8_SYM: return (float)q8 * s;
-    case CHAM_W_INT4_SYM: return (float)q4 * s;
-    case CHAM_W_INT8_ASYM:
-    case CHAM_W_INT4_ASYM: return ((float)u - z) * s;
-    case CHAM_W_FP4: return e2m1_decode(u) * s;
-    case CHAM_W_NF4: return nf4_level(u) * nfa;
-    case CHAM_W_MXINT8: return ldexpf((float)q8, e8 - 127 - 6);
-    case CHAM_W_MXINT4: return ldexpf((float)q4, e8 - 127 - 2);
-    default: return ldexpf(e2m1_decode(u), e8 - 127);  // MXFP4
-    }
-}
-
-// Column sum of channel n (one wavefront): lane l adds elements 8(l + 64 j) .. + 7 in order
-// in binary64, then the lanes are added by a fixed tree, so the sum is the same every run.
-CHAM_DEV void colsum_channel(const RecArgs& a, int n) {
-    const int lane = threadIdx.x & 63;
-    const int K = a.K;
-    const int f = a.wfmt[n];
-    double acc = 0.0;
-    if (f < CHAM_W_NFMT && ((a.mask >> f) & 1u)) {
-        const int gsz = a.gsel ? *a.gsel : 0;
-        float s = a.gsel ? 0.0f : a.wscale[n], z = a.gsel ? 0.0f : a.wzero[n];
-        for (int k0 = 8 * lane; k0 < K; k0 += 512) {
-            float nfa = 0.0f;
-            if (gsz) {  // the 8 elements lie in one group (group sizes are multiples of 32)
-                s = a.gscale[(int64_t)n * (K / 32) + k0 / gsz];
-                z = a.gzero[(int64_t)n * (K / 32) + k0 / gsz];
-                nfa = s;
-            } else if (f == CHAM_W_NF4) {
-                nfa = a.wnf4[(int64_t)n * (K / 64) + k0 / 64];
-            }
-            uint32_t w0, w1;
-            if (a.code_bits == 4) {
-                const uint32_t w = *reinterpret_cast<const uint32_t*>(a.wc + (int64_t)n * (K / 2) + k0 / 2);
-                w0 = (w & 0x0F0F0F0Fu);  // even k of the 8, one per byte
-                w1 = (w >> 4) & 0x0F0F0F0Fu;
-            } else {
-                const uint2 w = *reinterpret_cast<const uint2*>(a.wc + (int64_t)n * K + k0);
-                w0 = w.x;
-                w1 = w.y;
-            }
-            const int e8 = is_mx(f) ? (int)a.we8[(int64_t)n * (K / 32) + k0 / 32] : 0;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                // 4-bit layout: k0 + j is byte j/2 of the word, even j low nibble
-                const uint32_t u = a.code_bits == 4 ? (((j & 1) ? w1 : w0) >> (8 * (j >> 1))) & 0xFFu
-                                                    : ((j < 4 ? w0 : w1) >> (8 * (j & 3))) & 0xFFu;
-                acc += (double)dequant_code(f, u, s, z, nfa, e8);
-            }
-        }
-    }
-    acc = wave_sum(acc);
-    if (lane == 0) a.colsum[n] = (float)acc;
-}
 
 __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
     __shared__ ColPrep cp[kRecChannels];
@@ -292,16 +237,7 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
         group_channels<256>(B.g[blockIdx.x], nullptr);
         return;
     }
-    const int cb_all = (int)blockIdx.x - B.ng;
-    if (cb_all < B.cs_end[B.nl - 1]) {  // column sums: four channels per workgroup
-        int li = 0;
-        while (li + 1 < B.nl && cb_all >= B.cs_end[li]) ++li;
-        const RecArgs& a = B.r[li];
-        const int n = 4 * (cb_all - (li ? B.cs_end[li - 1] : 0)) + (threadIdx.x >> 6);
-        if (n < a.N) colsum_channel(a, n);
-        return;
-    }
-    const int rb = cb_all - B.cs_end[B.nl - 1];  // record workgroup index
+    const int rb = (int)blockIdx.x - B.ng;  // record workgroup index
     int li = 0;
     while (li + 1 < B.nl && rb >= B.wg_end[li]) ++li;
     const RecArgs& a = B.r[li];
@@ -425,20 +361,61 @@ __global__ __launch_bounds__(256) void record_kernel(RecBatch B) {
         }
     }
     __syncthreads();
-    if (!live) return;
     const ColPrep c = cp[(t & 63) >> 1];
     auto table = [&](float nfa, float gz, int e8) __attribute__((always_inline)) {
         return gsz && !is_mx(c.fmt) ? group_table(c, nfa, gz) : record_table(c, nfa, e8);
     };
+    // the sum of the record's decoded weights (the half-precision values the GEMM uses,
+    // relative to colscale), through the GEMM's own decode and binary32 dot products
+    const bool int8c = a.code_bits == 8 && is_8bit(c.fmt);
+    auto record_sum = [&](const uint4 (&code)[2], const Table& tb) __attribute__((always_inline)) {
+        float sum = 0.0f;
+        const half2v one = {(_Float16)1.0f, (_Float16)1.0f};
 #pragma unroll
-    for (int i = 0; i < kRecPrefetch; ++i)
-        if (kb + 4 * i < ke) store_rec(kb + 4 * i, pc[i], table(pn[i], pz[i], pe[i]));
-    for (int k = kb + 4 * kRecPrefetch; k < ke; k += 4) {
-        uint4 code[2];
-        float nfa, gz;
-        int e8;
-        load_rec(k, code, nfa, gz, e8);
-        store_rec(k, code, table(nfa, gz, e8));
+        for (int q = 0; q < 4; ++q) {
+            H8 v;
+            if (a.code_bits == 4) {
+                const uint32_t w = q == 0 ? code[0].x : q == 1 ? code[0].y : q == 2 ? code[0].z : code[0].w;
+                v.h = decode_nibbles(tb, w);
+            } else {
+                const uint4& cc = code[q >> 1];
+                const uint32_t w0 = (q & 1) ? cc.z : cc.x, w1 = (q & 1) ? cc.w : cc.y;
+                v.h = int8c ? decode_bytes_int(tb, w0, w1) : decode_bytes_table(tb, w0, w1);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sum = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, v.u[r]), one, sum, false);
+        }
+        return sum;
+    };
+    double psum = 0.0;
+    if (live) {
+#pragma unroll
+        for (int i = 0; i < kRecPrefetch; ++i)
+            if (kb + 4 * i < ke) {
+                const Table tb = table(pn[i], pz[i], pe[i]);
+                store_rec(kb + 4 * i, pc[i], tb);
+                psum += (double)record_sum(pc[i], tb);
+            }
+        for (int k = kb + 4 * kRecPrefetch; k < ke; k += 4) {
+            uint4 code[2];
+            float nfa, gz;
+            int e8;
+            load_rec(k, code, nfa, gz, e8);
+            const Table tb = table(nfa, gz, e8);
+            store_rec(k, code, tb);
+            psum += (double)record_sum(code, tb);
+        }
+    }
+    // the channel's sum over this workgroup's k-steps: its 8 threads (2 halves x 4 k-phases)
+    // added in a fixed order, times the channel's scale
+    __shared__ double part[4][64];
+    part[t >> 6][t & 63] = psum;
+    __syncthreads();
+    if (t < kRecChannels && n0 + t < a.N) {
+        double s2 = 0.0;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) s2 += part[p][2 * t] + part[p][2 * t + 1];
+        a.colsum[(int64_t)kc * a.N + n0 + t] = (float)(s2 * (double)cp[t].colscale);
     }
 }
 
@@ -461,7 +438,8 @@ struct GemmArgs {
     const float* xz;         // activation zero point per sample
     int rps;                 // rows per sample
     const ColPrep* cols;     // [N]
-    const float* colsum;     // [N] sum over k of the dequantized weights
+    const float* colsum;     // [nkc][N] per k-chunk sums of the decoded weights
+    int nkc;
     const uint4* rec;        // [K/64][N][2][pieces]
     float* Y;
     int M, N, K;
@@ -645,7 +623,9 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
         const ColPrep cp = n < N ? a.cols[n] : ColPrep{CHAM_W_NFMT, 0, 0.0f, 0.0f};
         int8[j] = CODE_BITS == 8 && is_8bit(cp.fmt);
         cs[j] = cp.colscale;
-        csum[j] = (AF == kAInt8 && n < N) ? a.colsum[n] : 0.0f;
+        csum[j] = 0.0f;
+        if (AF == kAInt8 && n < N)
+            for (int q = 0; q < a.nkc; ++q) csum[j] += a.colsum[(int64_t)q * N + n];
     }
     auto decode = [&](const Rec& r, int j, int s) __attribute__((always_inline)) -> half8 {
         if (CODE_BITS == 4) {
@@ -709,6 +689,19 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
             for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
     };
+    // the decode of the next sub-step's weights spread between this sub-step's MFMAs, so the
+    // VALU work issues while the matrix cores run
+    auto interleave = [&]() __attribute__((always_inline)) {
+#if CHAM_GEMM_SCHED == 1
+        constexpr int NM = TM * TN;
+        constexpr int VPM = (24 * TN * (CODE_BITS / 4) + NM - 1) / NM + 1;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
+        }
+#endif
+    };
     auto step = [&](int k, int buf, const WStage& Wc, const WStage& Wn, WStage& Wl, AStage& Ra)
                     __attribute__((always_inline)) {
         if (k + 1 < nsteps) store_a(Ra, buf ^ 1);
@@ -723,6 +716,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
 #pragma unroll
             for (int j = 0; j < TN; ++j) bn[j] = decode(Wc.r[j], j, s + 1);
             mfmas();
+            interleave();
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < TM; ++i) af[i] = an[i];
@@ -737,6 +731,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
 #pragma unroll
         for (int j = 0; j < TN; ++j) bn[j] = decode(Wn.r[j], j, 0);
         mfmas();
+        interleave();
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < TM; ++i) af[i] = an[i];
@@ -895,6 +890,9 @@ int col_tiles(int N, int tn) { return (N + tile_width(tn) - 1) / tile_width(tn);
 Plan plan_gemm(int M, int N, int K, int code_bits) {
     const int P = cu_count();
     const int nsteps = K / BK;
+#ifdef CHAM_FORCE_BM
+    if (code_bits == 4) return Plan{1, 1, {Launch{0, M, CHAM_FORCE_BM, 2}, Launch{0, 0, 0, 0}}};
+#endif
     TileCost costs[kNumTiles];
     for (int b = 0; b < kNumTiles; ++b) costs[b] = kTileCosts[b];
     if (code_bits != 4) {  // the full-width 128-high tile with 8-bit codes: one per CU
@@ -978,10 +976,21 @@ int64_t record_bytes(int64_t N, int64_t K) { return N * (K / BK) * 2 * 64; }
 
 using namespace cham;
 
-// The packed layout: ColPrep[N], the column sums [N], then the records.
+// Chunks of k-steps the record pre-pass splits a weight into: about one workgroup per CU per
+// layer (all of a batch resident at once), at least 4 k-steps each.
+static void rec_chunks(int64_t N, int64_t K, int* nkc, int* rchunk) {
+    const int nblk = (int)((N + kRecChannels - 1) / kRecChannels), nst = (int)(K / BK);
+    const int n = std::max(1, std::min((256 + nblk - 1) / nblk, (nst + 3) / 4));
+    *rchunk = (nst + n - 1) / n;
+    *nkc = (nst + *rchunk - 1) / *rchunk;
+}
+
+// The packed layout: ColPrep[N], the column-sum partials [k-chunks][N], then the records.
 extern "C" size_t cham_packed_bytes(int64_t N, int64_t K) {
-    if (N < 1 || K < 1) return 0;
-    return align256((size_t)N * sizeof(ColPrep)) + align256((size_t)N * 4) + (size_t)record_bytes(N, K);
+    if (N < 1 || K < 64) return 0;
+    int nkc, rchunk;
+    rec_chunks(N, K, &nkc, &rchunk);
+    return align256((size_t)N * sizeof(ColPrep)) + align256((size_t)nkc * (size_t)N * 4) + (size_t)record_bytes(N, K);
 }
 
 struct Layout {
@@ -989,13 +998,15 @@ struct Layout {
     float* colsum;
     uint4* rec;
 };
-static Layout layout_at(void* p, int64_t N) {
+static Layout layout_at(void* p, int64_t N, int64_t K) {
+    int nkc, rchunk;
+    rec_chunks(N, K, &nkc, &rchunk);
     char* c = (char*)p;
     Layout l;
     l.cols = (ColPrep*)c;
     c += align256((size_t)N * sizeof(ColPrep));
     l.colsum = (float*)c;
-    c += align256((size_t)N * 4);
+    c += align256((size_t)nkc * (size_t)N * 4);
     l.rec = (uint4*)c;
     return l;
 }
@@ -1035,18 +1046,14 @@ static RecArgs record_args(const WView& v, const Layout& L, int* wgs) {
     const int N = (int)v.N, K = (int)v.K;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
-    // about one workgroup per CU per layer (all of a batch resident at once), at least 4
-    // k-steps each
-    const int nblk = (N + kRecChannels - 1) / kRecChannels, nst = K / BK;
-    const int nkc = std::max(1, std::min((256 + nblk - 1) / nblk, (nst + 3) / 4));
-    const int rchunk = (nst + nkc - 1) / nkc;
-    *wgs = nblk * ((nst + rchunk - 1) / rchunk);
+    const int nblk = (N + kRecChannels - 1) / kRecChannels;
+    int nkc, rchunk;
+    rec_chunks(N, K, &nkc, &rchunk);
+    *wgs = nblk * nkc;
     // block metadata only of the enabled formats (the pre-pass reads it ahead of the format)
     return RecArgs{v.fmt, v.scale, v.zero, nf4 && !v.gsel ? v.nf4 : nullptr, wmx ? v.e8 : nullptr, v.codes,
                    mask, N, K, v.code_bits, rchunk, L.cols, L.colsum, L.rec, v.gsel, v.gscale, v.gzero};
 }
-
-static int colsum_wgs(int64_t N) { return (int)((N + 3) / 4); }
 
 static void launch_records(const WView& v, const Layout& L, hipStream_t s) {
     RecBatch B;
@@ -1054,9 +1061,8 @@ static void launch_records(const WView& v, const Layout& L, hipStream_t s) {
     B.ng = 0;
     int wgs = 0;
     B.r[0] = record_args(v, L, &wgs);
-    B.cs_end[0] = colsum_wgs(v.N);
     B.wg_end[0] = wgs;
-    hipLaunchKernelGGL(record_kernel, dim3((unsigned)(wgs + B.cs_end[0])), dim3(256), 0, s, B);
+    hipLaunchKernelGGL(record_kernel, dim3((unsigned)wgs), dim3(256), 0, s, B);
 }
 
 // Writes the packed layout of n searched weights (called by the search entry points, which
@@ -1067,18 +1073,16 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
         RecBatch B;
         B.nl = std::min(kRecBatchMax, n - i0);
         B.ng = 0;
-        int total = 0, cs = 0;
+        int total = 0;
         for (int j = 0; j < B.nl; ++j) {
             const cham_wq* wq = wqs[i0 + j];
             int wgs = 0;
-            B.r[j] = record_args(view_of(wq), layout_at(wq->packed, wq->N), &wgs);
+            B.r[j] = record_args(view_of(wq), layout_at(wq->packed, wq->N, wq->K), &wgs);
             total += wgs;
             B.wg_end[j] = total;
-            cs += colsum_wgs(wq->N);
-            B.cs_end[j] = cs;
             if (wq->perm || wq->group_off) B.g[B.ng++] = GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off};
         }
-        hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + cs + B.ng)), dim3(256), 0, s, B);
+        hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + B.ng)), dim3(256), 0, s, B);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;
@@ -1087,7 +1091,7 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
 // The packed layout of a group-scaled weight (called by the grouped search after its
 // launches, which have checked the arguments).
 int cham_pack_grouped(const cham_gwq* gq, hipStream_t s) {
-    launch_records(view_of(gq), layout_at(gq->packed, gq->N), s);
+    launch_records(view_of(gq), layout_at(gq->packed, gq->N, gq->K), s);
     CHAM_CHECK_LAUNCH();
     return CHAM_OK;
 }
@@ -1156,7 +1160,7 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     float* rowscale = (float*)w;
     w += align256((size_t)M * 4);
     // the search's packed layout replaces the pre-pass
-    const Layout lay = layout_at(wq->packed ? wq->packed : (void*)w, N);
+    const Layout lay = layout_at(wq->packed ? wq->packed : (void*)w, N, K);
     w += align256(cham_packed_bytes(N, K));
     float* part = (float*)w;
 
@@ -1178,6 +1182,10 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     a.rps = M / xq->nsamples;
     a.cols = lay.cols;
     a.colsum = lay.colsum;
+    {
+        int rchunk;
+        rec_chunks(N, K, &a.nkc, &rchunk);
+    }
     a.rec = lay.rec;
     a.Y = Y;
     a.M = M;
