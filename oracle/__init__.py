@@ -95,6 +95,7 @@ def _load():
     lib.orc_gq_row.argtypes = [i32, i32, P, i64, P, P, P, P, P]
     lib.orc_linear.argtypes = [i64, i64, i64, P, P, P, P]
     lib.orc_linear_pairs.argtypes = [i64, i64, P, P, P, P, P, P]
+    lib.orc_conv3x3.argtypes = [i64, i64, i64, i64, i64, P, P, P, P]
     if not lib.orc_rounding_ok():
         raise RuntimeError("oracle requires round-to-nearest-even")
     _lib = lib
@@ -402,3 +403,18 @@ def linear_pairs(Xh: np.ndarray, Wh: np.ndarray, mm: np.ndarray, nn: np.ndarray)
     Bm = np.zeros(mm.shape[0], np.float64)
     _load().orc_linear_pairs(K, mm.shape[0], _p(mm), _p(nn), _p(Xh), _p(Wh), _p(Y), _p(Bm))
     return Y, Bm
+
+
+def conv3x3(Xh: np.ndarray, Wh: np.ndarray):
+    """3x3 convolution, stride 1, zero padding 1, on dequantized operands (binary64):
+    Xh [B, H, W, C] channels last, Wh [Co, 9C] with k = (ky * 3 + kx) * C + c.
+    Returns (Y [B, H, W, Co], sum of |products| [B, H, W, Co])."""
+    Xh, Wh = _f32(Xh), _f32(Wh)
+    B, H, W, C = Xh.shape
+    Co = Wh.shape[0]
+    assert Wh.shape[1] == 9 * C
+    Y = np.zeros((B, H, W, Co), np.float64)
+    Bm = np.zeros((B, H, W, Co), np.float64)
+    _load().orc_conv3x3(B, H, W, C, Co, _p(Xh), _p(Wh), _p(Y), _p(Bm))
+    return Y, Bm
+

@@ -824,3 +824,35 @@ void orc_gq_row(int f, int g, const float* w, int64_t K, uint8_t* codes, float* 
                 float* gz, uint8_t* e8) {
     gq_row(f, g, w, K, codes, wh, gs, gz, e8);
 }
+
+/* ------------------------------------------------------------------------- */
+/* 3x3 convolution (stride 1, zero padding 1) on dequantized operands -- the UNet   */
+/* path's conv layers, e.g. the up-block resnet conv1 downstream of a shortcut     */
+/* concatenation that Sec. 4.6 routes to MXFP8 -- in binary64.  Xh [B][H][W][C]      */
+/* (channels last), Wh [Co][3][3][C] (tap-major rows of 9C, the linear layer's      */
+/* [N][K] with K = 9C), Y [B][H][W][Co]; Babs the sum of |products| (tolerance).    */
+/* ------------------------------------------------------------------------- */
+void orc_conv3x3(int64_t B, int64_t H, int64_t W, int64_t C, int64_t Co, const float* Xh,
+                 const float* Wh, double* Y, double* Babs) {
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t y = 0; y < H; ++y)
+            for (int64_t x = 0; x < W; ++x)
+                for (int64_t o = 0; o < Co; ++o) {
+                    double acc = 0.0, ab = 0.0;
+                    for (int64_t ky = 0; ky < 3; ++ky)
+                        for (int64_t kx = 0; kx < 3; ++kx) {
+                            const int64_t yy = y + ky - 1, xx = x + kx - 1;
+                            if (yy < 0 || yy >= H || xx < 0 || xx >= W) continue;
+                            const float* xp = Xh + ((b * H + yy) * W + xx) * C;
+                            const float* wp = Wh + o * 9 * C + (ky * 3 + kx) * C;
+                            for (int64_t c = 0; c < C; ++c) {
+                                const double p = (double)xp[c] * (double)wp[c];
+                                acc += p;
+                                ab += fabs(p);
+                            }
+                        }
+                    const int64_t i = ((b * H + y) * W + x) * Co + o;
+                    Y[i] = acc;
+                    if (Babs) Babs[i] = ab;
+                }
+}

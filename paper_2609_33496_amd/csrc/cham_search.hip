@@ -9,7 +9,7 @@
 // per-element reconstructions are the exact binary32 values the format defines (E2M1 via
 // the gfx950 FP4 converters, which round to nearest even and saturate exactly as the format
 // requires; NF4 through a 33-cell table in LDS plus one exact threshold comparison).  If
-// the two smallest error sums are within 2^-12 of each other -- far above the binary32
+// the two smallest error sums are within 2^-15 of each other -- above the binary32
 // summation error -- the errors of every enabled format are recomputed with binary64 sums,
 // so the choice is always the binary64 argmin.  The winner's codes and metadata are then
 // written packed.  Nothing is re-read from HBM.
@@ -412,13 +412,13 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     const float amax = fmaxf(fabsf(lo), fabsf(hi));
 
     RowParams p;
-    p.s_sym8 = floor_scale(amax / 127.0f); p.r_sym8 = 1.0f / p.s_sym8;
-    p.s_sym4 = floor_scale(amax / 7.0f);   p.r_sym4 = 1.0f / p.s_sym4;
+    p.s_sym8 = floor_scale(amax / 127.0f); p.r_sym8 = rcp_rn(p.s_sym8);
+    p.s_sym4 = floor_scale(amax / 7.0f);   p.r_sym4 = rcp_rn(p.s_sym4);
     int_asym_scale_zp(lo, hi, 255.0f, &p.s_as8, &p.z_as8);
-    p.r_as8 = 1.0f / p.s_as8;
+    p.r_as8 = rcp_rn(p.s_as8);
     int_asym_scale_zp(lo, hi, 15.0f, &p.s_as4, &p.z_as4);
-    p.r_as4 = 1.0f / p.s_as4;
-    p.s_fp4 = floor_scale(amax / 6.0f); p.r_fp4 = 1.0f / p.s_fp4;
+    p.r_as4 = rcp_rn(p.s_as4);
+    p.s_fp4 = floor_scale(amax / 6.0f); p.r_fp4 = rcp_rn(p.s_fp4);
 
     // ---- binary32 error sums of every enabled format, one fused pass
     float e[CHAM_W_NFMT];
@@ -478,8 +478,11 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 #pragma unroll
     for (int f = 0; f < CHAM_W_NFMT; ++f) ed[f] = (double)e[f];
     // ---- near tie (or exact tie), or sums outside binary32's comfortable range (tiny or
-    // huge rows): binary64 re-check of every enabled format
-    if (second >= 0 && (!(es - eb > 0x1p-12f * es) || !(eb > 0x1p-100f) || !(es < 0x1p100f))) {
+    // huge rows): binary64 re-check of every enabled format.  Each binary32 sum carries a
+    // relative error below (n + 9) 2^-24 for the n <= 160 roundings of a lane's serial sum
+    // (128 elements at most, MX chunks one more per 4) and the 9 of the reductions, so two
+    // sums more than 2^-15 apart are in the order of their exact values.
+    if (second >= 0 && (!(es - eb > 0x1p-15f * es) || !(eb > 0x1p-100f) || !(es < 0x1p100f))) {
 #pragma unroll
         for (int f = 0; f < CHAM_W_NFMT; ++f) {
             if (!(mask & (1u << f))) continue;
