@@ -138,8 +138,8 @@ typedef struct cham_wq {
 /* Search the formats of W [N][K] (device, binary32, finite) and fill *wq's buffers.
  * Ownership: the caller owns W and every buffer in *wq.  Errors: CHAM_EINVAL (NULL W/wq/
  * required buffer, N < 1), CHAM_EFORMAT (mask), CHAM_ESHAPE (K not a multiple of 32, or of
- * 64 with NF4 enabled or a packed layout requested, or K > 8192: a row is held in the
- * registers of one workgroup), CHAM_EHIP. */
+ * 64 with NF4 enabled, a packed layout requested or K > 8192; K > 32768: a row is held in
+ * the registers of one workgroup), CHAM_EHIP. */
 int cham_select_weight_formats(const float* W, cham_wq* wq, void* stream);
 
 /* Bytes of the packed GEMM layout of an N x K weight (see cham_wq.packed). */
@@ -356,6 +356,27 @@ int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, 
  * decode is not built: CHAM_EFORMAT).  ws: CHAM_OP_LINEAR bytes. */
 int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, float* Y, void* ws, size_t ws_bytes,
                               void* stream);
+
+/* The UNet path's 3x3 convolution (stride 1, zero padding 1) on quantized activations, as
+ * an implicit GEMM on the same kernels: the layers downstream of a shortcut concatenation
+ * (up-block resnet conv1) whose inputs Sec. 4.6 routes to MXFP8 whatever the LUT's gates
+ * say (cham_build_act_lut's is_shortcut).  xq: the activation codes of B images of H x W
+ * pixels with C channels, channels last (xq->M = B H W rows, xq->K = C, C % 64 == 0; its
+ * samples are 1 or B images).  wq: the weights as a linear layer [Co][9 C] with
+ * k = (ky * 3 + kx) * C + c (searched like any linear weight).  Y [B H W][Co] (device,
+ * binary32): Y[b,y,x][o] = sum over ky, kx, c of x^[b, y+ky-1, x+kx-1, c] w^[o, k],
+ * out-of-image pixels zero.  A pre-pass writes the zero-padded activation in half
+ * precision (MX formats relative to the tensor's largest block exponent: exact for blocks
+ * within 2^28 of it; INT8-asym q - z rounded once when beyond 2^11) that the GEMM gathers
+ * per output pixel and tap; accuracy as cham_mixed_linear.  ws: cham_conv3x3_workspace_bytes.
+ * Errors: CHAM_EINVAL (sizes, pointers, samples), CHAM_EFORMAT, CHAM_ESHAPE (C % 64, the
+ * padded copy beyond 2^31 bytes), CHAM_EWORKSPACE, CHAM_EHIP. */
+int cham_conv3x3_mixed(const cham_aq* xq, int32_t B, int32_t H, int32_t W, const cham_wq* wq, float* Y,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes of cham_conv3x3_mixed for B images of H x W x C and Co output channels
+ * (0 for sizes out of range). */
+size_t cham_conv3x3_workspace_bytes(int64_t B, int64_t H, int64_t W, int64_t C, int64_t Co);
 
 /* The launch plan cham_mixed_linear takes for M x N x K with 4- or 8-bit weight codes
  * (diagnostics; host only, launches nothing).  out (host, out_len >= 10 int32) receives

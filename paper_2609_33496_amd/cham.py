@@ -105,6 +105,9 @@ def lib():
     L.cham_quantize_act_noalloc.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P]
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_mixed_linear_grouped.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_GWQ), _P, _P, sz, _P]
+    L.cham_conv3x3_mixed.argtypes = [ctypes.POINTER(_AQ), i32, i32, i32, ctypes.POINTER(_WQ), _P, _P, sz, _P]
+    L.cham_conv3x3_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    L.cham_conv3x3_workspace_bytes.restype = sz
     L.cham_select_group_formats.argtypes = [_P, _P, ctypes.POINTER(_GWQ), _P, sz, _P]
     L.cham_act_colsq_accumulate.argtypes = [_P, i64, i64, _P, _P, sz, _P]
     L.cham_workspace_bytes.argtypes = [i32, i64, i64, i64]
@@ -115,7 +118,7 @@ def lib():
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_quantize_act_noalloc",
-                 "cham_mixed_linear", "cham_mixed_linear_grouped", "cham_select_group_formats",
+                 "cham_mixed_linear", "cham_mixed_linear_grouped", "cham_select_group_formats", "cham_conv3x3_mixed",
                  "cham_act_colsq_accumulate",
                  "cham_linear_plan"):
         getattr(L, name).restype = ctypes.c_int
@@ -550,3 +553,20 @@ def mixed_linear(xq: AQ, wq: WQ, Y: Optional[torch.Tensor] = None, ws=None, stre
     _check(lib().cham_mixed_linear(ctypes.byref(a), ctypes.byref(w), _ptr(Y), _ptr(ws), nb, _stream(stream)),
            "mixed_linear")
     return Y
+
+
+def conv3x3_mixed(xq: AQ, B: int, H: int, W: int, wq: WQ, Y: Optional[torch.Tensor] = None, ws=None,
+                  stream=None) -> torch.Tensor:
+    """3x3 convolution (stride 1, zero padding 1) of channels-last activation codes xq
+    (M = B H W rows, K = C) with weights wq [Co][9 C]; returns Y [B H W, Co]."""
+    if Y is None:
+        Y = torch.empty((xq.M, wq.N), dtype=torch.float32, device=xq.codes.device)
+    _dev_tensor(Y, torch.float32, "Y")
+    if ws is None:
+        nb = int(lib().cham_conv3x3_workspace_bytes(B, H, W, xq.K, wq.N))
+        ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=Y.device)
+    a, w = xq.struct(), wq.struct()
+    _check(lib().cham_conv3x3_mixed(ctypes.byref(a), B, H, W, ctypes.byref(w), _ptr(Y), _ptr(ws), ws.numel(),
+                                    _stream(stream)), "conv3x3_mixed")
+    return Y
+

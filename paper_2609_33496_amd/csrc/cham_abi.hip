@@ -12,7 +12,7 @@ extern "C" const char* cham_status_string(int status) {
     switch (status) {
     case CHAM_OK: return "ok";
     case CHAM_EINVAL: return "invalid argument (NULL pointer, size or index out of range, misaligned buffer)";
-    case CHAM_ESHAPE: return "unsupported shape (K must be a multiple of 32; of 64 when NF4 is enabled and for mixed_linear; at most 8192 for the weight search)";
+    case CHAM_ESHAPE: return "unsupported shape (K must be a multiple of 32; of 64 when NF4 is enabled and for mixed_linear; for the weight search at most 32768, beyond 8192 a multiple of 64; at most 8192 for the group search)";
     case CHAM_EFORMAT: return "unknown format id or bad palette mask";
     case CHAM_EHIP: return "HIP launch or runtime error";
     case CHAM_EWORKSPACE: return "workspace missing or too small";

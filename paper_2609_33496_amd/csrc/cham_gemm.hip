@@ -48,10 +48,6 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float float16v __attribute__((ext_vector_type(16)));
 
-#ifndef CHAM_GEMM_SCHED
-#define CHAM_GEMM_SCHED 0
-#endif
-
 constexpr int BK = 64;
 constexpr int kThreads = 256;
 // TN = 32-channel MFMA blocks per wavefront: a tile is 128 TN channels wide (four wavefronts)
@@ -113,6 +109,91 @@ __global__ __launch_bounds__(256) void prep_kernel(PrepArgs p) {
         *reinterpret_cast<half8*>(out + 8 * g) = h;
     }
     if (threadIdx.x == 0) p.rowscale[m] = ldexpf(1.0f, eref);
+}
+
+// ------------------------------------------------------------------------------------
+// pre-pass of the 3x3 convolution: the activation codes -> a zero-padded half-precision
+// copy [B][H+2][W+2][C] (the border is the padding) that the GEMM gathers per output pixel
+// and tap.  MX formats relative to the tensor's largest block exponent (every output row
+// gathers nine pixels, so they need one reference), per-tensor formats as code values
+// (E4M3, E5M2 exact) or q - z (INT8-asym) with the sample's scale as the row scale.
+// ------------------------------------------------------------------------------------
+struct PrepConvArgs {
+    const uint8_t* xc;
+    const uint8_t* xe8;
+    int afmt;
+    int B, H, W, C;
+    int perm4;
+    const float* xs;  // per-sample scale / zero point (per-tensor formats)
+    const float* xz;
+    int rps;          // rows (pixels) per sample
+    int* emax;        // MX: the largest biased block exponent of the tensor (device)
+    _Float16* Xh;
+    float* rowscale;  // [B*H*W]
+};
+
+// One workgroup: the largest E8M0 byte of n (a plain maximum, so the order is free).
+__global__ __launch_bounds__(1024) void emax_kernel(const uint8_t* e8, int64_t n, int* out) {
+    int m = 0;
+    for (int64_t i = threadIdx.x; i < n; i += 1024) m = max(m, (int)e8[i]);
+    for (int o = 32; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, kWave));
+    __shared__ int wm[16];
+    if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < 16; ++i) m = max(m, wm[i]);
+        *out = max(m, wm[0]);
+    }
+}
+
+// One workgroup per padded pixel.
+__global__ __launch_bounds__(256) void prep_conv_kernel(PrepConvArgs p) {
+    const int C = p.C, Wp = p.W + 2, Hp = p.H + 2;
+    const int pp = blockIdx.x, xp = pp % Wp, yb = pp / Wp, yp = yb % Hp, b = yb / Hp;
+    _Float16* out = p.Xh + (int64_t)pp * C;
+    const bool border = xp == 0 || yp == 0 || xp == Wp - 1 || yp == Hp - 1;
+    if (border) {
+        for (int g = threadIdx.x; g < C / 8; g += blockDim.x) *reinterpret_cast<uint4*>(out + 8 * g) = make_uint4(0u, 0u, 0u, 0u);
+        return;
+    }
+    const int64_t m = ((int64_t)b * p.H + (yp - 1)) * p.W + (xp - 1);  // source = output row
+    const bool mx = p.afmt == CHAM_A_MXFP8_E4M3 || p.afmt == CHAM_A_MXINT8;
+    const float z = mx ? 0.0f : p.xz[m / p.rps];
+    // MX: the tensor's reference exponent; INT8-asym: the power of two that keeps q - z
+    // within half precision's range
+    const float zm = fabsf(z) + 255.0f;
+    const int eref = mx ? *p.emax - 127 - 14
+                        : (p.afmt == CHAM_A_INT8_ASYM && zm >= 32768.0f ? floor_log2(zm) - 14 : 0);
+    const uint8_t* row = p.xc + m * C;
+    for (int g = threadIdx.x; g < C / 8; g += blockDim.x) {
+        const uint2 c2 = *reinterpret_cast<const uint2*>(row + 8 * g);
+        const int kb = mx ? (int)p.xe8[m * (C / 32) + (g >> 2)] - 127 : 0;
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const uint32_t c = ((j < 4 ? c2.x : c2.y) >> (8 * (j & 3))) & 0xFFu;
+            switch (p.afmt) {
+            case CHAM_A_MXFP8_E4M3: v[j] = ldexpf(e4m3_decode(c), kb - eref); break;
+            case CHAM_A_MXINT8: v[j] = ldexpf((float)(int8_t)c, kb - 6 - eref); break;
+            case CHAM_A_FP8_E4M3: v[j] = e4m3_decode(c); break;
+            case CHAM_A_FP8_E5M2: v[j] = e5m2_decode(c); break;
+            default: v[j] = ldexpf((float)c - z, -eref); break;  // INT8-asym
+            }
+        }
+        half8 h;
+        if (p.perm4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[2 * j] = (_Float16)v[j];
+                h[2 * j + 1] = (_Float16)v[j + 4];
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) h[j] = (_Float16)v[j];
+        }
+        *reinterpret_cast<half8*>(out + 8 * g) = h;
+    }
+    if (threadIdx.x == 0) p.rowscale[m] = mx ? ldexpf(1.0f, eref) : ldexpf(p.xs[m / p.rps], eref);
 }
 
 // ------------------------------------------------------------------------------------
@@ -448,11 +529,16 @@ struct GemmArgs {
     int splits;      // k-splits: workgroup b takes tile b % tiles and k-steps of split b / tiles
     int kchunk;      // k-steps per split
     float* part;     // splits > 1: [splits][M][N] partial outputs, summed by reduce_kernel
+    // 3x3 convolution (implicit GEMM): Xh is the zero-padded activation [B][H+2][W+2][C] in
+    // half precision; row m = (b, y, x) of the output, k = (ky * 3 + kx) * C + c
+    int H, W, C;
+    uint32_t xh_bytes;
 };
 
-// Activation operand source: the half-precision copy of the pre-pass (MX formats), or the
-// per-tensor codes, decoded while they are staged into LDS.
-constexpr int kAF16 = 0, kAInt8 = 1, kAE4M3 = 2, kAE5M2 = 3;
+// Activation operand source: the half-precision copy of the pre-pass (MX formats), the
+// per-tensor codes, decoded while they are staged into LDS, or (3x3 convolution) the
+// pre-pass's zero-padded half-precision copy, gathered per output pixel and tap.
+constexpr int kAF16 = 0, kAInt8 = 1, kAE4M3 = 2, kAE5M2 = 3, kAConv = 4;
 
 // 8 activation codes (k0..k3 in w0, k4..k7 in w1) -> 8 halves, in the order
 // (0,4,1,5,2,6,3,7) when perm4, else natural; exact for all three per-tensor formats.
@@ -490,7 +576,8 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     constexpr int BN = tile_width(TN);
     constexpr int CW = CODE_BITS / 4;  // 16-byte code pieces per record
     constexpr int P = CW + 2;          // 16-byte pieces per record (codes + two table planes)
-    constexpr int AQ = AF == kAF16 ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
+    constexpr bool HALF = AF == kAF16 || AF == kAConv;   // the operand comes in half precision
+    constexpr int AQ = HALF ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
     constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
     __shared__ uint4 lds[2][A_CH];
     __shared__ __align__(16) float Rs[BM];
@@ -515,7 +602,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     // (split 0 only).
     if (t < BM) {
         const int m = t < rows ? m0 + t : m0;
-        if (AF == kAF16) {
+        if (HALF) {
             Rs[t] = a.rowscale[m];
         } else {
             Rs[t] = a.xs[m / a.rps];
@@ -526,7 +613,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
         }
     }
     // the staging rows of this thread (row q >> 2 of load q = 256 i + t): their -(1024 + z1)
-    constexpr int AQ0 = AF == kAF16 ? 1 : (TM + 1) / 2;
+    constexpr int AQ0 = HALF ? 1 : (TM + 1) / 2;
     half2v negz[AQ0];
 #pragma unroll
     for (int i = 0; i < AQ0; ++i) {
@@ -547,21 +634,46 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     //  codes: load q is row q >> 2, codes 16 (q & 3) .. + 15 = chunks 2 (q & 3), + 1.
     const bool perm4 = CODE_BITS == 4;
     const __amdgpu_buffer_rsrc_t ra =
-        AF == kAF16 ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.Xh + (int64_t)m0 * K + kb * BK), (short)0,
-                                                        (rows * K - kb * BK) * 2, kBufferFlags)
-                    : __builtin_amdgcn_make_buffer_rsrc((void*)(a.xc + (int64_t)m0 * K + kb * BK), (short)0,
-                                                        rows * K - kb * BK, kBufferFlags);
-    const uint32_t aoff0 = AF == kAF16 ? (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4))
-                                       : (uint32_t)((t >> 2) * K + ((t & 3) << 4));
+        AF == kAConv ? __builtin_amdgcn_make_buffer_rsrc((void*)a.Xh, (short)0, (int)a.xh_bytes, kBufferFlags)
+        : AF == kAF16 ? __builtin_amdgcn_make_buffer_rsrc((void*)(a.Xh + (int64_t)m0 * K + kb * BK), (short)0,
+                                                          (rows * K - kb * BK) * 2, kBufferFlags)
+                      : __builtin_amdgcn_make_buffer_rsrc((void*)(a.xc + (int64_t)m0 * K + kb * BK), (short)0,
+                                                          rows * K - kb * BK, kBufferFlags);
+    const uint32_t aoff0 = HALF ? (uint32_t)((t >> 3) * K * 2 + (((t & 7) ^ ((t >> 4) & 7)) << 4))
+                                : (uint32_t)((t >> 2) * K + ((t & 3) << 4));
+    // convolution: the padded pixel of each staging row (row (t >> 3) + 32 i) at tap (0, 0);
+    // rows past the tile's last take an offset past the buffer (loads return zeros)
+    int pix[AF == kAConv ? AQ : 1];
+#pragma unroll
+    for (int i = 0; i < (AF == kAConv ? AQ : 1); ++i) {
+        pix[i] = -1;
+        if (AF == kAConv) {
+            const int r = (t >> 3) + 32 * i;
+            if (r < rows) {
+                const int m = m0 + r, x = m % a.W, yb = m / a.W, y = yb % a.H, b = yb / a.H;
+                pix[i] = (b * (a.H + 2) + y) * (a.W + 2) + x;
+            }
+        }
+    }
     struct AStage {
         uint4 v[AQ];
     };
     auto load_a = [&](AStage& S, int k) __attribute__((always_inline)) {
+        int tapoff = 0, ci0 = 0;
+        if (AF == kAConv) {  // k-step -> tap (ky, kx) and channel offset (C % 64 == 0)
+            const int kk = (kb + k) * BK, tap = kk / a.C;
+            ci0 = kk - tap * a.C;
+            tapoff = (tap / 3) * (a.W + 2) + tap % 3;
+        }
 #pragma unroll
         for (int i = 0; i < AQ; ++i) {
-            const uint32_t off = AF == kAF16 ? aoff0 + (uint32_t)(i * 64 * K + k * BK * 2)
-                                             : aoff0 + (uint32_t)(i * 64 * K + k * BK);
-            S.v[i] = (AF != kAF16 && i * 256 + t >= BM * 4)
+            uint32_t off;
+            if (AF == kAConv)
+                off = pix[i] < 0 ? 0x7FFFFFF0u
+                                 : (uint32_t)(((pix[i] + tapoff) * a.C + ci0) * 2) + (aoff0 - (uint32_t)((t >> 3) * K * 2));
+            else
+                off = HALF ? aoff0 + (uint32_t)(i * 64 * K + k * BK * 2) : aoff0 + (uint32_t)(i * 64 * K + k * BK);
+            S.v[i] = (!HALF && i * 256 + t >= BM * 4)
                          ? make_uint4(0u, 0u, 0u, 0u)
                          : __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)off, 0, 0));
         }
@@ -569,7 +681,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     auto store_a = [&](const AStage& S, int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < AQ; ++i) {
-            if (AF == kAF16) {
+            if (HALF) {
                 lds[buf][i * 256 + t] = S.v[i];
             } else {
                 const int q = i * 256 + t;
@@ -689,19 +801,6 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
             for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf[j], acc[i][j], 0, 0, 0);
     };
-    // the decode of the next sub-step's weights spread between this sub-step's MFMAs, so the
-    // VALU work issues while the matrix cores run
-    auto interleave = [&]() __attribute__((always_inline)) {
-#if CHAM_GEMM_SCHED == 1
-        constexpr int NM = TM * TN;
-        constexpr int VPM = (24 * TN * (CODE_BITS / 4) + NM - 1) / NM + 1;
-#pragma unroll
-        for (int m = 0; m < NM; ++m) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
-        }
-#endif
-    };
     auto step = [&](int k, int buf, const WStage& Wc, const WStage& Wn, WStage& Wl, AStage& Ra)
                     __attribute__((always_inline)) {
         if (k + 1 < nsteps) store_a(Ra, buf ^ 1);
@@ -716,7 +815,6 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
 #pragma unroll
             for (int j = 0; j < TN; ++j) bn[j] = decode(Wc.r[j], j, s + 1);
             mfmas();
-            interleave();
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < TM; ++i) af[i] = an[i];
@@ -731,7 +829,6 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
 #pragma unroll
         for (int j = 0; j < TN; ++j) bn[j] = decode(Wn.r[j], j, 0);
         mfmas();
-        interleave();
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < TM; ++i) af[i] = an[i];
@@ -890,9 +987,6 @@ int col_tiles(int N, int tn) { return (N + tile_width(tn) - 1) / tile_width(tn);
 Plan plan_gemm(int M, int N, int K, int code_bits) {
     const int P = cu_count();
     const int nsteps = K / BK;
-#ifdef CHAM_FORCE_BM
-    if (code_bits == 4) return Plan{1, 1, {Launch{0, M, CHAM_FORCE_BM, 2}, Launch{0, 0, 0, 0}}};
-#endif
     TileCost costs[kNumTiles];
     for (int b = 0; b < kNumTiles; ++b) costs[b] = kTileCosts[b];
     if (code_bits != 4) {  // the full-width 128-high tile with 8-bit codes: one per CU
@@ -963,6 +1057,7 @@ void launch_gemm(GemmArgs a, const Launch& l, int af, hipStream_t s) {
     case kAInt8: launch_gemm_af<CODE_BITS, kAInt8>(a, l, s); break;
     case kAE4M3: launch_gemm_af<CODE_BITS, kAE4M3>(a, l, s); break;
     case kAE5M2: launch_gemm_af<CODE_BITS, kAE5M2>(a, l, s); break;
+    case kAConv: launch_gemm_af<CODE_BITS, kAConv>(a, l, s); break;
     default: launch_gemm_af<CODE_BITS, kAF16>(a, l, s); break;
     }
 }
@@ -1118,13 +1213,34 @@ extern "C" int cham_linear_plan(int64_t M, int64_t N, int64_t K, int32_t code_bi
     return CHAM_OK;
 }
 
-static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* ws, size_t ws_bytes, void* stream) {
+// 3x3 convolution geometry (images B x H x W, channels last)
+struct ConvSpec {
+    int B, H, W;
+};
+
+// Workspace of the convolution: the padded half-precision copy, the row scales, the block
+// exponent maximum, the weights' layout (no packed layout given) and the k-split partials.
+static size_t conv_workspace(int64_t B, int64_t H, int64_t W, int64_t C, int64_t Co) {
+    const int64_t M = B * H * W;
+    return align256((size_t)(B * (H + 2) * (W + 2) * C) * 2) + align256((size_t)M * 4) + 256 +
+           align256(cham_packed_bytes(Co, 9 * C)) + split_bytes(M, Co, 9 * C);
+}
+
+static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* ws, size_t ws_bytes, void* stream,
+                             const ConvSpec* cv = nullptr) {
     const WView* wq = &v;
     if (!xq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
     if (!wq->fmt || !wq->codes) return CHAM_EINVAL;
     if (!wq->gsel && (!wq->scale || !wq->zero)) return CHAM_EINVAL;
     if (wq->gsel && (!wq->gscale || !wq->gzero)) return CHAM_EINVAL;
-    if (xq->M < 1 || wq->N < 1 || xq->K < 1 || xq->K != wq->K) return CHAM_EINVAL;
+    if (xq->M < 1 || wq->N < 1 || xq->K < 1 || (cv ? 9 * xq->K : xq->K) != wq->K) return CHAM_EINVAL;
+    if (cv) {
+        if (cv->B < 1 || cv->H < 1 || cv->W < 1 || (int64_t)cv->B * cv->H * cv->W != xq->M) return CHAM_EINVAL;
+        if (xq->K % 64 != 0) return CHAM_ESHAPE;  // a k-step never straddles two taps
+        const int64_t xb = (int64_t)cv->B * (cv->H + 2) * (cv->W + 2) * xq->K * 2;
+        if (xb > (int64_t)INT32_MAX - 4096) return CHAM_ESHAPE;  // 32-bit buffer offsets
+        if (xq->nsamples != 1 && xq->nsamples != cv->B) return CHAM_EINVAL;  // a sample is whole images
+    }
     if (xq->fmt < 0 || xq->fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
     if (xq->nsamples < 1 || xq->M % xq->nsamples != 0) return CHAM_EINVAL;
     const uint32_t mask = wq->mask;
@@ -1132,11 +1248,11 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     const int code_bits = (mask & 0x7u) ? 8 : 4;
     if (wq->code_bits != code_bits) return CHAM_EFORMAT;
     if (wq->gsel && code_bits != 4) return CHAM_EFORMAT;  // the 8-bit group-scaled decode is not built
-    if (xq->K % 64 != 0) return CHAM_ESHAPE;
+    if (wq->K % 64 != 0) return CHAM_ESHAPE;
     // 32-bit buffer offsets: a 256-row activation tile and the weight records stay below
     // 2^31 bytes
-    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || xq->K > (1 << 20) ||
-        record_bytes(wq->N, xq->K) > (int64_t)INT32_MAX)
+    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || wq->K > (1 << 20) ||
+        record_bytes(wq->N, wq->K) > (int64_t)INT32_MAX)
         return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;
     const bool wmx = (mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) != 0u;
@@ -1145,10 +1261,11 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     if (amx && !xq->e8m0) return CHAM_EINVAL;
     if (((uintptr_t)xq->codes & 15u) || ((uintptr_t)wq->codes & 15u) || ((uintptr_t)wq->packed & 255u))
         return CHAM_EINVAL;
-    const size_t need = cham_linear_workspace_bytes(xq->M, wq->N, xq->K);
+    const size_t need = cv ? conv_workspace(cv->B, cv->H, cv->W, xq->K, wq->N)
+                           : cham_linear_workspace_bytes(xq->M, wq->N, xq->K);
     if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return CHAM_EWORKSPACE;
     hipStream_t s = (hipStream_t)stream;
-    const int M = (int)xq->M, N = (int)wq->N, K = (int)xq->K;
+    const int M = (int)xq->M, N = (int)wq->N, K = (int)wq->K;
     const Plan plan = plan_gemm(M, N, K, code_bits);
     const int kchunk = (K / BK + plan.splits - 1) / plan.splits;
     // every split holds at least one k-step (the operand ranges of the kernel rely on it)
@@ -1156,15 +1273,27 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
 
     char* w = (char*)ws;
     _Float16* Xh = (_Float16*)w;
-    w += align256((size_t)M * (size_t)K * 2);
+    const size_t xh_bytes = cv ? (size_t)cv->B * (cv->H + 2) * (cv->W + 2) * xq->K * 2 : (size_t)M * (size_t)K * 2;
+    w += align256(xh_bytes);
     float* rowscale = (float*)w;
     w += align256((size_t)M * 4);
+    int* emax = (int*)w;
+    if (cv) w += 256;
     // the search's packed layout replaces the pre-pass
     const Layout lay = layout_at(wq->packed ? wq->packed : (void*)w, N, K);
     w += align256(cham_packed_bytes(N, K));
     float* part = (float*)w;
 
-    if (amx) {
+    if (cv) {
+        if (amx) {
+            hipLaunchKernelGGL(emax_kernel, dim3(1), dim3(1024), 0, s, xq->e8m0, xq->M * (xq->K / 32), emax);
+            CHAM_CHECK_LAUNCH();
+        }
+        PrepConvArgs p{xq->codes, xq->e8m0, xq->fmt, cv->B, cv->H, cv->W, (int)xq->K, code_bits == 4, xq->scale,
+                       xq->zero, (int)(xq->M / xq->nsamples), emax, Xh, rowscale};
+        hipLaunchKernelGGL(prep_conv_kernel, dim3((unsigned)(cv->B * (cv->H + 2) * (cv->W + 2))), dim3(256), 0, s, p);
+        CHAM_CHECK_LAUNCH();
+    } else if (amx) {
         PrepArgs p{xq->codes, xq->e8m0, xq->fmt, M, K, code_bits == 4, Xh, rowscale};
         hipLaunchKernelGGL(prep_kernel, dim3((unsigned)M), dim3(256), 0, s, p);
         CHAM_CHECK_LAUNCH();
@@ -1194,7 +1323,12 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     a.row0 = 0;
     a.row1 = M;
     a.part = part;
-    const int af = amx ? kAF16
+    a.H = cv ? cv->H : 0;
+    a.W = cv ? cv->W : 0;
+    a.C = cv ? (int)xq->K : 0;
+    a.xh_bytes = (uint32_t)xh_bytes;
+    const int af = cv ? kAConv
+                 : amx ? kAF16
                        : (xq->fmt == CHAM_A_INT8_ASYM ? kAInt8 : (xq->fmt == CHAM_A_FP8_E4M3 ? kAE4M3 : kAE5M2));
     a.splits = plan.splits;
     a.kchunk = kchunk;
@@ -1224,3 +1358,16 @@ extern "C" int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, 
     if (!gq || !gq->choice) return CHAM_EINVAL;
     return mixed_linear_impl(xq, view_of(gq), Y, ws, ws_bytes, stream);
 }
+
+extern "C" int cham_conv3x3_mixed(const cham_aq* xq, int32_t B, int32_t H, int32_t W, const cham_wq* wq, float* Y,
+                                  void* ws, size_t ws_bytes, void* stream) {
+    if (!wq) return CHAM_EINVAL;
+    const ConvSpec cv{B, H, W};
+    return mixed_linear_impl(xq, view_of(wq), Y, ws, ws_bytes, stream, &cv);
+}
+
+extern "C" size_t cham_conv3x3_workspace_bytes(int64_t B, int64_t H, int64_t W, int64_t C, int64_t Co) {
+    if (B < 1 || H < 1 || W < 1 || C < 64 || Co < 1) return 0;
+    return conv_workspace(B, H, W, C, Co);
+}
+

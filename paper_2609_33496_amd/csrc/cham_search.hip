@@ -373,9 +373,13 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     const int wv = threadIdx.x >> 6;
     const int K = a.K;
     const int SPLIT = a.split;
-    const int KP = K / SPLIT;  // elements of this wavefront
-    const int nq = KP >> 2;    // float4 of this wavefront
-    const float* row = a.W + n * (int64_t)K + (int64_t)part * KP;
+    // elements [sp, sp + lp) of the row: split rows are cut at 64-element block boundaries
+    // (K % 64 == 0), the quarters within one block of each other
+    const int nblk = K / 64;
+    const int sp = SPLIT > 1 ? (part * nblk / SPLIT) * 64 : 0;
+    const int lp = SPLIT > 1 ? ((part + 1) * nblk / SPLIT) * 64 - sp : K;
+    const int nq = lp >> 2;  // float4 of this wavefront
+    const float* row = a.W + n * (int64_t)K + sp;
     const uint32_t mask = MASK ? MASK : a.mask;
 
     float v[NCH][4];
@@ -555,7 +559,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         if (!valid[c]) continue;
-        const int q = c * 64 + lane + part * (KP >> 2);  // float4 index in the row
+        const int q = c * 64 + lane + (sp >> 2);  // float4 index in the row
         const uint32_t cw = cws[c];
         if (a.code_bits == 4) {
             reinterpret_cast<uint16_t*>(a.codes + n * (int64_t)(K / 2))[q] = (uint16_t)cw;
@@ -632,11 +636,14 @@ struct Variant {
     int split, nch;
 };
 Variant variant_of(int64_t N, int64_t K) {
-    // split when the quarter rows fill their 256-element chunks to at least 85 %
+    // split when the quarter rows fill their 256-element chunks to at least 85 %, and
+    // always for rows longer than one wavefront holds (8192)
     const int64_t qc = K / 4;
     const bool fill = K % 256 == 0 && qc * 100 >= 85 * ((qc + 255) / 256 * 256);
-    const int split = (fill && K >= 1024 && N < kSplitBelowChannels) ? 4 : 1;
-    const int nch = (int)((K / split + 255) / 256);
+    const int split = K > 8192 || (fill && K >= 1024 && N < kSplitBelowChannels) ? 4 : 1;
+    // the longest quarter: ceil(blocks / 4) 64-element blocks
+    const int64_t kp = split == 1 ? K : (K / 64 + 3) / 4 * 64;
+    const int nch = (int)((kp + 255) / 256);
     static const int counts[] = {2, 3, 5, 8, 10, 20, 32};
     int r = 32;
     for (int c : counts)
@@ -681,7 +688,9 @@ static int prepare_layer(const float* W, cham_wq* wq, SearchArgs& a) {
     if (!wq->fmt || !wq->codes || !wq->scale || !wq->zero) return CHAM_EINVAL;
     if ((nf4 && !wq->nf4_absmax) || (mx && !wq->e8m0)) return CHAM_EINVAL;
     if (((uintptr_t)W & 15u) || ((uintptr_t)wq->codes & 3u)) return CHAM_EINVAL;
-    if (K > 32 * 256) return CHAM_ESHAPE;  // rows up to 8192 are held in registers
+    // rows up to 8192 are held in one wavefront's registers, up to 32768 in four (cut at
+    // 64-element blocks)
+    if (K > 4 * 32 * 256 || (K > 32 * 256 && K % 64 != 0)) return CHAM_ESHAPE;
     if (wq->packed) {  // the packed GEMM layout: 64-wide k-steps, 32-bit record offsets
         if (K % 64 != 0) return CHAM_ESHAPE;
         if (((uintptr_t)wq->packed & 255u) || wq->N * (K / 64) * 128 > (int64_t)INT32_MAX) return CHAM_EINVAL;

@@ -595,3 +595,13 @@ def test_two_streams_match_one_stream():
     assert np.array_equal(_np(ref[1].nS), _np(two[1].nS))
     for ya, yb in zip(ref[3], two[3]):
         assert np.array_equal(_np(ya).view(np.uint32), _np(yb).view(np.uint32))
+
+
+@pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8])
+@pytest.mark.parametrize("N,K", [(12, 17280), (6, 23040), (5, 32768), (3, 8256)])
+def test_search_long_rows(mask, N, K):
+    """Rows longer than one wavefront holds (3x3 conv weights, K = 9 C_in): split over the
+    four wavefronts of a workgroup at 64-element block boundaries (unequal quarters)."""
+    W, _ = synth.hetero_weights(N + K, N, K)
+    wq, ref = _search_both(W, mask)
+    _assert_search_equal(wq, ref)
