@@ -56,6 +56,9 @@ def parse():
     p.add_argument("--cpu-budget-s", type=float, default=12.0, help="seconds of oracle work per baseline run")
     p.add_argument("--no-extras", action="store_true",
                    help="skip the C3 search, the single-step stack and the dense f16 comparison")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="first run one device-to-device copy of this many MiB (the known-size "
+                        "kernel that scales the profiler's HBM byte counters; 0: none)")
     p.add_argument("--layer-steps", type=int, default=2,
                    help="untimed steps after the timed ones for the per-layer GEMM breakdown (0: none)")
     return p.parse_args()
@@ -115,6 +118,12 @@ def main():
     side = torch.cuda.Stream(device=dev)  # the weight search of each step (default priority)
     S_side = ctypes.c_void_p(side.cuda_stream)
     P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    if args.calib_copy_mib > 0:
+        src = torch.ones(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     layers = synth.sdxl_stack_layers()
     nl = len(layers)

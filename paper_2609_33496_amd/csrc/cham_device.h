@@ -102,37 +102,9 @@ CHAM_DEV float e2m1_decode(uint32_t c) {
 }
 
 // ------------------------------------------------------------------------------------
-// FP8 E4M3 (OCP "FN", bias 7, max 448) and E5M2 (bias 15, max 57344): round to nearest
-// even with subnormals, sign of zero kept.  Input already clamped to the format's range.
+// FP8 E4M3 (OCP "FN", bias 7, max 448) and E5M2 (bias 15, max 57344) decoding, subnormals
+// and the sign of zero included.
 // ------------------------------------------------------------------------------------
-CHAM_DEV uint32_t e4m3_encode(float y) {
-    uint32_t sgn = (__float_as_uint(y) >> 24) & 0x80u;
-    float a = fabsf(y);
-    uint32_t code;
-    if (a < 0.015625f) {  // below 2^-6: subnormal step 2^-9 (8 -> min normal, code 8)
-        code = (uint32_t)rne(a * 512.0f);
-    } else {
-        uint32_t u = __float_as_uint(a);
-        u += 0x7FFFFu + ((u >> 20) & 1u);
-        code = ((((u >> 23) - 127u + 7u)) << 3) | ((u >> 20) & 7u);
-    }
-    return sgn | code;
-}
-
-CHAM_DEV uint32_t e5m2_encode(float y) {
-    uint32_t sgn = (__float_as_uint(y) >> 24) & 0x80u;
-    float a = fabsf(y);
-    uint32_t code;
-    if (a < 6.103515625e-05f) {  // below 2^-14: subnormal step 2^-16
-        code = (uint32_t)rne(a * 65536.0f);
-    } else {
-        uint32_t u = __float_as_uint(a);
-        u += 0xFFFFFu + ((u >> 21) & 1u);
-        code = ((((u >> 23) - 127u + 15u)) << 2) | ((u >> 21) & 3u);
-    }
-    return sgn | code;
-}
-
 CHAM_DEV float e4m3_decode(uint32_t c) {
     uint32_t e = (c >> 3) & 15u, m = c & 7u;
     float v = e == 0u ? (float)m * 0.001953125f : ldexpf((float)(8u + m), (int)e - 10);

@@ -375,6 +375,28 @@ def test_fp8_conversion_on_every_tie_and_boundary():
         _check_aq(aq, xs, fmt, 1.0, 0.0, dynamic=False)
 
 
+def test_mxfp8_conversion_on_every_tie():
+    """MXFP8: every E4M3 midpoint (and its neighbours) times the block scale 2^E, in
+    32-element blocks whose largest element fixes E, for several E (subnormal, clamped)."""
+    vals = sorted(set(oracle.mf_decode(oracle.MF_E4M3, c) for c in range(0x7F)))
+    xs = []
+    for a_, b_ in zip(vals[:-1], vals[1:]):
+        m = np.float32((a_ + b_) / 2)
+        xs += [m, np.nextafter(m, np.float32(0)), np.nextafter(m, np.float32(1e30))]
+    xs = np.array(xs + [-x for x in xs], np.float32)
+    xs = np.concatenate([xs, np.zeros((-xs.size) % 31, np.float32)]).reshape(-1, 31)
+    rows = []
+    for E in (-20, -3, 0, 7, 40):
+        blk = np.concatenate([np.full((xs.shape[0], 1), 256.0, np.float32), xs], axis=1) * np.float32(2.0 ** E)
+        rows.append(blk.reshape(-1))
+    X = np.concatenate(rows)
+    X = np.concatenate([X, np.zeros((-X.size) % 256, np.float32)]).reshape(-1, 256)
+    case(f"quantize_act MXFP8 ties M={X.shape[0]}")
+    aq = cham.quantize_act(torch.from_numpy(X).to(DEV), cham.A_MXFP8, dynamic=True)
+    torch.cuda.synchronize()
+    _check_aq(aq, X, cham.A_MXFP8)
+
+
 @pytest.mark.parametrize("dynamic", [False, True])
 def test_quantize_act_lut_lookup(dynamic):
     """Alg. runtime (static: the bucket's calibrated S, Z) and Alg. runtime_dit (dynamic:
