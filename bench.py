@@ -310,6 +310,7 @@ def main():
     if not args.no_extras:
         print("bench: single-step stack, PixArt-like search, dense comparison", file=sys.stderr, flush=True)
         out["single_step_stack"] = single_step_stack(cham, L, layers, Ms, Xs, wqs, stream, S)
+        out["compact_weights"] = compact_weights(cham, L, layers, Ms, wqs, aq_s, Ys, ws_lin, stream, S, ms_gemm)
         out["pixart_search"] = pixart_search(cham, synth, stream, dev)
         out["dense_f16_reference"] = dense_reference(layers, Ms, stream)
     del Ys
@@ -331,6 +332,36 @@ def time_calls(fn, stream, reps=3):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / reps
+
+
+def compact_weights(cham, L, layers, Ms, wqs, aq_s, Ys, ws_lin, stream, S, ms_gemm_packed):
+    """The step's 280 GEMMs on weights held only as the search's codes and metadata (no
+    packed layout: each call derives the decode layout in its workspace first), beside the
+    resident bytes per weight of that form and of the packed layout."""
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    lean = []
+    for w in wqs:
+        st = w.struct()  # a fresh descriptor: the packed layout dropped from it only
+        st.packed = None
+        lean.append(st)
+
+    def run():
+        for li in range(len(layers)):
+            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(lean[li]), P(Ys[li]), P(ws_lin),
+                                     ws_lin.numel(), S)
+            assert rc == 0, rc
+
+    ms = time_calls(run, stream)
+    nw = sum(N * K for (_, K, N, _) in layers)
+    nch = sum(N for (_, K, N, _) in layers)
+    compact = sum(N * K // 2 + N * (1 + 4 + 4) + 4 * (N * K // 64) + N * K // 32 for (_, K, N, _) in layers)
+    packed = sum(int(cham.lib().cham_packed_bytes(N, K)) for (_, K, N, _) in layers)
+    return {"gemm_ms": round(ms, 4), "gemm_ms_packed": round(ms_gemm_packed, 4),
+            "resident_bytes_per_weight": round(compact / nw, 4),
+            "packed_bytes_per_weight": round(packed / nw, 4), "channels": nch,
+            "what": "280 x mixed_linear with wq.packed = NULL (the record pre-pass runs in each call's workspace); "
+                    "resident = codes (4 bits) + NF4 absmax (4 B / 64) + E8M0 (1 B / 32) per weight + format, "
+                    "scale and zero point per channel"}
 
 
 def single_step_stack(cham, L, layers, Ms, Xs, wqs, stream, S):

@@ -342,20 +342,32 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  * across workgroups whose partial outputs a second kernel adds in split order; no atomics
  * are used, so Y is bitwise reproducible run to run.  If wq->packed is set it supplies the
  * weights' decode layout; otherwise a pre-pass derives it from the codes and metadata into
- * the workspace.  ws: CHAM_OP_LINEAR bytes (a half-precision copy of MX activations, per-row
- * scales, the weights' decode layout, the k-split partial outputs), 256-byte aligned.
+ * the workspace.  ws: what cham_mixed_linear_workspace_query reports for these operands
+ * (a half-precision copy of MX activations and their row scales, the weights' decode layout
+ * when wq->packed is NULL, the k-split partial outputs when the plan splits; possibly 0,
+ * then ws may be NULL), 256-byte aligned; CHAM_OP_LINEAR bytes always suffice.
  * Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE, CHAM_EWORKSPACE, CHAM_EHIP.
  * ------------------------------------------------------------------------------------- */
 int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y, void* ws, size_t ws_bytes,
                       void* stream);
 
+/* Exact workspace bytes of cham_mixed_linear for these operands (host only: reads the
+ * descriptors, launches nothing, dereferences no device pointer) into *bytes (host).
+ * Errors: those of cham_mixed_linear's argument checks (CHAM_EINVAL, CHAM_EFORMAT,
+ * CHAM_ESHAPE), and CHAM_EINVAL for a NULL bytes. */
+int cham_mixed_linear_workspace_query(const cham_aq* xq, const cham_wq* wq, size_t* bytes);
+
 /* The same linear layer with group-scaled weights from cham_select_group_formats (the DiT
  * path, Sec. 4.6 (i)): each 32-element half of a 64-wide k-step lies in one group (every
  * group size is a multiple of 32), whose scale and zero point build its decode table;
  * accuracy as above.  4-bit palettes only (gq->code_bits == 4; the 8-bit group-scaled
- * decode is not built: CHAM_EFORMAT).  ws: CHAM_OP_LINEAR bytes. */
+ * decode is not built: CHAM_EFORMAT).  ws: as cham_mixed_linear (exact bytes from
+ * cham_mixed_linear_grouped_workspace_query; CHAM_OP_LINEAR bytes always suffice). */
 int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, float* Y, void* ws, size_t ws_bytes,
                               void* stream);
+
+/* Exact workspace bytes of cham_mixed_linear_grouped (as cham_mixed_linear_workspace_query). */
+int cham_mixed_linear_grouped_workspace_query(const cham_aq* xq, const cham_gwq* gq, size_t* bytes);
 
 /* The UNet path's 3x3 convolution (stride 1, zero padding 1) on quantized activations, as
  * an implicit GEMM on the same kernels: the layers downstream of a shortcut concatenation

@@ -105,6 +105,9 @@ def lib():
     L.cham_quantize_act_noalloc.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P]
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_mixed_linear_grouped.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_GWQ), _P, _P, sz, _P]
+    L.cham_mixed_linear_workspace_query.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), ctypes.POINTER(sz)]
+    L.cham_mixed_linear_grouped_workspace_query.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_GWQ),
+                                                            ctypes.POINTER(sz)]
     L.cham_conv3x3_mixed.argtypes = [ctypes.POINTER(_AQ), i32, i32, i32, ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_conv3x3_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
     L.cham_conv3x3_workspace_bytes.restype = sz
@@ -167,6 +170,27 @@ def linear_plan(M: int, N: int, K: int, code_bits: int) -> dict:
     launches = [{"rows": (out[2 + 4 * i], out[3 + 4 * i]), "tile": (out[4 + 4 * i], out[5 + 4 * i])}
                 for i in range(out[0])]
     return {"splits": out[1], "launches": launches}
+
+
+def _exact_workspace(ws, device, query, a, w):
+    """The caller's workspace, else one of the exact size the query reports for these
+    operands (None when it is 0)."""
+    if ws is not None:
+        return ws, ws.numel()
+    nb = ctypes.c_size_t(0)
+    _check(query(ctypes.byref(a), ctypes.byref(w), ctypes.byref(nb)), "workspace query")
+    if nb.value == 0:
+        return None, 0
+    return torch.empty(nb.value, dtype=torch.uint8, device=device), nb.value
+
+
+def linear_workspace_query(xq: "AQ", wq: "WQ") -> int:
+    """Exact workspace bytes mixed_linear needs for these operands (host only)."""
+    a, w = xq.struct(), wq.struct()
+    nb = ctypes.c_size_t(0)
+    _check(lib().cham_mixed_linear_workspace_query(ctypes.byref(a), ctypes.byref(w), ctypes.byref(nb)),
+           "cham_mixed_linear_workspace_query")
+    return nb.value
 
 
 def _workspace(op, M, N, K, device, ws):
@@ -534,8 +558,8 @@ def mixed_linear_grouped(xq: "AQ", gq: GWQ, Y: Optional[torch.Tensor] = None, ws
     if Y is None:
         Y = torch.empty((xq.M, gq.N), dtype=torch.float32, device=xq.codes.device)
     _dev_tensor(Y, torch.float32, "Y")
-    ws, nb = _workspace(OP_LINEAR, xq.M, gq.N, gq.K, Y.device, ws)
     a, g = xq.struct(), gq.struct()
+    ws, nb = _exact_workspace(ws, Y.device, lib().cham_mixed_linear_grouped_workspace_query, a, g)
     _check(lib().cham_mixed_linear_grouped(ctypes.byref(a), ctypes.byref(g), _ptr(Y), _ptr(ws), nb, _stream(stream)),
            "mixed_linear_grouped")
     return Y
@@ -548,8 +572,8 @@ def mixed_linear(xq: AQ, wq: WQ, Y: Optional[torch.Tensor] = None, ws=None, stre
     if Y is None:
         Y = torch.empty((xq.M, wq.N), dtype=torch.float32, device=xq.codes.device)
     _dev_tensor(Y, torch.float32, "Y")
-    ws, nb = _workspace(OP_LINEAR, xq.M, wq.N, wq.K, Y.device, ws)
     a, w = xq.struct(), wq.struct()
+    ws, nb = _exact_workspace(ws, Y.device, lib().cham_mixed_linear_workspace_query, a, w)
     _check(lib().cham_mixed_linear(ctypes.byref(a), ctypes.byref(w), _ptr(Y), _ptr(ws), nb, _stream(stream)),
            "mixed_linear")
     return Y

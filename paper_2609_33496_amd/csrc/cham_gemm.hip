@@ -1226,10 +1226,30 @@ static size_t conv_workspace(int64_t B, int64_t H, int64_t W, int64_t C, int64_t
            align256(cham_packed_bytes(Co, 9 * C)) + split_bytes(M, Co, 9 * C);
 }
 
+// What one call uses of its workspace, in this order: the half-precision activation copy
+// and row scales (MX activations and the convolution only), the block exponent maximum
+// (convolution), the weight layout (when no packed layout comes with the weight) and the
+// k-split partials (when the plan splits).
+struct WsLayout {
+    size_t xh, rs, emax, rec, part, total;
+};
+static WsLayout ws_layout(bool half_copy, size_t xh_bytes, bool conv, bool packed, int64_t M, int64_t N, int64_t K,
+                          int splits) {
+    WsLayout l;
+    l.xh = 0;
+    l.rs = l.xh + (half_copy ? align256(xh_bytes) : 0);
+    l.emax = l.rs + (half_copy ? align256((size_t)M * 4) : 0);
+    l.rec = l.emax + (conv ? 256 : 0);
+    l.part = l.rec + (packed ? 0 : align256(cham_packed_bytes(N, K)));
+    l.total = l.part + (splits > 1 ? (size_t)splits * (size_t)M * (size_t)N * 4 : 0);
+    return l;
+}
+
+// ws_need != NULL: only report the workspace bytes these operands need (Y and ws unused).
 static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* ws, size_t ws_bytes, void* stream,
-                             const ConvSpec* cv = nullptr) {
+                             const ConvSpec* cv = nullptr, size_t* ws_need = nullptr) {
     const WView* wq = &v;
-    if (!xq || !Y || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
+    if (!xq || (!Y && !ws_need) || !xq->codes || !xq->scale || !xq->zero) return CHAM_EINVAL;
     if (!wq->fmt || !wq->codes) return CHAM_EINVAL;
     if (!wq->gsel && (!wq->scale || !wq->zero)) return CHAM_EINVAL;
     if (wq->gsel && (!wq->gscale || !wq->gzero)) return CHAM_EINVAL;
@@ -1261,28 +1281,27 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     if (amx && !xq->e8m0) return CHAM_EINVAL;
     if (((uintptr_t)xq->codes & 15u) || ((uintptr_t)wq->codes & 15u) || ((uintptr_t)wq->packed & 255u))
         return CHAM_EINVAL;
-    const size_t need = cv ? conv_workspace(cv->B, cv->H, cv->W, xq->K, wq->N)
-                           : cham_linear_workspace_bytes(xq->M, wq->N, xq->K);
-    if (!ws || ws_bytes < need || ((uintptr_t)ws & 255u)) return CHAM_EWORKSPACE;
-    hipStream_t s = (hipStream_t)stream;
     const int M = (int)xq->M, N = (int)wq->N, K = (int)wq->K;
     const Plan plan = plan_gemm(M, N, K, code_bits);
     const int kchunk = (K / BK + plan.splits - 1) / plan.splits;
     // every split holds at least one k-step (the operand ranges of the kernel rely on it)
     if (plan.splits < 1 || (plan.splits - 1) * kchunk >= K / BK) return CHAM_ESHAPE;
+    const size_t xh_bytes = cv ? (size_t)cv->B * (cv->H + 2) * (cv->W + 2) * xq->K * 2 : (size_t)M * (size_t)K * 2;
+    const WsLayout wl = ws_layout(amx || cv, xh_bytes, cv != nullptr, wq->packed != nullptr, M, N, K, plan.splits);
+    if (ws_need) {  // the size query: nothing is checked against a buffer, nothing launched
+        *ws_need = wl.total;
+        return CHAM_OK;
+    }
+    if (wl.total > 0 && (!ws || ws_bytes < wl.total || ((uintptr_t)ws & 255u))) return CHAM_EWORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
 
     char* w = (char*)ws;
-    _Float16* Xh = (_Float16*)w;
-    const size_t xh_bytes = cv ? (size_t)cv->B * (cv->H + 2) * (cv->W + 2) * xq->K * 2 : (size_t)M * (size_t)K * 2;
-    w += align256(xh_bytes);
-    float* rowscale = (float*)w;
-    w += align256((size_t)M * 4);
-    int* emax = (int*)w;
-    if (cv) w += 256;
+    _Float16* Xh = (_Float16*)(w + wl.xh);
+    float* rowscale = (float*)(w + wl.rs);
+    int* emax = (int*)(w + wl.emax);
     // the search's packed layout replaces the pre-pass
-    const Layout lay = layout_at(wq->packed ? wq->packed : (void*)w, N, K);
-    w += align256(cham_packed_bytes(N, K));
-    float* part = (float*)w;
+    const Layout lay = layout_at(wq->packed ? wq->packed : (void*)(w + wl.rec), N, K);
+    float* part = (float*)(w + wl.part);
 
     if (cv) {
         if (amx) {
@@ -1351,6 +1370,16 @@ extern "C" int cham_mixed_linear(const cham_aq* xq, const cham_wq* wq, float* Y,
                                  void* stream) {
     if (!wq) return CHAM_EINVAL;
     return mixed_linear_impl(xq, view_of(wq), Y, ws, ws_bytes, stream);
+}
+
+extern "C" int cham_mixed_linear_workspace_query(const cham_aq* xq, const cham_wq* wq, size_t* bytes) {
+    if (!wq || !bytes) return CHAM_EINVAL;
+    return mixed_linear_impl(xq, view_of(wq), nullptr, nullptr, 0, nullptr, nullptr, bytes);
+}
+
+extern "C" int cham_mixed_linear_grouped_workspace_query(const cham_aq* xq, const cham_gwq* gq, size_t* bytes) {
+    if (!gq || !gq->choice || !bytes) return CHAM_EINVAL;
+    return mixed_linear_impl(xq, view_of(gq), nullptr, nullptr, 0, nullptr, nullptr, bytes);
 }
 
 extern "C" int cham_mixed_linear_grouped(const cham_aq* xq, const cham_gwq* gq, float* Y, void* ws, size_t ws_bytes,

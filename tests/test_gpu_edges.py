@@ -251,3 +251,40 @@ def test_rcp_rn_equals_ieee_quotient_everywhere():
         torch.cuda.synchronize()
         ref = np.float32(1.0) / a
         assert np.array_equal(_np(rd).view(np.uint32), ref.view(np.uint32)), e
+
+
+@pytest.mark.parametrize("afmt,packed,M,N,K", [(cham.A_FP8_E5M2, True, 2048, 3840, 1280),
+                                                (cham.A_MXFP8, False, 2048, 1280, 5120),
+                                                (cham.A_INT8_ASYM, False, 300, 200, 640)])
+def test_linear_exact_workspace(afmt, packed, M, N, K):
+    """The workspace query names exactly what the call uses: the half-precision copy and
+    row scales only for MX activations, the weight layout only without a packed layout, the
+    partials only when the plan splits K; one byte less is refused before any launch, and
+    the output equals the one computed with the CHAM_OP_LINEAR upper bound."""
+    W = synth.hetero_weights_dev(77, N, K, DEV)
+    X = synth.diffusion_acts_dev(0, 3, 379, M, K, DEV)
+    case(f"exact workspace afmt={afmt} packed={packed} M={M} N={N} K={K}")
+    wq = cham.select_weight_formats(W, cham.MASK_W4, want_packed=packed)
+    xq = cham.quantize_act(X, afmt, dynamic=True)
+    need = cham.linear_workspace_query(xq, wq)
+    plan = cham.linear_plan(M, N, K, 4)
+    exp = 0
+    if afmt in (cham.A_MXFP8, cham.A_MXINT8):
+        exp += -(-M * K * 2 // 256) * 256 + -(-M * 4 // 256) * 256
+    if not packed:
+        exp += -(-int(cham.lib().cham_packed_bytes(N, K)) // 256) * 256
+    if plan["splits"] > 1:
+        exp += plan["splits"] * M * N * 4
+    assert need == exp, (need, exp, plan)
+    assert need <= cham.workspace_bytes(cham.OP_LINEAR, M, N, K)
+    full = torch.empty(cham.workspace_bytes(cham.OP_LINEAR, M, N, K), dtype=torch.uint8, device=DEV)
+    Y_full = cham.mixed_linear(xq, wq, ws=full)
+    Y_exact = cham.mixed_linear(xq, wq, ws=torch.empty(max(need, 1), dtype=torch.uint8, device=DEV)[:need]
+                                if need else None)
+    torch.cuda.synchronize()
+    assert torch.equal(Y_full, Y_exact)
+    if need:
+        short = torch.empty(need, dtype=torch.uint8, device=DEV)[: need - 1]
+        with pytest.raises(cham.ChamError) as ei:
+            cham.mixed_linear(xq, wq, ws=short)
+        assert ei.value.status == cham.EWORKSPACE
