@@ -36,6 +36,7 @@ struct SearchArgs {
     uint8_t* e8;
     double* err;
     int split;  // wavefronts per channel: 1, or 4 (a quarter of the row each)
+    int lpc;    // 16 or 32: lanes per channel of the several-channels-per-wavefront kernel; 0: not used
 };
 
 // per-channel parameters of the per-channel formats
@@ -576,6 +577,322 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
     }
 }
 
+// ------------------------------------------------------------------------------------
+// Rows of at most 2560 elements in layers with many channels: LPC (16 or 32) lanes per
+// channel, so a wavefront searches 64 / LPC channels at once, and each lane holds 8
+// consecutive elements per chunk (an MX block is 4 lanes, an NF4 block 8).  The per-row
+// work (reductions, scales, the choice, the metadata) is shared by 4 or 2 channels and
+// the per-block work (block maxima, MX exponents, the NF4 reciprocal) by 8 elements.
+// Every reduction stays inside the channel's aligned lane group, so channels may branch
+// apart; the binary64 re-check re-reads its row from memory (it is rare).
+// ------------------------------------------------------------------------------------
+template <int LPC>
+CHAM_DEV float grp_sum(float v) {
+    v = row_sum16(v);  // every lane of the row ends with the same sum (each step adds a pair)
+    if (LPC >= 32) v += __shfl_xor(v, 16, kWave);
+    return v;
+}
+template <int LPC>
+CHAM_DEV float grp_min(float v) {
+    v = fminf(v, dpp<0xB1>(v));
+    v = fminf(v, dpp<0x4E>(v));
+    v = fminf(v, dpp<0x141>(v));
+    v = fminf(v, dpp<0x140>(v));
+    if (LPC >= 32) v = fminf(v, __shfl_xor(v, 16, kWave));
+    return v;
+}
+template <int LPC>
+CHAM_DEV float grp_max(float v) {
+    v = max16_from8(max8(v));
+    if (LPC >= 32) v = fmaxf(v, __shfl_xor(v, 16, kWave));
+    return v;
+}
+template <int LPC>
+CHAM_DEV double grp_sumd(double v) {
+#pragma unroll
+    for (int o = LPC / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+// binary32 squared error of 8 consecutive elements in format F (as chunk_err)
+template <int F>
+CHAM_DEV float oct_err(const float (&w)[8], const RowParams& p, float blk64, const NF4Cell* cells, int e0, int e2) {
+    const float lo[4] = {w[0], w[1], w[2], w[3]};
+    const float hi[4] = {w[4], w[5], w[6], w[7]};
+    if (F == CHAM_W_MXINT4 || F == CHAM_W_MXINT8) {  // one rescale for the 8 elements
+        const int Fb = F == CHAM_W_MXINT8 ? 6 : 2;
+        const float Q = F == CHAM_W_MXINT8 ? 127.0f : 7.0f;
+        float es = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float y = ldexpf(w[j], Fb - e0);
+            const float d = y - __builtin_amdgcn_fmed3f(rne(y), -Q, Q);
+            es = __builtin_fmaf(d, d, es);
+        }
+        return ldexpf(es, 2 * (e0 - Fb));
+    }
+    // the other formats' per-element work is that of chunk_err, on two quads
+    return chunk_err<F>(lo, p, 0.0f, blk64, cells, e0, e2) + chunk_err<F>(hi, p, 0.0f, blk64, cells, e0, e2);
+}
+
+// NF4 error of 8 consecutive elements and their codes (4 bits each, or a byte each in
+// cw[0..1] with 8-bit codes)
+CHAM_DEV float oct_err_nf4(const float (&w)[8], float blk64, const NF4Cell* cells, int code_bits, uint32_t (&cw)[2]) {
+    const float a = floor_scale(blk64);
+    const float r = rcp_rn(a);
+    float e = 0.0f;
+    cw[0] = cw[1] = 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float y = w[j] * r;
+        const NF4Cell cl = nf4_cell(cells, y);
+        const bool up = y > cl.thr;
+        const float d = w[j] - (up ? cl.vhi : cl.vlo) * a;
+        e = __builtin_fmaf(d, d, e);
+        const uint32_t c = cl.cnt + (up ? 1u : 0u);
+        if (code_bits == 4) cw[0] |= c << (4 * j);
+        else cw[j >> 2] |= c << (8 * (j & 3));
+    }
+    return e;
+}
+
+// codes of 8 consecutive elements in the winning format F (layout as oct_err_nf4)
+template <int F>
+CHAM_DEV void oct_codes(const float (&w)[8], const RowParams& p, float b32, float b64, const NF4Cell* cells,
+                        int code_bits, uint32_t (&cw)[2]) {
+    cw[0] = cw[1] = 0u;
+    if (F == CHAM_W_MXFP4 || F == CHAM_W_FP4) {
+        // hardware converter: byte k holds elements 2k (low nibble) and 2k + 1
+        const float sc = F == CHAM_W_MXFP4 ? e8m0_scale(mx_exponent(b32, 2)) : 1.0f;
+        const float m = F == CHAM_W_MXFP4 ? 1.0f : p.r_fp4;
+        uint32_t c = 0u;
+        c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, w[0] * m, w[1] * m, sc, 0);
+        c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, w[2] * m, w[3] * m, sc, 1);
+        c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, w[4] * m, w[5] * m, sc, 2);
+        c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, w[6] * m, w[7] * m, sc, 3);
+        if (code_bits == 4) {
+            cw[0] = c;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) cw[j >> 2] |= ((c >> (4 * j)) & 15u) << (8 * (j & 3));
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float wh;
+            const uint32_t code = quant_one<F>(w[j], p, b32, b64, cells, &wh);
+            if (code_bits == 4) cw[0] |= (code & 15u) << (4 * j);
+            else cw[j >> 2] |= (code & 255u) << (8 * (j & 3));
+        }
+    }
+}
+
+// binary64 errors of every enabled format over the lane's elements, re-read from the row
+// (the rare near-tie path): per chunk the block maxima by the same lane exchanges, each
+// element through the exact quantize-dequantize, summed over the channel's lanes.
+template <int NCH, int LPC>
+CHAM_DEV void recheck_oct(const float* row, int K, int ll, uint32_t mask, const RowParams& p, const NF4Cell* cells,
+                          double (&ed)[CHAM_W_NFMT]) {
+    double acc[CHAM_W_NFMT];
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) acc[f] = 0.0;
+#pragma unroll 1
+    for (int c = 0; c < NCH; ++c) {
+        const int e0 = 8 * (ll + LPC * c);
+        const bool valid = e0 < K;
+        float w[8];
+        const float4 t0 = valid ? ld4(row + e0) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 t1 = valid ? ld4(row + e0 + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        w[0] = t0.x; w[1] = t0.y; w[2] = t0.z; w[3] = t0.w; w[4] = t1.x; w[5] = t1.y; w[6] = t1.z; w[7] = t1.w;
+        float m = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(w[j]));
+        m = fmaxf(m, dpp<0xB1>(m));
+        const float b32 = fmaxf(m, dpp<0x4E>(m));
+        const float b64 = fmaxf(b32, dpp<0x141>(b32));
+        if (!valid) continue;
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            if (!(mask & (1u << f))) continue;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                float wh;
+                switch (f) {
+                case 0: quant_one<0>(w[j], p, b32, b64, cells, &wh); break;
+                case 1: quant_one<1>(w[j], p, b32, b64, cells, &wh); break;
+                case 2: quant_one<2>(w[j], p, b32, b64, cells, &wh); break;
+                case 3: quant_one<3>(w[j], p, b32, b64, cells, &wh); break;
+                case 4: quant_one<4>(w[j], p, b32, b64, cells, &wh); break;
+                case 5: quant_one<5>(w[j], p, b32, b64, cells, &wh); break;
+                case 6: quant_one<6>(w[j], p, b32, b64, cells, &wh); break;
+                case 7: quant_one<7>(w[j], p, b32, b64, cells, &wh); break;
+                default: quant_one<8>(w[j], p, b32, b64, cells, &wh); break;
+                }
+                const double d = (double)(w[j] - wh);
+                acc[f] = fma(d, d, acc[f]);
+            }
+        }
+    }
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f)
+        if (mask & (1u << f)) ed[f] = grp_sumd<LPC>(acc[f]);
+}
+
+// Search of channel n by its LPC lanes (lane ll of the group); n < N for the whole group.
+template <uint32_t MASK, int NCH, int LPC>
+CHAM_DEV void search_oct(const SearchArgs& a, const NF4Cell* cells, int64_t n, int ll) {
+    const int K = a.K;
+    const float* row = a.W + n * (int64_t)K;
+    const uint32_t mask = MASK ? MASK : a.mask;
+    const int code_bits = MASK == CHAM_MASK_W4 ? 4 : (MASK == CHAM_MASK_W8 ? 8 : a.code_bits);
+
+    float v[NCH][8];
+    bool valid[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        const int e0 = 8 * (ll + LPC * c);
+        valid[c] = e0 < K;
+        const float4 t0 = valid[c] ? ld4(row + e0) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 t1 = valid[c] ? ld4(row + e0 + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[c][0] = t0.x; v[c][1] = t0.y; v[c][2] = t0.z; v[c][3] = t0.w;
+        v[c][4] = t1.x; v[c][5] = t1.y; v[c][6] = t1.z; v[c][7] = t1.w;
+    }
+
+    // ---- row and block statistics (invalid chunks are zeros: no effect on block maxima,
+    // and they stay out of lo / hi)
+    float lo = INFINITY, hi = -INFINITY;
+    float b32[NCH], b64[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        float m = 0.0f, l = INFINITY, h = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            m = fmaxf(m, fabsf(v[c][j]));
+            l = fminf(l, v[c][j]);
+            h = fmaxf(h, v[c][j]);
+        }
+        if (valid[c]) { lo = fminf(lo, l); hi = fmaxf(hi, h); }
+        m = fmaxf(m, dpp<0xB1>(m));
+        b32[c] = fmaxf(m, dpp<0x4E>(m));
+        b64[c] = fmaxf(b32[c], dpp<0x141>(b32[c]));
+    }
+    lo = grp_min<LPC>(lo);
+    hi = grp_max<LPC>(hi);
+    const float amax = fmaxf(fabsf(lo), fabsf(hi));
+
+    RowParams p;
+    p.s_sym8 = floor_scale(amax / 127.0f); p.r_sym8 = rcp_rn(p.s_sym8);
+    p.s_sym4 = floor_scale(amax / 7.0f);   p.r_sym4 = rcp_rn(p.s_sym4);
+    int_asym_scale_zp(lo, hi, 255.0f, &p.s_as8, &p.z_as8);
+    p.r_as8 = rcp_rn(p.s_as8);
+    int_asym_scale_zp(lo, hi, 15.0f, &p.s_as4, &p.z_as4);
+    p.r_as4 = rcp_rn(p.s_as4);
+    p.s_fp4 = floor_scale(amax / 6.0f); p.r_fp4 = rcp_rn(p.s_fp4);
+
+    // ---- binary32 error sums of every enabled format, one fused pass
+    float e[CHAM_W_NFMT];
+    uint32_t nf4cw[NCH][2];
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) e[f] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        nf4cw[c][0] = nf4cw[c][1] = 0u;
+        if (!valid[c]) continue;
+        const bool nz32 = b32[c] > 0.0f;
+        const int fl32 = __builtin_amdgcn_frexp_expf(b32[c]) - 1;
+        const int e0 = mx_exponent_fl(fl32, nz32, 0), e2 = mx_exponent_fl(fl32, nz32, 2);
+        if (mask & (1u << 0)) e[0] += oct_err<0>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 1)) e[1] += oct_err<1>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 2)) e[2] += oct_err<2>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 3)) e[3] += oct_err<3>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 4)) e[4] += oct_err<4>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 5)) e[5] += oct_err_nf4(v[c], b64[c], cells, code_bits, nf4cw[c]);
+        if (mask & (1u << 6)) e[6] += oct_err<6>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 7)) e[7] += oct_err<7>(v[c], p, b64[c], cells, e0, e2);
+        if (mask & (1u << 8)) e[8] += oct_err<8>(v[c], p, b64[c], cells, e0, e2);
+    }
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f)
+        if (mask & (1u << f)) e[f] = grp_sum<LPC>(e[f]);
+    int best = -1, second = -1;
+    float eb = 0.0f, es = 0.0f;
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) {
+        if (!(mask & (1u << f))) continue;
+        if (best < 0 || e[f] < eb) {
+            second = best; es = eb;
+            best = f; eb = e[f];
+        } else if (second < 0 || e[f] < es) {
+            second = f; es = e[f];
+        }
+    }
+    double ed[CHAM_W_NFMT];
+#pragma unroll
+    for (int f = 0; f < CHAM_W_NFMT; ++f) ed[f] = (double)e[f];
+    // the re-check rule of search_row (the same binary32 error bound: a lane's serial sum
+    // runs over at most 80 elements here, plus the reductions)
+    if (second >= 0 && (!(es - eb > 0x1p-15f * es) || !(eb > 0x1p-100f) || !(es < 0x1p100f))) {
+        recheck_oct<NCH, LPC>(row, K, ll, mask, p, cells, ed);
+        best = -1;
+        double bd = 0.0;
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) {
+            if (!(mask & (1u << f))) continue;
+            if (best < 0 || ed[f] < bd) { best = f; bd = ed[f]; }
+        }
+    }
+    if (a.err && ll == 0) {
+#pragma unroll
+        for (int f = 0; f < CHAM_W_NFMT; ++f) a.err[n * CHAM_W_NFMT + f] = (mask & (1u << f)) ? ed[f] : -1.0;
+    }
+
+    // ---- emit the winner's codes and metadata
+    const int f = best;
+    if (ll == 0) {
+        a.fmt[n] = (uint8_t)f;
+        float s = 0.0f, z = 0.0f;
+        if (f == CHAM_W_INT8_SYM) s = p.s_sym8;
+        else if (f == CHAM_W_INT4_SYM) s = p.s_sym4;
+        else if (f == CHAM_W_INT8_ASYM) { s = p.s_as8; z = p.z_as8; }
+        else if (f == CHAM_W_INT4_ASYM) { s = p.s_as4; z = p.z_as4; }
+        else if (f == CHAM_W_FP4) s = p.s_fp4;
+        a.scale[n] = s;
+        a.zero[n] = z;
+    }
+    const bool is_mx = f == CHAM_W_MXINT8 || f == CHAM_W_MXINT4 || f == CHAM_W_MXFP4;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if (!valid[c]) continue;
+        uint32_t cw[2];
+        switch (f) {
+        case 0: oct_codes<0>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 1: oct_codes<1>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 2: oct_codes<2>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 3: oct_codes<3>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 4: oct_codes<4>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 5: cw[0] = nf4cw[c][0]; cw[1] = nf4cw[c][1]; break;
+        case 6: oct_codes<6>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        case 7: oct_codes<7>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        default: oct_codes<8>(v[c], p, b32[c], b64[c], cells, code_bits, cw); break;
+        }
+        const int e0 = 8 * (ll + LPC * c);  // first element of the lane's 8
+        if (code_bits == 4) {
+            reinterpret_cast<uint32_t*>(a.codes + n * (int64_t)(K / 2))[e0 >> 3] = cw[0];
+        } else {
+            uint32_t* dst = reinterpret_cast<uint32_t*>(a.codes + n * (int64_t)K) + (e0 >> 2);
+            dst[0] = cw[0];
+            dst[1] = cw[1];
+        }
+        if (a.e8 && (ll & 3) == 0) {
+            const int E = f == CHAM_W_MXFP4 ? mx_exponent(b32[c], 2) : mx_exponent(b32[c], 0);
+            a.e8[n * (int64_t)(K / 32) + (e0 >> 5)] = is_mx ? (uint8_t)(E + 127) : (uint8_t)0;
+        }
+        if (a.nf4a && (ll & 7) == 0) {
+            a.nf4a[n * (int64_t)(K / 64) + (e0 >> 6)] = f == CHAM_W_NF4 ? floor_scale(b64[c]) : 0.0f;
+        }
+    }
+}
+
 constexpr int kGroupThreads = 1024;
 constexpr int kGroupLdsChannels = 16000;  // with the static arrays, within 64 KB of LDS
 
@@ -618,6 +935,29 @@ __global__ __launch_bounds__(256) void search_kernel(SearchBatch B) {
     if (n < a.N) search_row<MASK, NCH>(a, cells, n, a.split == 1 ? 0 : wv, &sl);  // workgroup-uniform for split 4
 }
 
+// LPC lanes per channel, 256 / LPC channels per workgroup.
+template <uint32_t MASK, int NCH, int LPC>
+__global__ __launch_bounds__(256) void search_oct_kernel(SearchBatch B) {
+    __shared__ NF4Cell cells[33];
+    nf4_cells_init(cells);
+    __syncthreads();
+    const int64_t b = blockIdx.x;
+    int i = 0;
+    while (i + 1 < B.nl && b >= B.wg_end[i]) ++i;
+    const SearchArgs& a = B.l[i];
+    const int64_t lb = b - (i ? B.wg_end[i - 1] : 0);
+    const int64_t n = lb * (256 / LPC) + (int)threadIdx.x / LPC;
+    if (n < a.N) search_oct<MASK, NCH, LPC>(a, cells, n, (int)threadIdx.x % LPC);  // uniform per lane group
+}
+
+template <int NCH, int LPC>
+void launch_oct(const SearchBatch& B, uint32_t mask, hipStream_t s) {
+    const dim3 grid((unsigned)B.wg_end[B.nl - 1]);
+    if (mask == CHAM_MASK_W4) hipLaunchKernelGGL((search_oct_kernel<CHAM_MASK_W4, NCH, LPC>), grid, dim3(256), 0, s, B);
+    else if (mask == CHAM_MASK_W8) hipLaunchKernelGGL((search_oct_kernel<CHAM_MASK_W8, NCH, LPC>), grid, dim3(256), 0, s, B);
+    else hipLaunchKernelGGL((search_oct_kernel<0u, NCH, LPC>), grid, dim3(256), 0, s, B);
+}
+
 template <int NCH>
 void launch_search(const SearchBatch& B, uint32_t mask, hipStream_t s) {
     const dim3 grid((unsigned)B.wg_end[B.nl - 1]);
@@ -633,9 +973,19 @@ constexpr int64_t kSplitBelowChannels = 4096;
 // Kernel variant of a layer: rows split over 4 wavefronts or not, and the register
 // chunks (256 elements) per wavefront, rounded up to an instantiated count.
 struct Variant {
-    int split, nch;
+    int split, nch, lpc;
 };
+// Rows up to 2560 elements in layers of at least this many channels take the
+// several-channels-per-wavefront kernel: 16 lanes per channel up to 640 elements, 32 up to
+// 2560 (8 elements per lane and chunk, at most 10 chunks; at most 5 up to 1280, which keeps
+// the kernel at four wavefronts per SIMD).
+constexpr int64_t kOctMinChannels = 1024;
 Variant variant_of(int64_t N, int64_t K) {
+    if (K <= 2560 && N >= kOctMinChannels) {
+        const int lpc = K <= 640 ? 16 : 32;
+        const int nch = (int)((K + 8 * lpc - 1) / (8 * lpc));
+        return Variant{1, nch <= 2 ? 2 : (nch <= 3 ? 3 : (nch <= 5 ? 5 : 10)), lpc};
+    }
     // split when the quarter rows fill their 256-element chunks to at least 85 %, and
     // always for rows longer than one wavefront holds (8192)
     const int64_t qc = K / 4;
@@ -648,11 +998,29 @@ Variant variant_of(int64_t N, int64_t K) {
     int r = 32;
     for (int c : counts)
         if (nch <= c) { r = c; break; }
-    return Variant{split, r};
+    return Variant{split, r, 0};
 }
 
-void launch_variant(int nch, const SearchBatch& B, uint32_t mask, hipStream_t s) {
-    switch (nch) {
+void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipStream_t s) {
+    if (v.lpc == 16) {
+        switch (v.nch) {
+        case 2: launch_oct<2, 16>(B, mask, s); break;
+        case 3: launch_oct<3, 16>(B, mask, s); break;
+        case 5: launch_oct<5, 16>(B, mask, s); break;
+        default: launch_oct<10, 16>(B, mask, s); break;
+        }
+        return;
+    }
+    if (v.lpc == 32) {
+        switch (v.nch) {
+        case 2: launch_oct<2, 32>(B, mask, s); break;
+        case 3: launch_oct<3, 32>(B, mask, s); break;
+        case 5: launch_oct<5, 32>(B, mask, s); break;
+        default: launch_oct<10, 32>(B, mask, s); break;
+        }
+        return;
+    }
+    switch (v.nch) {
     case 2: launch_search<2>(B, mask, s); break;
     case 3: launch_search<3>(B, mask, s); break;
     case 5: launch_search<5>(B, mask, s); break;
@@ -732,9 +1100,11 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
             if (done[j]) continue;
             const Variant vj = variant_of(args[j].N, args[j].K);
             const uint32_t kj = args[j].mask == CHAM_MASK_W4 || args[j].mask == CHAM_MASK_W8 ? args[j].mask : 0u;
-            if (vj.nch != v.nch || kj != key) continue;
+            if (vj.nch != v.nch || vj.lpc != v.lpc || kj != key) continue;
             args[j].split = vj.split;
-            wgs += vj.split == 1 ? (args[j].N + 3) / 4 : args[j].N;
+            args[j].lpc = vj.lpc;
+            const int64_t per_wg = vj.lpc ? 256 / vj.lpc : (vj.split == 1 ? 4 : 1);  // channels per workgroup
+            wgs += (args[j].N + per_wg - 1) / per_wg;
             B.l[B.nl] = args[j];
             B.wg_end[B.nl] = wgs;
             ++B.nl;
@@ -742,7 +1112,7 @@ extern "C" int cham_select_weight_formats_batch(const float* const* W, cham_wq* 
             if (B.nl == kBatchMax) break;
         }
         // a mixed palette (key 0) reads each layer's mask at run time
-        launch_variant(v.nch, B, key ? key : 0u, s);
+        launch_variant(v, B, key ? key : 0u, s);
         CHAM_CHECK_LAUNCH();
     }
     for (int i = 0; i < nlayers; ++i) wq[i].code_bits = args[i].code_bits;

@@ -76,9 +76,9 @@ def test_search_hetero_rows(mask, N, K):
     _assert_search_equal(wq, ref)
 
 
-@pytest.mark.parametrize("K", [256, 1024])  # 1024: each row split over four wavefronts
-def test_search_known_winners_and_degenerate_rows(K):
-    g = np.random.default_rng(0)
+def _special_rows(K, g):
+    """Rows with known winners (NF4 levels, INT4 grid, E2M1 grid with one block scale --
+    an exact FP4 / MXFP4 tie --, E2M1 with a scale per block) and degenerate rows."""
     rows = []
     v = oracle.nf4_table()
     r = v[g.integers(0, 16, K)]
@@ -101,10 +101,34 @@ def test_search_known_winners_and_degenerate_rows(K):
     rr = g.normal(size=K); rr[:128] = 0                        # half zero (all-zero blocks)
     rows.append(rr)
     rows.append(np.where(g.random(K) < 0.5, -0.0, 0.0))       # signed zeros
-    W = np.stack(rows).astype(np.float32)
+    return rows
+
+
+@pytest.mark.parametrize("K", [256, 1024])  # 1024: each row split over four wavefronts
+def test_search_known_winners_and_degenerate_rows(K):
+    W = np.stack(_special_rows(K, np.random.default_rng(0))).astype(np.float32)
     for mask in (oracle.MASK_W4, oracle.MASK_W8, 0x1FF):
         wq, ref = _search_both(W, mask)
         _assert_search_equal(wq, ref)
+
+
+@pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8, 0x1FF,
+                                  (1 << oracle.W_INT4_SYM) | (1 << oracle.W_FP4) | (1 << oracle.W_MXFP4)])
+@pytest.mark.parametrize("K", [64, 640, 1152, 2560])
+def test_search_several_channels_per_wavefront(mask, K):
+    """Layers of >= 1024 channels with rows up to 2560 elements: 2 or 4 channels per
+    wavefront, 8 consecutive elements per lane (ragged last chunk at K = 1152 and 64).  The
+    special rows (exact ties take the binary64 re-check) sit at every offset within a
+    wavefront's channel groups; the rest are heterogeneous rows."""
+    g = np.random.default_rng(K)
+    sp = _special_rows(K, g) if K >= 256 else []
+    H, _ = synth.hetero_weights(K + 5, 1031, K)
+    rows = list(H)
+    for i, r in enumerate(sp):  # row 3 i + (0, 1, 2): different lane groups and wavefronts
+        rows[3 * i + i % 3] = r
+    W = np.stack(rows).astype(np.float32)
+    wq, ref = _search_both(W, mask)
+    _assert_search_equal(wq, ref)
 
 
 def test_search_full_size_sampled():
