@@ -36,7 +36,7 @@ struct SearchArgs {
     uint8_t* e8;
     double* err;
     int split;  // wavefronts per channel: 1, or 4 (a quarter of the row each)
-    int lpc;    // 16 or 32: lanes per channel of the several-channels-per-wavefront kernel; 0: not used
+    int lpc;    // 16, 32 or 64: lanes per channel of the 8-elements-per-lane kernel; 0: not used
 };
 
 // per-channel parameters of the per-channel formats
@@ -578,7 +578,7 @@ CHAM_DEV void search_row(const SearchArgs& a, const NF4Cell* cells, int64_t n, i
 }
 
 // ------------------------------------------------------------------------------------
-// Rows of at most 2560 elements in layers with many channels: LPC (16 or 32) lanes per
+// Rows of at most 5120 elements in layers with many channels: LPC (16, 32 or 64) lanes per
 // channel, so a wavefront searches 64 / LPC channels at once, and each lane holds 8
 // consecutive elements per chunk (an MX block is 4 lanes, an NF4 block 8).  The per-row
 // work (reductions, scales, the choice, the metadata) is shared by 4 or 2 channels and
@@ -590,6 +590,7 @@ template <int LPC>
 CHAM_DEV float grp_sum(float v) {
     v = row_sum16(v);  // every lane of the row ends with the same sum (each step adds a pair)
     if (LPC >= 32) v += __shfl_xor(v, 16, kWave);
+    if (LPC >= 64) v += __shfl_xor(v, 32, kWave);
     return v;
 }
 template <int LPC>
@@ -599,12 +600,14 @@ CHAM_DEV float grp_min(float v) {
     v = fminf(v, dpp<0x141>(v));
     v = fminf(v, dpp<0x140>(v));
     if (LPC >= 32) v = fminf(v, __shfl_xor(v, 16, kWave));
+    if (LPC >= 64) v = fminf(v, __shfl_xor(v, 32, kWave));
     return v;
 }
 template <int LPC>
 CHAM_DEV float grp_max(float v) {
     v = max16_from8(max8(v));
     if (LPC >= 32) v = fmaxf(v, __shfl_xor(v, 16, kWave));
+    if (LPC >= 64) v = fmaxf(v, __shfl_xor(v, 32, kWave));
     return v;
 }
 template <int LPC>
@@ -975,13 +978,14 @@ constexpr int64_t kSplitBelowChannels = 4096;
 struct Variant {
     int split, nch, lpc;
 };
-// Rows up to 2560 elements in layers of at least this many channels take the
-// several-channels-per-wavefront kernel: 16 lanes per channel up to 640 elements, 32 up to
-// 2560 (8 elements per lane and chunk, at most 10 chunks; at most 5 up to 1280, which keeps
-// the kernel at four wavefronts per SIMD).
+// Rows up to 5120 elements in layers of at least this many channels (512 for rows longer
+// than 1280) take the 8-elements-per-lane kernel: 16 lanes per channel up to 640 elements,
+// 32 up to 2560 (two channels per wavefront), a whole wavefront up to 5120 (at most 10
+// chunks; at most 5 up to 1280, which keeps the kernel at four wavefronts per SIMD).
 constexpr int64_t kOctMinChannels = 1024;
 Variant variant_of(int64_t N, int64_t K) {
-    if (K <= 2560 && N >= kOctMinChannels) {
+    if (K > 2560 && K <= 5120 && N >= kOctMinChannels) return Variant{1, 10, 64};
+    if (K <= 2560 && N >= (K > 1280 ? kOctMinChannels / 2 : kOctMinChannels)) {
         const int lpc = K <= 640 ? 16 : 32;
         const int nch = (int)((K + 8 * lpc - 1) / (8 * lpc));
         return Variant{1, nch <= 2 ? 2 : (nch <= 3 ? 3 : (nch <= 5 ? 5 : 10)), lpc};
@@ -1009,6 +1013,10 @@ void launch_variant(const Variant& v, const SearchBatch& B, uint32_t mask, hipSt
         case 5: launch_oct<5, 16>(B, mask, s); break;
         default: launch_oct<10, 16>(B, mask, s); break;
         }
+        return;
+    }
+    if (v.lpc == 64) {
+        launch_oct<10, 64>(B, mask, s);
         return;
     }
     if (v.lpc == 32) {

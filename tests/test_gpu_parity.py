@@ -114,10 +114,10 @@ def test_search_known_winners_and_degenerate_rows(K):
 
 @pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8, 0x1FF,
                                   (1 << oracle.W_INT4_SYM) | (1 << oracle.W_FP4) | (1 << oracle.W_MXFP4)])
-@pytest.mark.parametrize("K", [64, 640, 1152, 2560])
+@pytest.mark.parametrize("K", [64, 640, 1152, 2560, 3200, 5120])
 def test_search_several_channels_per_wavefront(mask, K):
-    """Layers of >= 1024 channels with rows up to 2560 elements: 2 or 4 channels per
-    wavefront, 8 consecutive elements per lane (ragged last chunk at K = 1152 and 64).  The
+    """Layers of >= 1024 channels with rows up to 5120 elements: 4, 2 or 1 channels per
+    wavefront, 8 consecutive elements per lane (ragged last chunk at K = 1152, 3200 and 64).  The
     special rows (exact ties take the binary64 re-check) sit at every offset within a
     wavefront's channel groups; the rest are heterogeneous rows."""
     g = np.random.default_rng(K)
