@@ -19,8 +19,8 @@ Printed: one JSON line.  `value` = the step's GEMM flops / step time (everything
 step counts against it).  `roofline` is for the dominant kernel, the mixed-format GEMM: its
 280 calls timed with HIP events on the launch stream inside the timed steps; per layer kind
 (width x linear) from untimed steps with an event between calls.  Beside it: the weight
-search of the whole stack timed as its own call (no packing; §8(d) bytes), the packing pass
-by difference, the PixArt-like 28-block search at W4 and W8, the single-step (batch 1)
+search of the whole stack timed as its own call (no packing; the search's own algorithmic
+bytes), the packing pass by difference, the PixArt-like 28-block search at W4 and W8, the single-step (batch 1)
 stack's quantize + GEMM pass with one fixed A8 format per layer, and `cpu_baseline`: the CPU
 oracle on a bounded sample of the step, single-threaded and on all host cores.
 """
@@ -84,7 +84,7 @@ def committed_traffic():
 
 
 def search_bytes(N: int, K: int, bits: int = 4) -> float:
-    """Algorithmic bytes of the weight search of one layer (§8(d)): 4 B read per weight, the
+    """Algorithmic bytes of the weight search of one layer: 4 B read per weight, the
     codes (bits / 8 B), the chosen format's block metadata for every channel (NF4 absmax 4 B /
     64, E8M0 1 B / 32 at W4; E8M0 at W8) and 13 B per channel (format, scale, zero, perm)."""
     meta = (4.0 / 64 + 1.0 / 32) if bits == 4 else 1.0 / 32
@@ -290,7 +290,7 @@ def main():
         "search": {"ms": round(ms_search, 4), "GBps": round(search_gbps, 1),
                    "frac_hbm": round(search_gbps / HBM_PEAK_GBPS, 4), "bytes": int(sb), "weights": nweights,
                    "what": "select_weight_formats_batch over the 280 layers without packing, HIP events over 3 "
-                           "calls; bytes per §8(d): 4 B read + 0.5 B codes + block metadata per weight, 13 B per "
+                           "calls; algorithmic bytes: 4 B read + 0.5 B codes + block metadata per weight, 13 B per "
                            "channel"},
         "pack": {"ms": round(ms_search_pack - ms_search, 4),
                  "GBps": round(pb / max(ms_search_pack - ms_search, 1e-6) / 1e6, 1), "bytes": int(pb),
@@ -441,7 +441,7 @@ def pixart_search(cham, synth, stream, dev):
                     "format_hist": {cham.W_NAMES[i]: int(hist[i]) for i in range(9) if hist[i]}}
         del outs, sb
     res["weights"] = sum(N * K for (_, K, N) in blocks)
-    res["what"] = "28 blocks x 5 linears in one batched call per palette, HIP events over 3 calls, §8(d) bytes"
+    res["what"] = "28 blocks x 5 linears in one batched call per palette, HIP events over 3 calls, the search's algorithmic bytes"
     return res
 
 
