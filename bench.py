@@ -262,6 +262,43 @@ def main():
     search_gbps = sb / (ms_search * 1e-3) / 1e9
     del wq_np, nb_search
 
+    # ---- the activation side's parts, each timed alone on the launch stream: the batched
+    # moments over the 280 inputs (4 B read per element), the LUT build, and the 280
+    # quantize calls (4 B read + 1 B written per element, + 1/32 B of E8M0 for MX formats)
+    print("bench: activation side", file=sys.stderr, flush=True)
+    numel = sum(M * K for (_, K, _, _), M in zip(layers, Ms))
+
+    def stats_call():
+        rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, nl,
+                                               ctypes.byref(st_s), P(tbatch.ws), tbatch.ws_bytes, S)
+        assert rc == 0, rc
+
+    def lut_call():
+        rc = L.cham_build_act_lut(ctypes.byref(st_s), ctypes.byref(sc_s), None, ctypes.byref(lut_s), None, S)
+        assert rc == 0, rc
+
+    def quant_calls():
+        for li in range(nl):
+            rc = L.cham_quantize_act_lut(P(Xs[li]), ctypes.byref(lut_s), Fh, li, args.t, 0, ctypes.byref(aq_s[li]),
+                                         P(ws_q), ws_q.numel(), S)
+            assert rc == 0, rc
+
+    ms_stats = time_calls(stats_call, stream)
+    ms_lut = time_calls(lut_call, stream)
+    ms_quant = time_calls(quant_calls, stream)
+    qbytes = sum(M * K * (5.0 + (1.0 / 32 if int(lut.F_host[li * B_BUCKETS + bucket]) >= 3 else 0.0))
+                 for li, ((_, K, _, _), M) in enumerate(zip(layers, Ms)))
+    act_side = {
+        "stats": {"ms": round(ms_stats, 4), "GBps": round(4.0 * numel / (ms_stats * 1e-3) / 1e9, 1),
+                  "frac_hbm": round(4.0 * numel / (ms_stats * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                  "what": "act_stats_accumulate_batch over the 280 layer inputs (binary64 power sums), 4 B per element"},
+        "lut": {"ms": round(ms_lut, 4), "what": "build_act_lut, L = 280, B = 10"},
+        "quantize": {"ms": round(ms_quant, 4), "GBps": round(qbytes / (ms_quant * 1e-3) / 1e9, 1),
+                     "frac_hbm": round(qbytes / (ms_quant * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "what": "280 x quantize_act_lut (static LUT scales), 5 B per element (+1/32 for MX)"},
+        "elements": int(numel),
+    }
+
     fmts = [int(lut.F_host[li * B_BUCKETS + bucket]) for li in range(nl)]
     hist = np.bincount(torch.cat([w.fmt for w in wqs]).cpu().numpy(), minlength=9)
     afh = np.bincount(np.array(fmts), minlength=5)
@@ -296,6 +333,7 @@ def main():
                  "GBps": round(pb / max(ms_search_pack - ms_search, 1e-6) / 1e6, 1), "bytes": int(pb),
                  "what": "the same call writing each layer's packed GEMM layout, minus the search alone"},
         "search_in_step_ms": round(ms_search_step, 4),
+        "activation_side": act_side,
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4),
                      "traffic": committed_traffic(),
