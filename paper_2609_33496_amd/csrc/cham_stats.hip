@@ -17,7 +17,7 @@ namespace {
 
 constexpr int kStatsThreads = 256;
 constexpr int kStatsMaxBlocks = 1024;
-constexpr int kStatsLoads = 8;  // 16-byte loads in flight per thread
+constexpr int kStatsLoads = 16;  // 16-byte loads in flight per thread
 
 struct Partial {
     double s1, s2, s3, s4;
@@ -27,7 +27,7 @@ struct Partial {
 
 // Tensors of one accumulate call (several for the batched call): workgroups of tensor i are
 // [blk_end[i-1], blk_end[i]); partials are stored at the workgroup index.
-constexpr int kStatsBatchMax = 16;
+constexpr int kStatsBatchMax = 64;
 struct StatsBatch {
     int n;
     int blk_end[kStatsBatchMax];
@@ -281,7 +281,7 @@ extern "C" int cham_act_stats_reset(cham_act_stats* st, void* stream) {
 
 static int stats_blocks(int64_t numel) {
     int64_t nq = numel >> 2;
-    int64_t b = (nq + kStatsThreads * kStatsLoads - 1) / (kStatsThreads * kStatsLoads);  // >= 8 float4 per thread
+    int64_t b = (nq + kStatsThreads * kStatsLoads - 1) / (kStatsThreads * kStatsLoads);  // >= kStatsLoads float4 per thread
     if (b < 1) b = 1;
     if (b > kStatsMaxBlocks) b = kStatsMaxBlocks;
     return (int)b;
