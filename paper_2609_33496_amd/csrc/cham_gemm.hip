@@ -976,10 +976,13 @@ struct Plan {
     int splits;  // k-splits of a single launch (1: none)
     Launch l[2];
 };
-// k-split reduction: one extra launch reading the partials and writing the output
-// (measured ≈ 7 TB/s: the partials come back from the last-level cache in part)
+// k-split: the GEMM writes one binary32 partial output per split (≈ 5 TB/s, on top of its
+// k-steps), and one extra launch reads them back and writes the output (measured ≈ 7 TB/s:
+// the partials come back from the last-level cache in part)
 double reduce_cost(int64_t M, int64_t N, int splits) {
-    return splits > 1 ? 2.0 + (double)(splits + 1) * (double)(M * N * 4) / 7.0e6 : 0.0;
+    return splits > 1 ? 2.0 + (double)(splits + 1) * (double)(M * N * 4) / 7.0e6 +
+                            (double)splits * (double)(M * N * 4) / 5.0e6
+                      : 0.0;
 }
 
 int col_tiles(int N, int tn) { return (N + tile_width(tn) - 1) / tile_width(tn); }
