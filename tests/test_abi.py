@@ -155,3 +155,27 @@ def test_linear_plans_are_valid():
         cham.linear_plan(0, 64, 64, 4)
     with pytest.raises(cham.ChamError):
         cham.linear_plan(64, 64, 64, 6)
+
+
+def test_linear_workspace_query_on_the_host():
+    """The exact-workspace query checks the operands like mixed_linear, launches nothing and
+    reads no device memory: the decode layout without a packed one, nothing with it (FP8
+    activations, no split at these sizes), the half-precision copy and row scales for MX."""
+    L = cham.lib()
+    P = ctypes.c_void_p
+    nb = ctypes.c_size_t(12345)
+    aq = cham._AQ(4, 64, cham.A_FP8_E4M3, 1, P(16), P(16), P(16), P(16))
+    w = _wq(code_bits=4)
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aq), ctypes.byref(w), None) == cham.EINVAL
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aq), ctypes.byref(w), ctypes.byref(nb)) == cham.OK
+    rec = (int(L.cham_packed_bytes(4, 64)) + 255) // 256 * 256
+    assert nb.value == rec
+    wp = _wq(code_bits=4, packed=256)
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aq), ctypes.byref(wp), ctypes.byref(nb)) == cham.OK
+    assert nb.value == 0
+    aqm = cham._AQ(4, 64, cham.A_MXFP8, 1, P(16), P(16), P(16), P(16))
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aqm), ctypes.byref(wp), ctypes.byref(nb)) == cham.OK
+    assert nb.value == 512 + 256  # 4 x 64 halves (512 B) and 4 row scales, each rounded up to 256 bytes
+    assert nb.value <= cham.workspace_bytes(cham.OP_LINEAR, 4, 4, 64)
+    aqk = cham._AQ(4, 128, cham.A_FP8_E4M3, 1, P(16), P(16), P(16), P(16))  # K mismatch
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aqk), ctypes.byref(w), ctypes.byref(nb)) == cham.EINVAL
