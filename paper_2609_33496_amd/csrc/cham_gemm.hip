@@ -767,17 +767,20 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     // ---- main loop.  Step k computes from LDS buffer k & 1.  At its start it stores the
     // activation tile of step k + 1 (loaded DA steps earlier) into the other buffer and
     // issues the loads of step k + 1 + DA (activations) and k + DW (weights) into register
-    // rings of DA and DW + 1 stages; short steps (small tiles) take deeper rings so the
-    // loads have more than one memory latency to arrive.  Sub-steps 0-2 run with the
+    // rings of DA and DW + 1 stages.  Short steps (64-row tiles) take deeper rings so the
+    // loads have more than one memory latency to arrive, and so do half-width tiles, whose
+    // layers run one or two workgroups per CU with little else to hide that latency behind
+    // (there a 4-stage weight ring was 3-7 % faster than 2 stages).  Sub-steps 0-2 run with the
     // operand reads and weight decode one sub-step ahead; then one barrier makes the new
     // tile visible (and retires every read of this step's buffer), and the first operands
     // of step k + 1 are read and decoded behind the MFMAs of sub-step 3.  Step indices past
     // the end are clamped (harmless reloads); scheduling barriers keep the compiler from
     // sinking the reads next to their uses.  The loop is unrolled by a multiple of both
-    // ring lengths so every ring index is a constant.
-    constexpr int DW = TM == 2 ? 3 : 1;
+    // ring lengths and of the two LDS buffers, so every ring and buffer index is a constant.
+    constexpr int DW = TM == 2 || TN == 1 ? 3 : 1;
     constexpr int DA = TM == 2 ? 2 : 1;
-    constexpr int U = (DW + 1) > 2 ? (DW + 1) : 2;  // DA divides it
+    constexpr int U = (DW + 1) > 2 ? (DW + 1) : 2;
+    static_assert(U % DA == 0 && U % 2 == 0, "the unrolled steps must repeat every ring and buffer index");
     const int klast = nsteps - 1;
     AStage R[DA];
     WStage W[DW + 1];
