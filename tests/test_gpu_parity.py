@@ -651,3 +651,56 @@ def test_search_long_rows(mask, N, K):
     W, _ = synth.hetero_weights(N + K, N, K)
     wq, ref = _search_both(W, mask)
     _assert_search_equal(wq, ref)
+
+
+# ---------------------------------------------------------------------------------------
+# seeded random shapes and palettes
+@pytest.mark.parametrize("seed", range(16))
+def test_search_random_shapes(seed):
+    """A random non-empty palette, K (a multiple of 32, of 64 with NF4) and channel count
+    (below and above the several-channels-per-wavefront threshold): every output bit-exact."""
+    g = np.random.default_rng(1000 + seed)
+    mask = int(g.integers(1, 512))
+    step = 64 if (mask >> oracle.W_NF4) & 1 else 32
+    K = step * int(g.integers(1, 5120 // step + 1))
+    N = int(g.integers(1, 200)) if seed % 2 else int(g.integers(1024, 1600))
+    W, _ = synth.hetero_weights(2000 + seed, N, K)
+    wq, ref = _search_both(W, mask)
+    _assert_search_equal(wq, ref)
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_linear_random_shapes(seed):
+    """Random M, N, K, palette, activation format, sample count and weight layout (packed
+    by the search or derived per call): activation codes bit-exact, sampled outputs within
+    1e-3 * sum|x^ w^| of the oracle."""
+    g = np.random.default_rng(3000 + seed)
+    masks = [oracle.MASK_W4, oracle.MASK_W8, 0x1FF] + [1 << f for f in range(9)]
+    mask = int(masks[int(g.integers(0, len(masks)))])
+    K = 64 * int(g.integers(1, 41))
+    M, N = int(g.integers(1, 2500)), int(g.integers(1, 2500))
+    afmt = int(g.integers(0, 5))
+    ns = int(g.choice([d for d in (1, 2, 3, 4) if M % d == 0]))
+    packed = bool(g.integers(0, 2))
+    X = synth.diffusion_acts(seed, 3, int(g.integers(0, 1000)), M, K)
+    W, _ = synth.hetero_weights(4000 + seed, N, K)
+    case(f"mixed_linear random M={M} N={N} K={K} mask={mask:#x} afmt={afmt} nsamples={ns} packed={packed}")
+    wq = cham.select_weight_formats(torch.from_numpy(W).to(DEV), mask, want_packed=packed)
+    xq = cham.quantize_act(torch.from_numpy(X).to(DEV), afmt, dynamic=True, nsamples=ns)
+    Y = _np(cham.mixed_linear(xq, wq)).astype(np.float64)
+    if packed:  # the per-call pre-pass gives the kernels the same operands
+        wq.packed = None
+        assert np.array_equal(_np(cham.mixed_linear(xq, wq)).astype(np.float64), Y)
+    codes, e8, xh, s, z = oracle.quantize_act_per_sample(X, afmt, ns, want_xhat=True)
+    assert np.array_equal(_np(xq.codes), codes)
+    assert np.array_equal(_np(xq.scale).view(np.uint32), s.view(np.uint32))
+    mm = np.concatenate([g.integers(0, M, 1200), [M - 1, 0]])
+    nn = np.concatenate([g.integers(0, N, 1200), [N - 1, 0]])
+    rows = np.unique(nn)
+    ref = oracle.select_weight_formats(W[rows], mask, want_err=False, want_perm=False)
+    assert np.array_equal(_np(wq.fmt)[rows], ref["fmt"])
+    Wh = np.zeros((N, K), np.float32)
+    Wh[rows] = oracle.dequant_weights(ref, K)
+    yr, bm = oracle.linear_pairs(xh, Wh, mm, nn)
+    err = np.abs(Y[mm, nn] - yr)
+    assert np.all(err <= 1e-3 * bm), (err / np.maximum(bm, 1e-300)).max()
