@@ -337,7 +337,9 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
  * (NF4 and MX weights, MX activations) are held relative to the largest block of their
  * channel or row: blocks within 2^28 of it are exact (NF4: one rounding), blocks further
  * below fall into half precision's subnormal range and lose bits.  xq->K must equal wq->K and be a multiple of
- * 64; xq->codes, wq->codes and Y must be 16-byte aligned.  Y [M][N] is written in the
+ * 64; the kernels address operands with 32-bit offsets, so K <= 2^20, N < 2^21 and the
+ * weights' decode layout (cham_packed_bytes) stays below 2^31 bytes (CHAM_ESHAPE otherwise);
+ * xq->codes, wq->codes and Y must be 16-byte aligned.  Y [M][N] is written in the
  * original channel order.  When the output has too few tiles to fill the GPU, K is split
  * across workgroups whose partial outputs a second kernel adds in split order; no atomics
  * are used, so Y is bitwise reproducible run to run.  If wq->packed is set it supplies the

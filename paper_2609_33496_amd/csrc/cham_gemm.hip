@@ -53,6 +53,7 @@ constexpr int kThreads = 256;
 // TN = 32-channel MFMA blocks per wavefront: a tile is 128 TN channels wide (four wavefronts)
 constexpr int tile_width(int TN) { return 128 * TN; }
 constexpr int kBufferFlags = 0x00020000;  // buffer descriptor word 3: 32-bit data, raw
+constexpr int kStoreNonTemporal = 2;      // cache-policy operand of a buffer store: nt
 
 // ------------------------------------------------------------------------------------
 // pre-pass for MX activation formats: codes -> half precision relative to the row's
@@ -850,9 +851,17 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
             step(k + u, u & 1, W[u % (DW + 1)], W[(u + 1) % (DW + 1)], W[(u + DW) % (DW + 1)], R[(u + 1) % DA]);
 
     // ---- epilogue: 32x32 block, lane holds column l32, rows 8*(r/4) + 4*h + r%4; the
-    // lane's 16 row scales of block i are 4 aligned float4 in LDS
-    const bool full = rows == BM && n0 + BN <= N;
+    // lane's 16 row scales of block i are 4 aligned float4 in LDS.  Stores go through a
+    // buffer resource over the tile's rows of the output: the lane's offset is one VGPR per
+    // block, each row's offset a wave-uniform SGPR, and the range check drops the rows past
+    // the last of a ragged tile (the lane skips columns past the last).  The output is not
+    // read again here, so it is stored non-temporally (the L2 stays with the operand tiles
+    // other workgroups still read); k-split partials, which the reduction reads back at
+    // once, take ordinary stores.
     float* const out = a.splits > 1 ? a.part + (int64_t)split * a.M * N : a.Y;
+    const __amdgpu_buffer_rsrc_t ro =
+        __builtin_amdgcn_make_buffer_rsrc((void*)(out + (int64_t)m0 * N), (short)0, rows * N * 4, kBufferFlags);
+    const bool partial = a.splits > 1;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         float rs[16], rc[16];
@@ -868,27 +877,17 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
             const int n = n0 + nl + 32 * j;
-            float* base = out + (int64_t)(m0 + 32 * i + 4 * h) * N + n;
-            // (acc rs) cs, plus the zero-point correction of INT8-asym activations
-            auto outv = [&](int r) __attribute__((always_inline)) {
-                const float v = (acc[i][j][r] * rs[r]) * cs[j];
-                return AF == kAInt8 ? v + rc[r] * csum[j] : v;
-            };
-            if (full && a.splits > 1) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = outv(r);
-            } else if (full) {
-                // the output is not read again here: non-temporal stores keep the L2 for the
-                // operand tiles other workgroups still read (partials, read back by the
-                // reduction, take ordinary stores)
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    __builtin_nontemporal_store(outv(r), &base[(int64_t)(8 * (r >> 2) + (r & 3)) * N]);
-            } else if (n < N) {
+            if (n < N) {
+                const int voff = ((32 * i + 4 * h) * N + n) * 4;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int ml = 32 * i + 8 * (r >> 2) + 4 * h + (r & 3);
-                    if (ml < rows) base[(int64_t)(8 * (r >> 2) + (r & 3)) * N] = outv(r);
+                    // (acc rs) cs, plus the zero-point correction of INT8-asym activations
+                    float v = (acc[i][j][r] * rs[r]) * cs[j];
+                    if (AF == kAInt8) v = v + rc[r] * csum[j];
+                    const uint32_t bits = __builtin_bit_cast(uint32_t, v);
+                    const int soff = (8 * (r >> 2) + (r & 3)) * N * 4;
+                    if (partial) __builtin_amdgcn_raw_buffer_store_b32(bits, ro, voff, soff, 0);
+                    else __builtin_amdgcn_raw_buffer_store_b32(bits, ro, voff, soff, kStoreNonTemporal);
                 }
             }
         }
@@ -1275,9 +1274,9 @@ static int mixed_linear_impl(const cham_aq* xq, const WView& v, float* Y, void* 
     if (wq->code_bits != code_bits) return CHAM_EFORMAT;
     if (wq->gsel && code_bits != 4) return CHAM_EFORMAT;  // the 8-bit group-scaled decode is not built
     if (wq->K % 64 != 0) return CHAM_ESHAPE;
-    // 32-bit buffer offsets: a 256-row activation tile and the weight records stay below
-    // 2^31 bytes
-    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 2 || wq->K > (1 << 20) ||
+    // 32-bit buffer offsets: a 256-row activation tile, a 256-row output tile and the
+    // weight records stay below 2^31 bytes
+    if (xq->M > INT32_MAX / 2 || wq->N > INT32_MAX / 1024 || wq->K > (1 << 20) ||
         record_bytes(wq->N, wq->K) > (int64_t)INT32_MAX)
         return CHAM_ESHAPE;
     const bool nf4 = (mask >> CHAM_W_NF4) & 1u;

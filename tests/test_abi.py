@@ -179,3 +179,20 @@ def test_linear_workspace_query_on_the_host():
     assert nb.value <= cham.workspace_bytes(cham.OP_LINEAR, 4, 4, 64)
     aqk = cham._AQ(4, 128, cham.A_FP8_E4M3, 1, P(16), P(16), P(16), P(16))  # K mismatch
     assert L.cham_mixed_linear_workspace_query(ctypes.byref(aqk), ctypes.byref(w), ctypes.byref(nb)) == cham.EINVAL
+
+
+def test_linear_size_limits_on_the_host():
+    """The kernels address operands with 32-bit offsets: N of 2^21 channels (a 256-row output
+    tile past 2^31 bytes) and K beyond 2^20 are rejected before any launch; N just below
+    the limit passes the checks."""
+    L = cham.lib()
+    P = ctypes.c_void_p
+    nb = ctypes.c_size_t(0)
+    aq = cham._AQ(4, 64, cham.A_FP8_E4M3, 1, P(16), P(16), P(16), P(16))
+    big = _wq(N=1 << 21, code_bits=4, packed=256)
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aq), ctypes.byref(big), ctypes.byref(nb)) == cham.ESHAPE
+    ok = _wq(N=(1 << 21) - 1, code_bits=4, packed=256)
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aq), ctypes.byref(ok), ctypes.byref(nb)) == cham.OK
+    aqk = cham._AQ(4, (1 << 20) + 64, cham.A_FP8_E4M3, 1, P(16), P(16), P(16), P(16))
+    wk = _wq(K=(1 << 20) + 64, code_bits=4, packed=256)
+    assert L.cham_mixed_linear_workspace_query(ctypes.byref(aqk), ctypes.byref(wk), ctypes.byref(nb)) == cham.ESHAPE
