@@ -9,11 +9,16 @@ table over B = 10 timestep buckets (scaled-linear schedule 0.00085 -> 0.012, T =
 One step = one pass of every step of the path over one batch (one sampler step), all inputs
 resident in HBM:
   select_weight_formats_batch (the 280 layers, writing each layer's packed GEMM layout) ->
-  act_stats_accumulate_batch (the 280 layer inputs, into the step's bucket) ->
-  build_act_lut (280 x 10) -> quantize_act_lut (280, static LUT scales) -> mixed_linear (280).
-The weight side runs on a second stream (default priority) beside the statistics, LUT and
-quantization on the launch stream, which waits for it before the GEMMs; the next step's
-search waits for this step's GEMMs (they read the packed weights it rewrites).
+  quantize_act_lut_accumulate_batch (the 280 layer inputs quantized with the LUT's static
+  scales while their moments are added into the step's bucket: one read of each input) ->
+  build_act_lut (280 x 10, from the moments so far) -> mixed_linear (280).
+As a deployed model does, a step quantizes with the LUT calibrated before it (the setup's
+calibration plus the steps already run) and gathers its own inputs' moments for the LUT the
+next step uses; the formats' host mirror is refreshed from each step's LUT (a 2.8 KB copy
+that the next step's launch waits for).  The weight side runs on a second stream (default
+priority) beside the activation side on the launch stream, which waits for it before the
+GEMMs; the next step's search waits for this step's GEMMs (they read the packed weights it
+rewrites).
 
 Printed: one JSON line.  `value` = the step's GEMM flops / step time (everything else in the
 step counts against it).  `roofline` is for the dominant kernel, the mixed-format GEMM: its
@@ -151,7 +156,10 @@ def main():
         del cal
     sched = cham.Schedule(T=T_SCHED)
     lut = cham.build_act_lut(stats, sched, want_kappa=True)
-    lut.mirror()
+    # the host mirror of the LUT's formats, in pinned memory: each step refreshes it from
+    # the LUT it builds, for the next step's lookups
+    lut.F_host = torch.empty(lut.F.numel(), dtype=torch.uint8, pin_memory=True)
+    lut.F_host.copy_(lut.F)
     bucket = cham.bucket(args.t, T_SCHED, B_BUCKETS)
 
     # prepared C structs (the step issues raw C-ABI calls)
@@ -161,8 +169,10 @@ def main():
     st_s, sc_s, lut_s = stats.struct(), sched.struct(), lut.struct()
     aq_s = [a.struct() for a in aqs]
     Fh = ctypes.c_void_p(lut.F_host.data_ptr())
+    qsb = cham.QuantStatsBatch(Xs, list(range(nl)), aqs, lut, stats)
     ev = {k: [] for k in ("search", "gemm", "layer")}
     prev_end = [None]
+    f_copied = [None]
 
     def step(record=False, per_layer_events=False):
         if prev_end[0] is not None:
@@ -176,22 +186,23 @@ def main():
         searched.record(side)
         if record:
             ev["search"].append((e0, searched))
-        rc = L.cham_act_stats_accumulate_batch(tbatch.ptrs, tbatch.numel, tbatch.layer, tbatch.bucket, nl,
-                                               ctypes.byref(st_s), P(tbatch.ws), tbatch.ws_bytes, S)
+        if f_copied[0] is not None:
+            f_copied[0].synchronize()  # the formats of the LUT the previous step built
+        rc = L.cham_quantize_act_lut_accumulate_batch(qsb.ptrs, qsb.layer, nl, args.t, ctypes.byref(qsb.l), Fh,
+                                                      qsb.aq, ctypes.byref(qsb.s), P(qsb.ws), qsb.ws_bytes, S)
         assert rc == 0, rc
         rc = L.cham_build_act_lut(ctypes.byref(st_s), ctypes.byref(sc_s), None, ctypes.byref(lut_s), None, S)
         assert rc == 0, rc
-        for li in range(nl):
-            rc = L.cham_quantize_act_lut(P(Xs[li]), ctypes.byref(lut_s), Fh, li, args.t, 0, ctypes.byref(aq_s[li]),
-                                         P(ws_q), ws_q.numel(), S)
-            assert rc == 0, rc
+        lut.F_host.copy_(lut.F, non_blocking=True)
+        f_copied[0] = torch.cuda.Event()
+        f_copied[0].record(stream)
         stream.wait_event(searched)
         if record:
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
         marks = [e2] if record else []
         for li in range(nl):
-            rc = L.cham_mixed_linear(ctypes.byref(aq_s[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
+            rc = L.cham_mixed_linear(ctypes.byref(qsb.aq[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
                                      ws_lin.numel(), S)
             assert rc == 0, rc
             if per_layer_events and li + 1 < nl:
@@ -262,9 +273,10 @@ def main():
     search_gbps = sb / (ms_search * 1e-3) / 1e9
     del wq_np, nb_search
 
-    # ---- the activation side's parts, each timed alone on the launch stream: the batched
-    # moments over the 280 inputs (4 B read per element), the LUT build, and the 280
-    # quantize calls (4 B read + 1 B written per element, + 1/32 B of E8M0 for MX formats)
+    # ---- the activation side's parts, each timed alone on the launch stream: the step's
+    # fused pass (4 B read + 1 B written per element, + 1/32 B of E8M0 for MX formats), the
+    # LUT build, and for comparison the two passes it replaces: the batched moments (4 B read
+    # per element) and the 280 quantize calls (5 B per element)
     print("bench: activation side", file=sys.stderr, flush=True)
     numel = sum(M * K for (_, K, _, _), M in zip(layers, Ms))
 
@@ -283,12 +295,22 @@ def main():
                                          P(ws_q), ws_q.numel(), S)
             assert rc == 0, rc
 
+    def fused_call():
+        rc = L.cham_quantize_act_lut_accumulate_batch(qsb.ptrs, qsb.layer, nl, args.t, ctypes.byref(qsb.l), Fh,
+                                                      qsb.aq, ctypes.byref(qsb.s), P(qsb.ws), qsb.ws_bytes, S)
+        assert rc == 0, rc
+
+    ms_fused = time_calls(fused_call, stream)
     ms_stats = time_calls(stats_call, stream)
     ms_lut = time_calls(lut_call, stream)
     ms_quant = time_calls(quant_calls, stream)
     qbytes = sum(M * K * (5.0 + (1.0 / 32 if int(lut.F_host[li * B_BUCKETS + bucket]) >= 3 else 0.0))
                  for li, ((_, K, _, _), M) in enumerate(zip(layers, Ms)))
     act_side = {
+        "quantize_and_moments": {"ms": round(ms_fused, 4), "GBps": round(qbytes / (ms_fused * 1e-3) / 1e9, 1),
+                                 "frac_hbm": round(qbytes / (ms_fused * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                 "what": "the step's quantize_act_lut_accumulate_batch over the 280 layer inputs, "
+                                         "5 B per element (+1/32 for MX)"},
         "stats": {"ms": round(ms_stats, 4), "GBps": round(4.0 * numel / (ms_stats * 1e-3) / 1e9, 1),
                   "frac_hbm": round(4.0 * numel / (ms_stats * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
                   "what": "act_stats_accumulate_batch over the 280 layer inputs (binary64 power sums), 4 B per element"},
@@ -348,7 +370,7 @@ def main():
     if not args.no_extras:
         print("bench: single-step stack, PixArt-like search, dense comparison", file=sys.stderr, flush=True)
         out["single_step_stack"] = single_step_stack(cham, L, layers, Ms, Xs, wqs, stream, S)
-        out["compact_weights"] = compact_weights(cham, L, layers, Ms, wqs, aq_s, Ys, ws_lin, stream, S, ms_gemm)
+        out["compact_weights"] = compact_weights(cham, L, layers, Ms, wqs, qsb.aq, Ys, ws_lin, stream, S, ms_gemm)
         out["pixart_search"] = pixart_search(cham, synth, stream, dev)
         out["dense_f16_reference"] = dense_reference(layers, Ms, stream)
     del Ys

@@ -323,6 +323,24 @@ int cham_quantize_act_lut(const float* X, const cham_lut* lut, const uint8_t* F_
                           int32_t layer, int32_t t, int32_t dynamic, cham_aq* out, void* ws,
                           size_t ws_bytes, void* stream);
 
+/* Alg. 2's runtime quantization and Alg. 1's moment gathering in one pass over each input,
+ * for a model that keeps calibrating while it runs: tensor X[i] (out[i].M x out[i].K
+ * binary32, device, 16-byte aligned) of layer[i] at timestep t is quantized as
+ * cham_quantize_act_lut(X[i], lut, F_host, layer[i], t, 0, &out[i], ...) would do it
+ * (static scales: the LUT's S/Z of (layer[i], b), b = cham_bucket(t, lut->T, lut->B), as
+ * the device holds them when the kernel runs), and its moments are added into st at
+ * (layer[i], b) as cham_act_stats_accumulate_batch adds them.  Codes, E8M0 bytes, scales,
+ * zero points and accumulators are the bits those two calls give, in that order, on the
+ * same inputs.  A LUT built afterwards from st sees this call's moments; the codes of this
+ * call do not depend on them.  out: host array of n descriptors (fmt is filled in from
+ * F_host).  layer: host array of n.  st->L, B must equal lut's.  ws: the sum of
+ * cham_workspace_bytes(CHAM_OP_STATS, out[i].M * out[i].K, 0, 0) over i.  Every argument is
+ * checked before anything is launched.  Errors: CHAM_EINVAL, CHAM_EFORMAT, CHAM_ESHAPE
+ * (K % 32), CHAM_EWORKSPACE, CHAM_EHIP. */
+int cham_quantize_act_lut_accumulate_batch(const float* const* X, const int32_t* layer, int32_t n, int32_t t,
+                                           const cham_lut* lut, const uint8_t* F_host, cham_aq* out,
+                                           cham_act_stats* st, void* ws, size_t ws_bytes, void* stream);
+
 /* ---------------------------------------------------------------------------------------
  * 4. the mixed-format linear layer
  *

@@ -103,6 +103,9 @@ def lib():
     L.cham_quantize_act_lut.argtypes = [_P, ctypes.POINTER(_LUT), _P, i32, i32, i32, ctypes.POINTER(_AQ), _P, sz,
                                         _P]
     L.cham_quantize_act_noalloc.argtypes = [_P, i32, i32, _P, _P, ctypes.POINTER(_AQ), _P]
+    L.cham_quantize_act_lut_accumulate_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(i32), i32, i32,
+                                                         ctypes.POINTER(_LUT), _P, ctypes.POINTER(_AQ),
+                                                         ctypes.POINTER(_Stats), _P, sz, _P]
     L.cham_mixed_linear.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), _P, _P, sz, _P]
     L.cham_mixed_linear_grouped.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_GWQ), _P, _P, sz, _P]
     L.cham_mixed_linear_workspace_query.argtypes = [ctypes.POINTER(_AQ), ctypes.POINTER(_WQ), ctypes.POINTER(sz)]
@@ -121,6 +124,7 @@ def lib():
     for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_quantize_act_noalloc",
+                 "cham_quantize_act_lut_accumulate_batch",
                  "cham_mixed_linear", "cham_mixed_linear_grouped", "cham_select_group_formats", "cham_conv3x3_mixed",
                  "cham_act_colsq_accumulate",
                  "cham_linear_plan"):
@@ -487,6 +491,47 @@ def quantize_act_lut(X: torch.Tensor, lut: LUT, layer: int, t: int, dynamic: boo
            "quantize_act_lut")
     out.fmt = a.fmt
     return out
+
+
+class QuantStatsBatch:
+    """Prepared C arguments of a fused quantize-and-accumulate call: inputs Xs[i] of
+    layers[i] quantized into outs[i] with the LUT's static scales at timestep t while their
+    moments are added into st (reusable across calls with the same tensors)."""
+
+    def __init__(self, Xs, layers, outs, lut: "LUT", st: Stats, ws=None):
+        n = len(Xs)
+        assert n > 0 and len(layers) == n and len(outs) == n
+        for X, o in zip(Xs, outs):
+            _dev_tensor(X, torch.float32, "X")
+            assert X.shape == (o.M, o.K), "X and its AQ differ in shape"
+        if lut.F_host is None:
+            lut.mirror()
+        self.Xs, self.outs, self.lut, self.st = list(Xs), list(outs), lut, st
+        self.ptrs = (_P * n)(*[X.data_ptr() for X in Xs])
+        self.layer = (ctypes.c_int32 * n)(*layers)
+        self.aq = (_AQ * n)(*[o.struct() for o in outs])
+        nb = sum(workspace_bytes(OP_STATS, X.numel(), 0, 0) for X in Xs)
+        self.ws = ws if ws is not None else torch.empty(max(nb, 256), dtype=torch.uint8, device=Xs[0].device)
+        self.ws_bytes = self.ws.numel()
+        self.s = st.struct()
+        self.l = lut.struct()
+
+    def run(self, t: int, stream=None):
+        _check(lib().cham_quantize_act_lut_accumulate_batch(
+            self.ptrs, self.layer, len(self.Xs), t, ctypes.byref(self.l), ctypes.c_void_p(self.lut.F_host.data_ptr()),
+            self.aq, ctypes.byref(self.s), _ptr(self.ws), self.ws_bytes, _stream(stream)),
+            "quantize_act_lut_accumulate_batch")
+        for o, a in zip(self.outs, self.aq):
+            o.fmt = a.fmt
+
+
+def quantize_act_lut_accumulate_batch(Xs, layers, t: int, lut: "LUT", st: Stats, outs=None, stream=None):
+    """Quantize each Xs[i] as quantize_act_lut(Xs[i], lut, layers[i], t) does (static scales)
+    and add its moments into st at (layers[i], bucket of t), in one pass; returns the AQs."""
+    if outs is None:
+        outs = [alloc_aq(X.shape[0], X.shape[1], X.device) for X in Xs]
+    QuantStatsBatch(Xs, layers, outs, lut, st).run(t, stream)
+    return outs
 
 
 # -------------------------------------------------------------------------------------------

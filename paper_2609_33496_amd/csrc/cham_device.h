@@ -172,6 +172,71 @@ CHAM_DEV float group_max(float v) {
     return v;
 }
 
+// ------------------------------------------------------------------------------------
+// activation codes of one float4 (App. A.11; the quantize pass and the fused
+// quantize-and-accumulate pass share this arithmetic, so their codes are the same bits)
+// ------------------------------------------------------------------------------------
+// Four codes (already scaled, in range) packed into one word, element j in byte j.  FP8:
+// the gfx950 converters (round to nearest even, subnormals included; the operands are
+// clamped to the largest finite value first, so no saturation rule applies).
+template <int FMT>
+CHAM_DEV uint32_t pack_codes(float y0, float y1, float y2, float y3, float z) {
+    if (FMT == CHAM_A_INT8_ASYM) {
+        const float e[4] = {y0, y1, y2, y3};
+        uint32_t w = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w |= (uint32_t)clampf(rne(e[j]) + z, 0.0f, 255.0f) << (8 * j);
+        return w;
+    } else {
+        typedef short v2s __attribute__((ext_vector_type(2)));
+        v2s c = {0, 0};
+        if (FMT == CHAM_A_FP8_E4M3) {
+            c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, y0, y1, 1.0f, false);
+            c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, y2, y3, 1.0f, true);
+        } else {
+            c = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(c, y0, y1, 1.0f, false);
+            c = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(c, y2, y3, 1.0f, true);
+        }
+        return __builtin_bit_cast(uint32_t, c);
+    }
+}
+
+// Per-tensor formats (INT8-asym, E4M3, E5M2): x r with r = fl(1/s), FP8 clamped to the
+// format's largest finite value, INT8-asym rne(x r) + z clamped to [0, 255].
+template <int FMT>
+CHAM_DEV uint32_t act_codes4(const float4& t, float r, float z) {
+    if (FMT == CHAM_A_INT8_ASYM) return pack_codes<FMT>(t.x * r, t.y * r, t.z * r, t.w * r, z);
+    const float ymax = FMT == CHAM_A_FP8_E4M3 ? 448.0f : 57344.0f;
+    return pack_codes<FMT>(clampf(t.x * r, -ymax, ymax), clampf(t.y * r, -ymax, ymax), clampf(t.z * r, -ymax, ymax),
+                           clampf(t.w * r, -ymax, ymax), 0.0f);
+}
+
+// MX formats: the float4 is one eighth of a 32-block held by 8 consecutive lanes, which
+// must all be active; returns the codes and the block's exponent E (its E8M0
+// byte is E + 127).
+template <int FMT>
+CHAM_DEV uint32_t act_codes4_mx(const float4& t, int* Eout) {
+    const float e[4] = {t.x, t.y, t.z, t.w};
+    float m = fmaxf(fmaxf(fabsf(e[0]), fabsf(e[1])), fmaxf(fabsf(e[2]), fabsf(e[3])));
+    m = group_max<8>(m);
+    const int E = mx_exponent(m, 0);
+    uint32_t w = 0;
+    if (FMT == CHAM_A_MXFP8_E4M3) {
+        float y[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) y[j] = clampf(ldexpf(e[j], -E), -448.0f, 448.0f);
+        w = pack_codes<CHAM_A_FP8_E4M3>(y[0], y[1], y[2], y[3], 0.0f);
+    } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float k = clampf(rne(ldexpf(e[j], 6 - E)), -127.0f, 127.0f);
+            w |= ((uint32_t)(int)k & 0xFFu) << (8 * j);
+        }
+    }
+    *Eout = E;
+    return w;
+}
+
 }  // namespace cham
 
 // host-side helpers shared by the entry points

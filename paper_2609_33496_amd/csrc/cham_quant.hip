@@ -86,31 +86,6 @@ struct QArgs {
     float* zero_out;
 };
 
-// Four codes of one float4 (already scaled, in range) packed into one word, element j in
-// byte j.  FP8: the gfx950 converters (round to nearest even, subnormals included; the
-// operands are clamped to the largest finite value first, so no saturation rule applies).
-template <int FMT>
-CHAM_DEV uint32_t pack_codes(float y0, float y1, float y2, float y3, float z) {
-    if (FMT == CHAM_A_INT8_ASYM) {
-        const float e[4] = {y0, y1, y2, y3};
-        uint32_t w = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) w |= (uint32_t)clampf(rne(e[j]) + z, 0.0f, 255.0f) << (8 * j);
-        return w;
-    } else {
-        typedef short v2s __attribute__((ext_vector_type(2)));
-        v2s c = {0, 0};
-        if (FMT == CHAM_A_FP8_E4M3) {
-            c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, y0, y1, 1.0f, false);
-            c = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(c, y2, y3, 1.0f, true);
-        } else {
-            c = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(c, y0, y1, 1.0f, false);
-            c = __builtin_amdgcn_cvt_scalef32_pk_bf8_f32(c, y2, y3, 1.0f, true);
-        }
-        return __builtin_bit_cast(uint32_t, c);
-    }
-}
-
 // The first loads of every thread are issued before the workgroup learns the scale (its
 // fetch, or the fold of the dynamic partials, would otherwise stand in front of them), and
 // each iteration issues the next run's loads before it converts the current one.
@@ -156,18 +131,12 @@ __global__ __launch_bounds__(kQThreads) void quant_tensor_kernel(QArgs a) {
     __syncthreads();
     const float s = sh_s, z = sh_z;
     const float r = 1.0f / s;
-    const float ymax = FMT == CHAM_A_FP8_E4M3 ? 448.0f : 57344.0f;
     for (; i0 < nq; i0 += qstep(a.nbs)) {
         float4 tn[kQLoads];
         if (i0 + qstep(a.nbs) < nq) load(tn, i0 + qstep(a.nbs));
 #pragma unroll
         for (int u = 0; u < kQLoads; ++u) {
-            uint32_t w;
-            if (FMT == CHAM_A_INT8_ASYM)
-                w = pack_codes<FMT>(t[u].x * r, t[u].y * r, t[u].z * r, t[u].w * r, z);
-            else
-                w = pack_codes<FMT>(clampf(t[u].x * r, -ymax, ymax), clampf(t[u].y * r, -ymax, ymax),
-                                    clampf(t[u].z * r, -ymax, ymax), clampf(t[u].w * r, -ymax, ymax), 0.0f);
+            const uint32_t w = act_codes4<FMT>(t[u], r, z);
             const int64_t i = qidx(i0, u);
             if (i < nq) C4[i] = w;
         }
@@ -199,23 +168,8 @@ __global__ __launch_bounds__(kQThreads) void quant_mx_kernel(const float* X, int
         }
 #pragma unroll
         for (int u = 0; u < kQLoads; ++u) {
-            const float e[4] = {t[u].x, t[u].y, t[u].z, t[u].w};
-            float m = fmaxf(fmaxf(fabsf(e[0]), fabsf(e[1])), fmaxf(fabsf(e[2]), fabsf(e[3])));
-            m = group_max<8>(m);
-            const int E = mx_exponent(m, 0);
-            uint32_t w = 0;
-            if (FMT == CHAM_A_MXFP8_E4M3) {
-                float y[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) y[j] = clampf(ldexpf(e[j], -E), -448.0f, 448.0f);
-                w = pack_codes<CHAM_A_FP8_E4M3>(y[0], y[1], y[2], y[3], 0.0f);
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float k = clampf(rne(ldexpf(e[j], 6 - E)), -127.0f, 127.0f);
-                    w |= ((uint32_t)(int)k & 0xFFu) << (8 * j);
-                }
-            }
+            int E;
+            const uint32_t w = act_codes4_mx<FMT>(t[u], &E);
             const int64_t i = qidx(i0, u);
             if (i < nq) {
                 C4[i] = w;

@@ -10,20 +10,10 @@
 
 #include <algorithm>
 
-#include "cham_device.h"
+#include "cham_moments.h"
 
 namespace cham {
 namespace {
-
-constexpr int kStatsThreads = 256;
-constexpr int kStatsMaxBlocks = 1024;
-constexpr int kStatsLoads = 16;  // 16-byte loads in flight per thread
-
-struct Partial {
-    double s1, s2, s3, s4;
-    float lo, hi;
-    float pad0, pad1;
-};
 
 // Tensors of one accumulate call (several for the batched call): workgroups of tensor i are
 // [blk_end[i-1], blk_end[i]); partials are stored at the workgroup index.
@@ -35,70 +25,81 @@ struct StatsBatch {
     int64_t numel[kStatsBatchMax];
 };
 
-__global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(StatsBatch B, Partial* part) {
+// the batch entry (tensor) of workgroup blockIdx.x, its first workgroup and its count
+CHAM_DEV int batch_entry(const int* blk_end, int n, int* lb, int* nb) {
     int ti = 0;
-    while (ti + 1 < B.n && (int)blockIdx.x >= B.blk_end[ti]) ++ti;
-    const int b0 = ti ? B.blk_end[ti - 1] : 0;
-    const int lb = (int)blockIdx.x - b0, nb = B.blk_end[ti] - b0;  // this tensor's workgroups
-    const float* X = B.X[ti];
-    const int64_t numel = B.numel[ti];
-    double s1 = 0.0, s2 = 0.0, s3 = 0.0, s4 = 0.0;
-    float lo = INFINITY, hi = -INFINITY;
-    const int64_t nq = numel >> 2;
-    const int64_t stride = (int64_t)nb * blockDim.x;
-    const float4* X4 = reinterpret_cast<const float4*>(X);
-    auto add = [&](const float4& t) {
-        const float e[4] = {t.x, t.y, t.z, t.w};
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            double d = (double)e[j];
-            double d2 = d * d;
-            s1 += d;
-            s2 += d2;
-            s3 += d2 * d;
-            s4 += d2 * d2;
-            lo = fminf(lo, e[j]);
-            hi = fmaxf(hi, e[j]);
-        }
-    };
-    // kStatsLoads loads in flight per thread, then their sums in index order
-    int64_t i = (int64_t)lb * blockDim.x + threadIdx.x;
-    for (; i + (kStatsLoads - 1) * stride < nq; i += kStatsLoads * stride) {
-        float4 t[kStatsLoads];
-#pragma unroll
-        for (int q = 0; q < kStatsLoads; ++q) t[q] = X4[i + q * stride];
-#pragma unroll
-        for (int q = 0; q < kStatsLoads; ++q) add(t[q]);
+    while (ti + 1 < n && (int)blockIdx.x >= blk_end[ti]) ++ti;
+    const int b0 = ti ? blk_end[ti - 1] : 0;
+    *lb = (int)blockIdx.x - b0;
+    *nb = blk_end[ti] - b0;
+    return ti;
+}
+
+__global__ __launch_bounds__(kStatsThreads) void stats_partial_kernel(StatsBatch B, Partial* part) {
+    int lb, nb;
+    const int ti = batch_entry(B.blk_end, B.n, &lb, &nb);
+    moments_block(B.X[ti], B.numel[ti], lb, nb, [](const float4&, int64_t) {}, part + blockIdx.x);
+}
+
+// The fused pass: each tensor quantized with its static scale (as the quantize pass does it,
+// App. A.7 Alg. 2 with the LUT's (s, z)) while its moments are gathered exactly as the
+// statistics pass gathers them.  One read of X serves both.
+constexpr int kQSBatchMax = 32;
+struct QSBatch {
+    int n;
+    int blk_end[kQSBatchMax];
+    const float* X[kQSBatchMax];
+    int64_t numel[kQSBatchMax];
+    int fmt[kQSBatchMax];
+    int nsamples[kQSBatchMax];
+    const float* s_dev[kQSBatchMax];  // the LUT's (s, z) of the tensor's (layer, bucket)
+    const float* z_dev[kQSBatchMax];
+    uint32_t* codes[kQSBatchMax];
+    uint8_t* e8[kQSBatchMax];
+    float* scale_out[kQSBatchMax];
+    float* zero_out[kQSBatchMax];
+};
+
+template <int FMT>
+CHAM_DEV void quant_stats_tensor(const QSBatch& B, int ti, int lb, int nb, Partial* out) {
+    uint32_t* C4 = B.codes[ti];
+    if (FMT == CHAM_A_MXFP8_E4M3 || FMT == CHAM_A_MXINT8) {
+        if (lb == 0)
+            for (int q = threadIdx.x; q < B.nsamples[ti]; q += kStatsThreads) {
+                B.scale_out[ti][q] = 1.0f;
+                B.zero_out[ti][q] = 0.0f;
+            }
+        uint8_t* e8 = B.e8[ti];
+        moments_block(B.X[ti], B.numel[ti], lb, nb,
+                      [&](const float4& t, int64_t i) {
+                          int E;
+                          C4[i] = act_codes4_mx<FMT>(t, &E);
+                          if ((threadIdx.x & 7) == 0) e8[i >> 3] = (uint8_t)(E + 127);
+                      },
+                      out);
+    } else {
+        const float s = *B.s_dev[ti], z = *B.z_dev[ti];
+        if (lb == 0)
+            for (int q = threadIdx.x; q < B.nsamples[ti]; q += kStatsThreads) {
+                B.scale_out[ti][q] = s;
+                B.zero_out[ti][q] = z;
+            }
+        const float r = 1.0f / s;
+        moments_block(B.X[ti], B.numel[ti], lb, nb, [&](const float4& t, int64_t i) { C4[i] = act_codes4<FMT>(t, r, z); },
+                      out);
     }
-    // the last few: all loads issued first, then the sums in index order
-    {
-        float4 t[kStatsLoads - 1];
-#pragma unroll
-        for (int q = 0; q < kStatsLoads - 1; ++q) t[q] = i + q * stride < nq ? X4[i + q * stride] : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int q = 0; q < kStatsLoads - 1; ++q)
-            if (i + q * stride < nq) add(t[q]);
-    }
-    // scalar tail (numel % 4), handled by the first threads of the tensor's workgroup 0
-    if (lb == 0 && threadIdx.x < (numel & 3)) {
-        float x = X[(nq << 2) + threadIdx.x];
-        double d = (double)x, d2 = d * d;
-        s1 += d; s2 += d2; s3 += d2 * d; s4 += d2 * d2;
-        lo = fminf(lo, x); hi = fmaxf(hi, x);
-    }
-    s1 = wave_sum(s1); s2 = wave_sum(s2); s3 = wave_sum(s3); s4 = wave_sum(s4);
-    lo = wave_min(lo); hi = wave_max(hi);
-    __shared__ Partial wp[kStatsThreads / kWave];
-    const int w = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) wp[w] = Partial{s1, s2, s3, s4, lo, hi, 0.f, 0.f};
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        Partial r = wp[0];
-        for (int i = 1; i < kStatsThreads / kWave; ++i) {
-            r.s1 += wp[i].s1; r.s2 += wp[i].s2; r.s3 += wp[i].s3; r.s4 += wp[i].s4;
-            r.lo = fminf(r.lo, wp[i].lo); r.hi = fmaxf(r.hi, wp[i].hi);
-        }
-        part[blockIdx.x] = r;
+}
+
+__global__ __launch_bounds__(kStatsThreads) void quant_stats_kernel(QSBatch B, Partial* part) {
+    int lb, nb;
+    const int ti = batch_entry(B.blk_end, B.n, &lb, &nb);
+    Partial* out = part + blockIdx.x;
+    switch (B.fmt[ti]) {  // workgroup-uniform
+    case CHAM_A_INT8_ASYM: quant_stats_tensor<CHAM_A_INT8_ASYM>(B, ti, lb, nb, out); break;
+    case CHAM_A_FP8_E4M3: quant_stats_tensor<CHAM_A_FP8_E4M3>(B, ti, lb, nb, out); break;
+    case CHAM_A_FP8_E5M2: quant_stats_tensor<CHAM_A_FP8_E5M2>(B, ti, lb, nb, out); break;
+    case CHAM_A_MXFP8_E4M3: quant_stats_tensor<CHAM_A_MXFP8_E4M3>(B, ti, lb, nb, out); break;
+    default: quant_stats_tensor<CHAM_A_MXINT8>(B, ti, lb, nb, out); break;
     }
 }
 
@@ -289,6 +290,42 @@ static int stats_blocks(int64_t numel) {
 
 size_t cham_stats_workspace_bytes(int64_t numel) { return sizeof(Partial) * (size_t)stats_blocks(numel); }
 
+// The finalize launch of batch tensors [i0, i0 + m): per tensor its partials (counts nb[q])
+// and numel, and the accumulator targets (layer, bucket) in order of first appearance, each
+// with its tensors in batch order.
+static FinBatch fin_batch(const int64_t* numel, const int* nb, const int32_t* layer, const int32_t* bucket, int m,
+                          const cham_act_stats* st) {
+    FinBatch F;
+    F.ntgt = 0;
+    int blk = 0;
+    for (int q = 0; q < m; ++q) {
+        F.pbeg[q] = blk;
+        F.pcnt[q] = nb[q];
+        F.numel[q] = numel[q];
+        blk += nb[q];
+    }
+    int tgt_of[kStatsBatchMax];
+    for (int q = 0; q < m; ++q) {
+        const int64_t ti = (int64_t)layer[q] * st->B + bucket[q];
+        int j = 0;
+        while (j < F.ntgt && F.nS[j] != st->nS + 5 * ti) ++j;
+        if (j == F.ntgt) {
+            F.nS[j] = st->nS + 5 * ti;
+            F.lohi[j] = st->lohi + 2 * ti;
+            F.count[j] = 0;
+            ++F.ntgt;
+        }
+        tgt_of[q] = j;
+        ++F.count[j];
+    }
+    for (int j = 0, o = 0; j < F.ntgt; ++j) {
+        F.first[j] = o;
+        for (int q = 0; q < m; ++q)
+            if (tgt_of[q] == j) F.order[o++] = q;
+    }
+    return F;
+}
+
 extern "C" int cham_act_stats_accumulate_batch(const float* const* X, const int64_t* numel, const int32_t* layer,
                                                const int32_t* bucket, int32_t n, cham_act_stats* st, void* ws,
                                                size_t ws_bytes, void* stream) {
@@ -305,42 +342,81 @@ extern "C" int cham_act_stats_accumulate_batch(const float* const* X, const int6
     for (int i0 = 0; i0 < n; i0 += kStatsBatchMax) {  // launches in order: the accumulation order holds
         const int m = std::min(kStatsBatchMax, n - i0);
         StatsBatch B;
-        FinBatch F;
+        int nb[kStatsBatchMax];
         B.n = m;
-        F.ntgt = 0;
         int blk = 0;
         for (int q = 0; q < m; ++q) {
-            const int i = i0 + q;
-            const int nb = stats_blocks(numel[i]);
-            B.X[q] = X[i];
-            B.numel[q] = numel[i];
-            F.pbeg[q] = blk;
-            F.pcnt[q] = nb;
-            F.numel[q] = numel[i];
-            blk += nb;
+            nb[q] = stats_blocks(numel[i0 + q]);
+            B.X[q] = X[i0 + q];
+            B.numel[q] = numel[i0 + q];
+            blk += nb[q];
             B.blk_end[q] = blk;
         }
-        // targets in order of first appearance, each with its tensors in batch order
-        int tgt_of[kStatsBatchMax];
-        for (int q = 0; q < m; ++q) {
-            const int64_t ti = (int64_t)layer[i0 + q] * st->B + bucket[i0 + q];
-            int j = 0;
-            while (j < F.ntgt && F.nS[j] != st->nS + 5 * ti) ++j;
-            if (j == F.ntgt) {
-                F.nS[j] = st->nS + 5 * ti;
-                F.lohi[j] = st->lohi + 2 * ti;
-                F.count[j] = 0;
-                ++F.ntgt;
-            }
-            tgt_of[q] = j;
-            ++F.count[j];
-        }
-        for (int j = 0, o = 0; j < F.ntgt; ++j) {
-            F.first[j] = o;
-            for (int q = 0; q < m; ++q)
-                if (tgt_of[q] == j) F.order[o++] = q;
-        }
+        const FinBatch F = fin_batch(numel + i0, nb, layer + i0, bucket + i0, m, st);
         hipLaunchKernelGGL(stats_partial_kernel, dim3(blk), dim3(kStatsThreads), 0, s, B, part);
+        CHAM_CHECK_LAUNCH();
+        hipLaunchKernelGGL(stats_finalize_kernel, dim3(F.ntgt), dim3(kStatsThreads), 0, s, F, part);
+        CHAM_CHECK_LAUNCH();
+        part += blk;
+    }
+    return CHAM_OK;
+}
+
+// Bucket b of timestep t for every tensor; formats from the host mirror of the LUT's F.
+extern "C" int cham_quantize_act_lut_accumulate_batch(const float* const* X, const int32_t* layer, int32_t n,
+                                                      int32_t t, const cham_lut* lut, const uint8_t* F_host,
+                                                      cham_aq* out, cham_act_stats* st, void* ws, size_t ws_bytes,
+                                                      void* stream) {
+    if (!X || !layer || n < 1 || !lut || !F_host || !lut->S || !lut->Z || !out) return CHAM_EINVAL;
+    if (!st || !st->nS || !st->lohi || st->L != lut->L || st->B != lut->B) return CHAM_EINVAL;
+    const int32_t b = cham_bucket(t, lut->T, lut->B);
+    if (b < 0) return CHAM_EINVAL;
+    size_t parts = 0;
+    for (int i = 0; i < n; ++i) {
+        if (layer[i] < 0 || layer[i] >= lut->L) return CHAM_EINVAL;
+        const cham_aq& o = out[i];
+        if (!X[i] || !o.codes || !o.scale || !o.zero || o.M < 1 || o.K < 1) return CHAM_EINVAL;
+        if (o.nsamples < 1 || o.M % o.nsamples != 0) return CHAM_EINVAL;
+        if (((uintptr_t)X[i] & 15u) != 0 || ((uintptr_t)o.codes & 3u) != 0) return CHAM_EINVAL;
+        const int fmt = F_host[(int64_t)layer[i] * lut->B + b];
+        if (fmt < 0 || fmt >= CHAM_A_NFMT) return CHAM_EFORMAT;
+        if (o.K % 32 != 0) return CHAM_ESHAPE;
+        if ((fmt == CHAM_A_MXFP8_E4M3 || fmt == CHAM_A_MXINT8) && !o.e8m0) return CHAM_EINVAL;
+        parts += (size_t)stats_blocks(o.M * o.K);
+    }
+    if (!ws || ws_bytes < sizeof(Partial) * parts) return CHAM_EWORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    Partial* part = (Partial*)ws;
+    for (int i0 = 0; i0 < n; i0 += kQSBatchMax) {  // launches in order: the accumulation order holds
+        const int m = std::min(kQSBatchMax, n - i0);
+        QSBatch B;
+        int nb[kQSBatchMax];
+        int64_t numel[kQSBatchMax];
+        int32_t bucket[kQSBatchMax];
+        B.n = m;
+        int blk = 0;
+        for (int q = 0; q < m; ++q) {
+            cham_aq& o = out[i0 + q];
+            const int64_t li = (int64_t)layer[i0 + q] * lut->B + b;
+            o.fmt = F_host[li];
+            numel[q] = o.M * o.K;
+            bucket[q] = b;
+            nb[q] = stats_blocks(numel[q]);
+            B.X[q] = X[i0 + q];
+            B.numel[q] = numel[q];
+            B.fmt[q] = o.fmt;
+            B.nsamples[q] = o.nsamples;
+            B.s_dev[q] = lut->S + li;
+            B.z_dev[q] = lut->Z + li;
+            B.codes[q] = (uint32_t*)o.codes;
+            B.e8[q] = o.e8m0;
+            B.scale_out[q] = o.scale;
+            B.zero_out[q] = o.zero;
+            blk += nb[q];
+            B.blk_end[q] = blk;
+        }
+        const FinBatch F = fin_batch(numel, nb, layer + i0, bucket, m, st);
+        hipLaunchKernelGGL(quant_stats_kernel, dim3(blk), dim3(kStatsThreads), 0, s, B, part);
         CHAM_CHECK_LAUNCH();
         hipLaunchKernelGGL(stats_finalize_kernel, dim3(F.ntgt), dim3(kStatsThreads), 0, s, F, part);
         CHAM_CHECK_LAUNCH();

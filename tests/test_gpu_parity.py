@@ -443,6 +443,53 @@ def test_quantize_act_lut_lookup(dynamic):
                 _check_aq(aq, X, int(F[i]), S[i], Z[i], dynamic=False)
 
 
+def test_quantize_accumulate_matches_separate_calls():
+    """The fused pass (quantize with the LUT's static scales while adding the moments) gives
+    the bits of quantize_act_lut per tensor followed by act_stats_accumulate_batch: every
+    activation format (a host format mirror set per layer), ragged row counts, two samples,
+    K a multiple of 32 only, a layer seen twice, and more tensors than one launch takes;
+    the codes also against the oracle."""
+    L, B, t = 7, 4, 600
+    st0, _ = _calibrate(L, B, 64, 256, seed=4, steps_per_bucket=1)
+    lut = cham.build_act_lut(st0).mirror()
+    b = oracle.bucket(t, 1000, B)
+    F = lut.F_host.clone()
+    for l in range(L):  # every format, whatever the gates chose
+        F[l * B + b] = l % 5
+    lut.F_host = F
+    shapes = [(37 + 13 * i, 32 * (1 + i % 5)) for i in range(40)]
+    layers = [i % L for i in range(40)]
+    Xs = [torch.from_numpy(synth.diffusion_acts(6, l, t, M, K)).to(DEV) for (M, K), l in zip(shapes, layers)]
+    nsamp = [2 if M % 2 == 0 else 1 for (M, _) in shapes]
+    # separate calls on a copy of the accumulators
+    st_a = cham.alloc_stats(L, B, DEV)
+    st_a.nS.copy_(st0.nS)
+    st_a.lohi.copy_(st0.lohi)
+    st_b = cham.alloc_stats(L, B, DEV)
+    st_b.nS.copy_(st0.nS)
+    st_b.lohi.copy_(st0.lohi)
+    case("quantize_act_lut x 40 then act_stats_accumulate_batch")
+    ref = [cham.quantize_act_lut(X, lut, l, t, dynamic=False, nsamples=ns) for X, l, ns in zip(Xs, layers, nsamp)]
+    cham.act_stats_accumulate_batch(Xs, layers, [b] * len(Xs), st_a)
+    case("quantize_act_lut_accumulate_batch x 40")
+    outs = [cham.alloc_aq(X.shape[0], X.shape[1], DEV, nsamples=ns) for X, ns in zip(Xs, nsamp)]
+    cham.quantize_act_lut_accumulate_batch(Xs, layers, t, lut, st_b, outs=outs)
+    torch.cuda.synchronize()
+    assert np.array_equal(_np(st_a.nS).view(np.uint64), _np(st_b.nS).view(np.uint64))
+    assert np.array_equal(_np(st_a.lohi).view(np.uint32), _np(st_b.lohi).view(np.uint32))
+    S, Z = _np(lut.S), _np(lut.Z)
+    for i, (r, o, X, l) in enumerate(zip(ref, outs, Xs, layers)):
+        fmt = int(F[l * B + b])
+        assert o.fmt == r.fmt == fmt
+        assert np.array_equal(_np(o.codes), _np(r.codes)), i
+        assert np.array_equal(_np(o.scale).view(np.uint32), _np(r.scale).view(np.uint32)), i
+        assert np.array_equal(_np(o.zero).view(np.uint32), _np(r.zero).view(np.uint32)), i
+        if fmt >= 3:
+            assert np.array_equal(_np(o.e8m0), _np(r.e8m0)), i
+        if i < 10:
+            _check_aq(o, _np(X), fmt, S[l * B + b], Z[l * B + b], dynamic=False)
+
+
 # ---------------------------------------------------------------------------------------
 # mixed-format linear layer
 # ---------------------------------------------------------------------------------------
