@@ -579,6 +579,8 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     constexpr int P = CW + 2;          // 16-byte pieces per record (codes + two table planes)
     constexpr bool HALF = AF == kAF16 || AF == kAConv;   // the operand comes in half precision
     constexpr int AQ = HALF ? TM : (TM + 1) / 2;  // activation loads per thread per k-step
+    // codes: every load of the workgroup falls inside the tile (even TM), no range test
+    constexpr bool AFULL = HALF || AQ * kThreads == BM * 4;
     constexpr int A_CH = BM * BK * 2 / 16;      // 16-byte chunks of an activation tile
     __shared__ uint4 lds[2][A_CH];
     __shared__ __align__(16) float Rs[BM];
@@ -674,7 +676,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
                                  : (uint32_t)(((pix[i] + tapoff) * a.C + ci0) * 2) + (aoff0 - (uint32_t)((t >> 3) * K * 2));
             else
                 off = HALF ? aoff0 + (uint32_t)(i * 64 * K + k * BK * 2) : aoff0 + (uint32_t)(i * 64 * K + k * BK);
-            S.v[i] = (!HALF && i * 256 + t >= BM * 4)
+            S.v[i] = (!AFULL && i * 256 + t >= BM * 4)
                          ? make_uint4(0u, 0u, 0u, 0u)
                          : __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ra, (int)off, 0, 0));
         }
@@ -686,7 +688,7 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
                 lds[buf][i * 256 + t] = S.v[i];
             } else {
                 const int q = i * 256 + t;
-                if (q < BM * 4) {
+                if (AFULL || q < BM * 4) {
                     const int r = q >> 2, c = 2 * (q & 3), sw = (r >> 1) & 7;
                     lds[buf][r * 8 + (c ^ sw)] = decode_act8<AF>(S.v[i].x, S.v[i].y, perm4, negz[i]);
                     lds[buf][r * 8 + ((c + 1) ^ sw)] = decode_act8<AF>(S.v[i].z, S.v[i].w, perm4, negz[i]);
