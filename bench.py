@@ -16,13 +16,16 @@ As a deployed model does, a step quantizes with the LUT calibrated before it (th
 calibration plus the steps already run) and gathers its own inputs' moments for the LUT the
 next step uses; the formats' host mirror is refreshed from each step's LUT (a 2.8 KB copy
 that the next step's launch waits for).  The weight side runs on a second stream (default
-priority) beside the activation side on the launch stream, which waits for it before the
-GEMMs; the next step's search waits for this step's GEMMs (they read the packed weights it
-rewrites).
+priority) beside the activation side on the launch stream, in three chunks of consecutive
+layers (about equal weight counts): the GEMMs of a chunk wait only for that chunk's search,
+so the later chunks' searches share the chip with the earlier chunks' GEMMs, and the next
+step's search of a chunk waits for this step's GEMMs of that chunk (they read the packed
+weights it rewrites).
 
 Printed: one JSON line.  `value` = the step's GEMM flops / step time (everything else in the
 step counts against it).  `roofline` is for the dominant kernel, the mixed-format GEMM: its
-280 calls timed with HIP events on the launch stream inside the timed steps; per layer kind
+280 calls timed with HIP events on the launch stream inside the timed steps (where a search
+chunk runs beside them), and the same calls alone after the timed steps; per layer kind
 (width x linear) from untimed steps with an event between calls.  Beside it: the weight
 search of the whole stack timed as its own call (no packing; the search's own algorithmic
 bytes), the packing pass by difference, the PixArt-like 28-block search at W4 and W8, the single-step (batch 1)
@@ -64,6 +67,9 @@ def parse():
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="first run one device-to-device copy of this many MiB (the known-size "
                         "kernel that scales the profiler's HBM byte counters; 0: none)")
+    p.add_argument("--search-chunks", type=int, default=3,
+                   help="split the stack's search into this many chunks of consecutive layers (about equal "
+                        "weight counts); the GEMMs of a chunk wait only for its search")
     p.add_argument("--layer-steps", type=int, default=2,
                    help="untimed steps after the timed ones for the per-layer GEMM breakdown (0: none)")
     return p.parse_args()
@@ -165,27 +171,38 @@ def main():
     # prepared C structs (the step issues raw C-ABI calls)
     wq_s = [w.struct() for w in wqs]
     sbatch = cham.SearchBatch(Ws, wqs)
+    # chunks of consecutive layers with about equal weight counts: the search of chunk c runs
+    # on the side stream, the GEMMs of chunk c wait only for it, and the next step's search of
+    # chunk c only for this step's GEMMs of chunk c
+    nw = np.cumsum([N * K for (_, K, N, _) in layers])
+    cuts = sorted({int(np.searchsorted(nw, nw[-1] * (c + 1) / args.search_chunks)) + 1
+                   for c in range(max(args.search_chunks, 1) - 1)} - {0, nl})
+    chunks = list(zip([0] + cuts, cuts + [nl]))
+    sb_chunks = [cham.SearchBatch(Ws[a:b], wqs[a:b]) for a, b in chunks]
     tbatch = cham.StatsBatch(Xs, list(range(nl)), [bucket] * nl, stats)
     st_s, sc_s, lut_s = stats.struct(), sched.struct(), lut.struct()
     aq_s = [a.struct() for a in aqs]
     Fh = ctypes.c_void_p(lut.F_host.data_ptr())
     qsb = cham.QuantStatsBatch(Xs, list(range(nl)), aqs, lut, stats)
     ev = {k: [] for k in ("search", "gemm", "layer")}
-    prev_end = [None]
+    prev_done = [None] * len(chunks)
     f_copied = [None]
 
     def step(record=False, per_layer_events=False):
-        if prev_end[0] is not None:
-            side.wait_event(prev_end[0])
+        searched = []
+        for c, (a, b) in enumerate(chunks):
+            if prev_done[c] is not None:
+                side.wait_event(prev_done[c])
+            if record and c == 0:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e0.record(side)
+            sbc = sb_chunks[c]
+            rc = L.cham_select_weight_formats_batch(sbc.ptrs, sbc.structs, b - a, S_side)
+            assert rc == 0, rc
+            searched.append(torch.cuda.Event(enable_timing=record and c == len(chunks) - 1))
+            searched[-1].record(side)
         if record:
-            e0 = torch.cuda.Event(enable_timing=True)
-            e0.record(side)
-        rc = L.cham_select_weight_formats_batch(sbatch.ptrs, sbatch.structs, nl, S_side)
-        assert rc == 0, rc
-        searched = torch.cuda.Event(enable_timing=record)
-        searched.record(side)
-        if record:
-            ev["search"].append((e0, searched))
+            ev["search"].append((e0, searched[-1]))
         if f_copied[0] is not None:
             f_copied[0].synchronize()  # the formats of the LUT the previous step built
         rc = L.cham_quantize_act_lut_accumulate_batch(qsb.ptrs, qsb.layer, nl, args.t, ctypes.byref(qsb.l), Fh,
@@ -196,21 +213,25 @@ def main():
         lut.F_host.copy_(lut.F, non_blocking=True)
         f_copied[0] = torch.cuda.Event()
         f_copied[0].record(stream)
-        stream.wait_event(searched)
+        # the per-layer breakdown times the GEMMs alone: every chunk's search first
+        for e in (searched if per_layer_events else searched[:1]):
+            stream.wait_event(e)
         if record:
             e2 = torch.cuda.Event(enable_timing=True)
             e2.record(stream)
         marks = [e2] if record else []
-        for li in range(nl):
-            rc = L.cham_mixed_linear(ctypes.byref(qsb.aq[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
-                                     ws_lin.numel(), S)
-            assert rc == 0, rc
-            if per_layer_events and li + 1 < nl:
-                marks.append(torch.cuda.Event(enable_timing=True))
-                marks[-1].record(stream)
-        end = torch.cuda.Event(enable_timing=record)
-        end.record(stream)
-        prev_end[0] = end
+        for c, (a, b) in enumerate(chunks):
+            stream.wait_event(searched[c])
+            for li in range(a, b):
+                rc = L.cham_mixed_linear(ctypes.byref(qsb.aq[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
+                                         ws_lin.numel(), S)
+                assert rc == 0, rc
+                if per_layer_events and li + 1 < nl:
+                    marks.append(torch.cuda.Event(enable_timing=True))
+                    marks[-1].record(stream)
+            prev_done[c] = torch.cuda.Event(enable_timing=record and c == len(chunks) - 1)
+            prev_done[c].record(stream)
+        end = prev_done[-1]
         if per_layer_events:
             marks.append(end)
             ev["layer"].append(list(zip(marks[:-1], marks[1:])))
@@ -224,7 +245,7 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
-    prev_end[0] = t0
+    prev_done[:] = [t0] * len(chunks)
     for _ in range(args.steps):
         step(record=True)
     t1.record(stream)
@@ -272,6 +293,16 @@ def main():
     nweights = sum(N * K for (_, K, N, _) in layers)
     search_gbps = sb / (ms_search * 1e-3) / 1e9
     del wq_np, nb_search
+
+    # ---- the step's 280 GEMMs alone (nothing beside them on the chip), for comparison with
+    # their time inside the step, where the next chunk's search shares the chip with them
+    def gemms():
+        for li in range(nl):
+            rc = L.cham_mixed_linear(ctypes.byref(qsb.aq[li]), ctypes.byref(wq_s[li]), P(Ys[li]), P(ws_lin),
+                                     ws_lin.numel(), S)
+            assert rc == 0, rc
+    ms_gemm_alone = time_calls(gemms, stream)
+    gemm_alone_tflops = total_flops / (ms_gemm_alone * 1e-3) / 1e12
 
     # ---- the activation side's parts, each timed alone on the launch stream: the step's
     # fused pass (4 B read + 1 B written per element, + 1/32 B of E8M0 for MX formats), the
@@ -341,7 +372,7 @@ def main():
                                "M=2048; CFG batch 2), one sampler step of the 50-step sweep, W4 per-channel, A8 LUT "
                                "B=10 scaled-linear T=1000",
                    "linears": nl, "weights": nweights, "gemm_tflop_per_step": round(total_flops / 1e12, 3),
-                   "timestep": args.t, "bucket": bucket,
+                   "timestep": args.t, "bucket": bucket, "search_chunks": len(chunks),
                    "act_format_hist": {cham.A_NAMES[i]: int(afh[i]) for i in range(5) if afh[i]},
                    "weight_format_hist": {cham.W_NAMES[i]: int(hist[i]) for i in range(9) if hist[i]}},
         "gemm_tflops": round(gemm_tflops, 3),
@@ -359,6 +390,10 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": F16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / F16_PEAK_TFLOPS, 4),
                      "traffic": committed_traffic(),
+                     "alone": {"ms": round(ms_gemm_alone, 4), "achieved": round(gemm_alone_tflops, 3),
+                               "frac": round(gemm_alone_tflops / F16_PEAK_TFLOPS, 4),
+                               "what": "the same 280 calls with nothing else on the chip (HIP events over 3 "
+                                       "passes after the timed steps)"},
                      "per_layer": {"kinds": per_kind,
                                    "what": f"{args.layer_steps} untimed steps with an event between the GEMM calls "
                                            "(each adds a launch gap of about 2-3 us); t_roof = max(2MNK / f16 MFMA "

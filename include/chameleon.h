@@ -153,6 +153,17 @@ size_t cham_packed_bytes(int64_t N, int64_t K);
  * Errors: as cham_select_weight_formats, CHAM_EINVAL also for NULL arrays or nlayers < 1. */
 int cham_select_weight_formats_batch(const float* const* W, cham_wq* wq, int32_t nlayers, void* stream);
 
+/* The packing step of the search on its own: writes wq[i].packed for n weights whose
+ * fmt, codes, scale, zero, NF4 absmax and E8M0 a search (with packed = NULL) has already
+ * filled, with code_bits as that search set it; perm, group_off and err are not touched.
+ * The layout is the bits the search writes when it packs.  It lets a caller pack one group
+ * of layers on another stream while the search of the next group runs.  wq: host array of
+ * n descriptors.  Every descriptor is checked before anything is launched.  Errors:
+ * CHAM_EINVAL (NULL arrays or buffers, n < 1, packed not 256-byte aligned, code_bits not
+ * that of the palette), CHAM_EFORMAT (mask), CHAM_ESHAPE (K not a multiple of 64, or
+ * K > 8192), CHAM_EHIP. */
+int cham_pack_weights_batch(const cham_wq* wq, int32_t n, void* stream);
+
 /* ---------------------------------------------------------------------------------------
  * 1b. DiT joint (group size, format) weight search (Sec. 4.6 (i))
  *

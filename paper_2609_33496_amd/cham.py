@@ -89,6 +89,7 @@ def lib():
     L.cham_version.restype = ctypes.c_int
     L.cham_select_weight_formats.argtypes = [_P, ctypes.POINTER(_WQ), _P]
     L.cham_select_weight_formats_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(_WQ), i32, _P]
+    L.cham_pack_weights_batch.argtypes = [ctypes.POINTER(_WQ), i32, _P]
     L.cham_act_stats_reset.argtypes = [ctypes.POINTER(_Stats), _P]
     L.cham_act_stats_accumulate.argtypes = [_P, i64, i32, i32, ctypes.POINTER(_Stats), _P, sz, _P]
     L.cham_act_stats_accumulate_batch.argtypes = [ctypes.POINTER(_P), ctypes.POINTER(i64), ctypes.POINTER(i32),
@@ -121,7 +122,8 @@ def lib():
     L.cham_packed_bytes.argtypes = [i64, i64]
     L.cham_packed_bytes.restype = sz
     L.cham_linear_plan.argtypes = [i64, i64, i64, i32, ctypes.POINTER(ctypes.c_int32), i32]
-    for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_act_stats_reset", "cham_act_stats_accumulate",
+    for name in ("cham_select_weight_formats", "cham_select_weight_formats_batch", "cham_pack_weights_batch",
+                 "cham_act_stats_reset", "cham_act_stats_accumulate",
                  "cham_act_stats_accumulate_batch",
                  "cham_build_act_lut", "cham_quantize_act", "cham_quantize_act_lut", "cham_quantize_act_noalloc",
                  "cham_quantize_act_lut_accumulate_batch",
@@ -290,6 +292,31 @@ class SearchBatch:
                "select_weight_formats_batch")
         for o, st in zip(self.outs, self.structs):
             o.code_bits = st.code_bits
+
+
+class PackBatch:
+    """Prepared C arguments of the packing step on its own for several searched weights
+    (their descriptors, each with a packed buffer), reusable across calls."""
+
+    def __init__(self, wqs, packed):
+        assert len(wqs) == len(packed) and len(wqs) > 0
+        self.wqs = list(wqs)
+        structs = []
+        for w, buf in zip(wqs, packed):
+            st = w.struct()
+            st.packed = _ptr(buf)
+            st.perm = st.group_off = st.err = None
+            structs.append(st)
+        self.packed = list(packed)
+        self.structs = (_WQ * len(structs))(*structs)
+
+    def run(self, stream=None):
+        _check(lib().cham_pack_weights_batch(self.structs, len(self.wqs), _stream(stream)), "pack_weights_batch")
+
+
+def pack_weights_batch(wqs, stream=None):
+    """Write the packed layout of searched weights (each wq.packed set) on its own."""
+    PackBatch(wqs, [w.packed for w in wqs]).run(stream)
 
 
 def select_weight_formats_batch(Ws, mask: int = MASK_W4, outs=None, want_perm=True, want_err=False,

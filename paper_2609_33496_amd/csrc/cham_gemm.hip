@@ -37,6 +37,7 @@
 // byte those 8 values come in the order (0,4,1,5,2,6,3,7); the activation operand is
 // staged with its columns in that same order.
 #include <atomic>
+#include <vector>
 
 #include "cham_device.h"
 #include "cham_group.h"
@@ -1167,10 +1168,10 @@ static void launch_records(const WView& v, const Layout& L, hipStream_t s) {
     hipLaunchKernelGGL(record_kernel, dim3((unsigned)wgs), dim3(256), 0, s, B);
 }
 
-// Writes the packed layout of n searched weights (called by the search entry points, which
-// have checked the arguments and set code_bits), and groups the channels of those that ask
-// for perm / group_off; one launch per kRecBatchMax weights.
-int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
+// Writes the packed layout of n searched weights (the arguments checked and code_bits set),
+// and with `group` also groups the channels of those that ask for perm / group_off; one
+// launch per kRecBatchMax weights.
+static int pack_weights(const cham_wq* const* wqs, int n, bool group, hipStream_t s) {
     for (int i0 = 0; i0 < n; i0 += kRecBatchMax) {
         RecBatch B;
         B.nl = std::min(kRecBatchMax, n - i0);
@@ -1182,12 +1183,36 @@ int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) {
             B.r[j] = record_args(view_of(wq), layout_at(wq->packed, wq->N, wq->K), &wgs);
             total += wgs;
             B.wg_end[j] = total;
-            if (wq->perm || wq->group_off) B.g[B.ng++] = GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off};
+            if (group && (wq->perm || wq->group_off))
+                B.g[B.ng++] = GroupArgs{wq->fmt, (int)wq->N, wq->perm, wq->group_off};
         }
         hipLaunchKernelGGL(record_kernel, dim3((unsigned)(total + B.ng)), dim3(256), 0, s, B);
         CHAM_CHECK_LAUNCH();
     }
     return CHAM_OK;
+}
+
+// The search entry points' packing step (they have checked the arguments and set code_bits).
+int cham_pack_weights(const cham_wq* const* wqs, int n, hipStream_t s) { return pack_weights(wqs, n, true, s); }
+
+extern "C" int cham_pack_weights_batch(const cham_wq* wq, int32_t n, void* stream) {
+    if (!wq || n < 1) return CHAM_EINVAL;
+    std::vector<const cham_wq*> p((size_t)n);
+    for (int i = 0; i < n; ++i) {
+        const cham_wq& w = wq[i];
+        if (!w.fmt || !w.codes || !w.scale || !w.zero || !w.packed || w.N < 1) return CHAM_EINVAL;
+        if ((uintptr_t)w.packed & 255u) return CHAM_EINVAL;
+        const uint32_t mask = w.palette_mask;
+        if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
+        if (w.code_bits != ((mask & 0x7u) ? 8 : 4)) return CHAM_EINVAL;
+        if (w.K < 64 || w.K % 64 != 0 || w.K > 8192) return CHAM_ESHAPE;
+        if (((mask >> CHAM_W_NF4) & 1u) && !w.nf4_absmax) return CHAM_EINVAL;
+        if ((mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) && !w.e8m0)
+            return CHAM_EINVAL;
+        if (w.N * (w.K / 64) * 128 > (int64_t)INT32_MAX) return CHAM_EINVAL;
+        p[(size_t)i] = &w;
+    }
+    return pack_weights(p.data(), n, false, (hipStream_t)stream);
 }
 
 // The packed layout of a group-scaled weight (called by the grouped search after its

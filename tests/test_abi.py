@@ -84,6 +84,30 @@ def test_select_weight_formats_batch_argument_errors():
     assert L.cham_select_weight_formats_batch(nullw, (cham._WQ * 1)(good), 1, None) == cham.EINVAL
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(packed=None), cham.EINVAL),
+    (dict(packed=272), cham.EINVAL),          # 256-byte aligned
+    (dict(code_bits=0), cham.EINVAL),         # the searched code width
+    (dict(code_bits=8), cham.EINVAL),
+    (dict(K=96), cham.ESHAPE),
+    (dict(K=8256), cham.ESHAPE),
+    (dict(palette_mask=0), cham.EFORMAT),
+    (dict(nf4_absmax=None), cham.EINVAL),
+    (dict(palette_mask=1 << cham.W_MXFP4, e8m0=None), cham.EINVAL),
+    (dict(scale=None), cham.EINVAL),
+])
+def test_pack_weights_batch_argument_errors(kw, status):
+    """Every descriptor is checked before the packing launch: a bad one anywhere in the array
+    fails the call with nothing launched."""
+    L = cham.lib()
+    good = _wq(code_bits=4, packed=256)
+    bad = _wq(**{"code_bits": 4, "packed": 256, **kw})
+    assert L.cham_pack_weights_batch((cham._WQ * 2)(good, bad), 2, None) == status
+    assert L.cham_pack_weights_batch((cham._WQ * 1)(bad), 1, None) == status
+    assert L.cham_pack_weights_batch((cham._WQ * 1)(good), 0, None) == cham.EINVAL
+    assert L.cham_pack_weights_batch(None, 1, None) == cham.EINVAL
+
+
 def test_other_argument_errors():
     L = cham.lib()
     st = cham._Stats(2, 3, ctypes.c_void_p(16), ctypes.c_void_p(16))

@@ -216,6 +216,49 @@ def test_search_batch_matches_single_calls():
                 assert torch.equal(x, y), (i, name)
 
 
+def test_pack_batch_matches_packing_search():
+    """Packing on its own after a search that wrote no layout (in chunks, on a second stream
+    that waits for the search) gives the bytes the packing search writes, for 40 layers of
+    mixed shapes and palettes (more than one packing launch takes)."""
+    shapes = [(37, 640), (300, 1280), (24, 4608), (9, 5120), (5, 8192), (3, 64), (4100, 256), (1280, 1280),
+              (64, 5120), (130, 2048)]
+    masks = [oracle.MASK_W4, oracle.MASK_W8, 0x1FF, (1 << oracle.W_NF4) | (1 << oracle.W_MXFP4),
+             (1 << oracle.W_INT8_ASYM) | (1 << oracle.W_MXINT8)]
+    Ws, plain, packing = [], [], []
+    for i in range(40):
+        N, K = shapes[i % len(shapes)]
+        m = masks[i % len(masks)]
+        W, _ = synth.hetero_weights(900 + i, N, K)
+        Ws.append(torch.from_numpy(W).to(DEV))
+        a = cham.alloc_wq(N, K, m, DEV, want_perm=(i % 2 == 0))
+        a.packed = torch.zeros(cham.packed_bytes(N, K), dtype=torch.uint8, device=DEV)
+        b = cham.alloc_wq(N, K, m, DEV, want_perm=(i % 2 == 0), want_packed=True)
+        b.packed.zero_()
+        plain.append(a)
+        packing.append(b)
+    case("select_weight_formats_batch 40 layers, packing alone in chunks on a second stream")
+    bufs = [a.packed for a in plain]
+    for a in plain:
+        a.packed = None
+    cham.SearchBatch(Ws, plain).run()
+    for a, buf in zip(plain, bufs):
+        a.packed = buf
+    done = torch.cuda.Event()
+    done.record()
+    side = torch.cuda.Stream()
+    side.wait_event(done)
+    for c in range(0, 40, 13):
+        cham.PackBatch(plain[c:c + 13], bufs[c:c + 13]).run(side)
+    cham.select_weight_formats_batch(Ws, outs=packing)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(plain, packing)):
+        for name in ("fmt", "codes", "scale", "zero", "nf4_absmax", "e8m0", "perm", "group_off", "packed"):
+            x, y = getattr(a, name), getattr(b, name)
+            assert (x is None) == (y is None), (i, name)
+            if x is not None:
+                assert torch.equal(x, y), (i, name)
+
+
 def test_search_grouping_repeated_and_partial_outputs():
     """Repeated calls on one output object, a different matrix in between, and calls that
     request only perm or only group_off all give the stable sort of the formats."""
