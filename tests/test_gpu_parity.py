@@ -640,6 +640,9 @@ def test_linear_full_size_sampled():
     (240, 1152, 4096, oracle.MASK_W4, cham.A_FP8_E4M3),    # PixArt-like cross-attn KV: 240 rows, 8 k-splits
     (4096, 5120, 640, oracle.MASK_W4, cham.A_INT8_ASYM),   # 640-wide GEGLU at 4096 tokens
     (1024, 1280, 5120, oracle.MASK_W4, cham.A_FP8_E5M2),   # 1280-wide FF-out at 1024 tokens
+    (2048, 1280, 5120, oracle.MASK_W4, cham.A_INT8_ASYM),  # the sweep's FF-out: 3 k-splits, XCD-aware order
+    (1300, 2000, 4096, oracle.MASK_W8, cham.A_INT8_ASYM),  # XCD-aware order over 11 x 16 tiles, ragged M and N
+    (1300, 2000, 4096, oracle.MASK_W4, cham.A_MXFP8),      # the same with MX activations
 ])
 def test_linear_plans_sampled(M, N, K, mask, afmt):
     """Tile heights, k-splits and two-launch plans the sizes above select (each code width,
