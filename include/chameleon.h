@@ -161,7 +161,7 @@ int cham_select_weight_formats_batch(const float* const* W, cham_wq* wq, int32_t
  * n descriptors.  Every descriptor is checked before anything is launched.  Errors:
  * CHAM_EINVAL (NULL arrays or buffers, n < 1, packed not 256-byte aligned, code_bits not
  * that of the palette), CHAM_EFORMAT (mask), CHAM_ESHAPE (K not a multiple of 64, or
- * K > 8192), CHAM_EHIP. */
+ * K > 2^20), CHAM_EHIP. */
 int cham_pack_weights_batch(const cham_wq* wq, int32_t n, void* stream);
 
 /* ---------------------------------------------------------------------------------------

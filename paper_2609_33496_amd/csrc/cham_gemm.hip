@@ -1249,7 +1249,7 @@ extern "C" int cham_pack_weights_batch(const cham_wq* wq, int32_t n, void* strea
         const uint32_t mask = w.palette_mask;
         if (mask == 0u || (mask >> CHAM_W_NFMT) != 0u) return CHAM_EFORMAT;
         if (w.code_bits != ((mask & 0x7u) ? 8 : 4)) return CHAM_EINVAL;
-        if (w.K < 64 || w.K % 64 != 0 || w.K > 8192) return CHAM_ESHAPE;
+        if (w.K < 64 || w.K % 64 != 0 || w.K > (1 << 20)) return CHAM_ESHAPE;
         if (((mask >> CHAM_W_NF4) & 1u) && !w.nf4_absmax) return CHAM_EINVAL;
         if ((mask & ((1u << CHAM_W_MXINT8) | (1u << CHAM_W_MXINT4) | (1u << CHAM_W_MXFP4))) && !w.e8m0)
             return CHAM_EINVAL;
