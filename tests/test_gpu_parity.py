@@ -736,6 +736,80 @@ def test_two_streams_match_one_stream():
         assert np.array_equal(_np(ya).view(np.uint32), _np(yb).view(np.uint32))
 
 
+def test_chunked_step_schedule_matches_one_stream():
+    """The benchmark's step schedule: the search in chunks of layers on a second stream; on
+    the launch stream the fused quantize-and-moments pass with the LUT built before it, the
+    LUT rebuilt and its formats copied to the host mirror, then each chunk's GEMMs once that
+    chunk is searched; the next step's search of a chunk waits for this step's GEMMs of that
+    chunk.  New weights and inputs every step (a search that overtook the GEMMs still reading
+    its packed layout would show), three steps, the bits of the same calls on one stream."""
+    layers = [(640, 384), (1280, 256), (2560, 320), (640, 512), (1280, 384), (640, 256)]
+    chunks = [(0, 2), (2, 4), (4, 6)]
+    M, T, B, t, steps = 512, 1000, 4, 375, 3
+    nl = len(layers)
+    Ws = [[torch.from_numpy(synth.hetero_weights(70 + 10 * s + i, N, K)[0]).to(DEV) for i, (K, N) in enumerate(layers)]
+          for s in range(steps)]
+    Xs = [[torch.from_numpy(synth.diffusion_acts(4 + s, i, t, M, K)).to(DEV) for i, (K, _) in enumerate(layers)]
+          for s in range(steps)]
+    cal = [torch.from_numpy(synth.diffusion_acts(1, i, 100 + 250 * b, 64, K)).to(DEV)
+           for b in range(B) for i, (K, _) in enumerate(layers)]
+    sched = cham.Schedule(T=T)
+
+    def run(side, main):
+        wqs = [cham.alloc_wq(N, K, cham.MASK_W4, DEV, want_perm=True, want_packed=True) for (K, N) in layers]
+        for w in wqs:
+            w.packed.zero_()
+        st = cham.alloc_stats(nl, B, DEV)
+        cham.act_stats_reset(st, stream=main)
+        cham.act_stats_accumulate_batch(cal, [i for _ in range(B) for i in range(nl)],
+                                        [b for b in range(B) for _ in range(nl)], st, stream=main)
+        lut = cham.build_act_lut(st, sched, stream=main)
+        torch.cuda.synchronize()
+        lut.F_host = torch.empty(lut.F.numel(), dtype=torch.uint8, pin_memory=True)
+        lut.F_host.copy_(lut.F)
+        aqs = [cham.alloc_aq(M, K, DEV) for (K, _) in layers]
+        Ys = [[torch.empty((M, N), dtype=torch.float32, device=DEV) for (_, N) in layers] for _ in range(steps)]
+        done = [None] * len(chunks)
+        copied = None
+        for s in range(steps):
+            searched = []
+            for c, (a, b) in enumerate(chunks):
+                if done[c] is not None:
+                    side.wait_event(done[c])
+                cham.SearchBatch(Ws[s][a:b], wqs[a:b]).run(stream=side)
+                searched.append(torch.cuda.Event())
+                searched[-1].record(side)
+            if copied is not None:
+                copied.synchronize()
+            with torch.cuda.stream(main):
+                cham.QuantStatsBatch(Xs[s], list(range(nl)), aqs, lut, st).run(t, stream=main)
+                cham.build_act_lut(st, sched, out=lut, stream=main)
+                lut.F_host.copy_(lut.F, non_blocking=True)
+                copied = torch.cuda.Event()
+                copied.record(main)
+            for c, (a, b) in enumerate(chunks):
+                main.wait_event(searched[c])
+                for i in range(a, b):
+                    cham.mixed_linear(aqs[i], wqs[i], Ys[s][i], stream=main)
+                done[c] = torch.cuda.Event()
+                done[c].record(main)
+        torch.cuda.synchronize()
+        return wqs, st, Ys
+
+    cur = torch.cuda.current_stream()
+    case("chunked step schedule on one stream")
+    ref = run(cur, cur)
+    case("chunked step schedule on two streams")
+    two = run(torch.cuda.Stream(), cur)
+    for wa, wb in zip(ref[0], two[0]):
+        assert np.array_equal(_np(wa.fmt), _np(wb.fmt))
+        assert np.array_equal(_np(wa.packed), _np(wb.packed))
+    assert np.array_equal(_np(ref[1].nS), _np(two[1].nS))
+    for s in range(steps):
+        for ya, yb in zip(ref[2][s], two[2][s]):
+            assert np.array_equal(_np(ya).view(np.uint32), _np(yb).view(np.uint32)), s
+
+
 @pytest.mark.parametrize("mask", [oracle.MASK_W4, oracle.MASK_W8])
 @pytest.mark.parametrize("N,K", [(12, 17280), (6, 23040), (5, 32768), (3, 8256)])
 def test_search_long_rows(mask, N, K):
