@@ -19,7 +19,9 @@
  *   - Every pointer inside a descriptor or passed as a buffer is DEVICE memory unless its
  *     comment says "host".  The caller owns every buffer; the library allocates nothing and
  *     keeps no mutable global state beyond a per-device cache of the CU count (filled once,
- *     atomically).  Calls are thread-safe.
+ *     atomically) and, for cham_quantize_act_noalloc only, an 8 KB device array per GPU
+ *     with its address (see there).  Calls are thread-safe, except that calls of
+ *     cham_quantize_act_noalloc that overlap on one GPU share that array.
  *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only enqueues work
  *     on that stream and returns without synchronizing.
  *   - Argument errors are detected on the host and returned synchronously before anything is
