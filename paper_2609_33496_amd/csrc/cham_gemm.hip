@@ -575,7 +575,7 @@ CHAM_DEV uint4 decode_act8(uint32_t w0, uint32_t w1, bool perm4, half2v negz) {
 }
 
 template <int CODE_BITS, int TM, int AF, int TN>
-__global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 2 : 1) void gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kThreads, TN == 1 ? 3 : (TM == 4 && CODE_BITS == 4) ? 2 : 1) void gemm_kernel(GemmArgs a) {
     constexpr int BM = 32 * TM;
     constexpr int BN = tile_width(TN);
     constexpr int CW = CODE_BITS / 4;  // 16-byte code pieces per record
@@ -794,16 +794,18 @@ __global__ __launch_bounds__(kThreads, (TM == 4 && CODE_BITS == 4) || TN == 1 ? 
     // activation tile of step k + 1 (loaded DA steps earlier) into the other buffer and
     // issues the loads of step k + 1 + DA (activations) and k + DW (weights) into register
     // rings of DA and DW + 1 stages.  Short steps (64-row tiles) take deeper rings so the
-    // loads have more than one memory latency to arrive, and so do half-width tiles, whose
-    // layers run one or two workgroups per CU with little else to hide that latency behind
-    // (there a 4-stage weight ring was 3-7 % faster than 2 stages).  Sub-steps 0-2 run with the
+    // loads have more than one memory latency to arrive.  Half-width tiles keep 2-stage
+    // rings, which fit three workgroups per CU (at most 168 registers): with a 4-stage ring
+    // they fit two, which was 3-7 % faster than two workgroups with 2 stages, but three
+    // workgroups with 2 stages beat both (the QKV layers at 1280 4 % faster, the step 1 %,
+    // where the search shares the CUs).  Sub-steps 0-2 run with the
     // operand reads and weight decode one sub-step ahead; then one barrier makes the new
     // tile visible (and retires every read of this step's buffer), and the first operands
     // of step k + 1 are read and decoded behind the MFMAs of sub-step 3.  Step indices past
     // the end are clamped (harmless reloads); scheduling barriers keep the compiler from
     // sinking the reads next to their uses.  The loop is unrolled by a multiple of both
     // ring lengths and of the two LDS buffers, so every ring and buffer index is a constant.
-    constexpr int DW = TM == 2 || TN == 1 ? 3 : 1;
+    constexpr int DW = TM == 2 ? 3 : 1;
     constexpr int DA = TM == 2 ? 2 : 1;
     constexpr int U = (DW + 1) > 2 ? (DW + 1) : 2;
     static_assert(U % DA == 0 && U % 2 == 0, "the unrolled steps must repeat every ring and buffer index");
@@ -977,7 +979,9 @@ int cu_count() {
 // fixed cost (prologue, output write) per launch -- the workgroups of later rounds start
 // while earlier ones finish -- plus the k-steps of the rounds of workgroups.  Tiles 128 high
 // fit two workgroups on a CU; a round that shares the CUs runs at the slower shared step.
-// The half-width tile (128 x 128) is for layers whose full-width tiles cannot fill the CUs.
+// The half-width tile (128 x 128) is for layers whose full-width tiles cannot fill the CUs;
+// its kernel fits three workgroups on a CU, but the model counts two (its step costs were
+// fitted with two sharing a CU, and those layers launch fewer workgroups than two per CU).
 struct TileCost {
     int bm, tn, occ;             // tile height, 32-channel blocks per wavefront, workgroups per CU
     double step1, step2, fixed;  // us: k-step alone on the CU, k-step sharing it, per launch
