@@ -977,26 +977,29 @@ int cu_count() {
 
 // Modeled time (us) of a launch of one tile shape, fitted to measurements on MI355X: one
 // fixed cost (prologue, output write) per launch -- the workgroups of later rounds start
-// while earlier ones finish -- plus the k-steps of the rounds of workgroups.  Tiles 128 high
-// fit two workgroups on a CU; a round that shares the CUs runs at the slower shared step.
-// The half-width tile (128 x 128) is for layers whose full-width tiles cannot fill the CUs;
-// its kernel fits three workgroups on a CU, but the model counts two (its step costs were
-// fitted with two sharing a CU, and those layers launch fewer workgroups than two per CU).
+// while earlier ones finish -- plus the k-steps of the rounds of workgroups, each at the
+// k-step time of as many workgroups per CU as the round puts there.  Tiles 128 high fit two
+// workgroups on a CU, the half-width tile (128 x 128) three.
 struct TileCost {
-    int bm, tn, occ;             // tile height, 32-channel blocks per wavefront, workgroups per CU
-    double step1, step2, fixed;  // us: k-step alone on the CU, k-step sharing it, per launch
+    int bm, tn, occ;                   // tile height, 32-channel blocks per wavefront, workgroups per CU
+    double step1, step2, step3, fixed;  // us: k-step with 1, 2, 3 workgroups on the CU; per launch
 };
 constexpr int kNumTiles = 4;
-constexpr TileCost kTileCosts[kNumTiles] = {{256, 2, 1, 2.13, 2.13, 8.0},
-                                            {128, 2, 2, 1.21, 1.89, 9.0},
-                                            {128, 1, 2, 0.715, 1.26, 6.0},
-                                            {64, 2, 1, 0.82, 0.82, 6.2}};
+constexpr TileCost kTileCosts[kNumTiles] = {{256, 2, 1, 2.13, 2.13, 2.13, 8.0},
+                                            {128, 2, 2, 1.21, 1.89, 1.89, 9.0},
+                                            {128, 1, 3, 0.715, 1.26, 1.64, 6.0},
+                                            {64, 2, 1, 0.82, 0.82, 0.82, 6.2}};
+
+double step_cost(const TileCost& c, int64_t per_cu) {
+    return per_cu <= 1 ? c.step1 : per_cu == 2 ? c.step2 : c.step3;
+}
 
 double launch_cost(int64_t wgs, int nsteps, const TileCost& c, int P) {
     if (wgs <= 0) return 0.0;
     const int64_t slots = (int64_t)c.occ * P;
     const int64_t full = wgs / slots, rem = wgs % slots;
-    return c.fixed + (double)full * nsteps * c.step2 + (rem == 0 ? 0.0 : nsteps * (rem <= P ? c.step1 : c.step2));
+    return c.fixed + (double)full * nsteps * step_cost(c, c.occ) +
+           (rem == 0 ? 0.0 : nsteps * step_cost(c, (rem + P - 1) / P));
 }
 
 struct Launch {
@@ -1025,14 +1028,15 @@ Plan plan_gemm(int M, int N, int K, int code_bits) {
     for (int b = 0; b < kNumTiles; ++b) costs[b] = kTileCosts[b];
     if (code_bits != 4) {  // the full-width 128-high tile with 8-bit codes: one per CU
         costs[1].occ = 1;
-        costs[1].step2 = costs[1].step1;
+        costs[1].step2 = costs[1].step3 = costs[1].step1;
     }
-    // half-width tiles only where the full-width ones leave CUs idle
-    const bool narrow = (int64_t)((M + 127) / 128) * col_tiles(N, 2) < P;
+    // half-width tiles: with 4-bit codes wherever the model prefers them; with 8-bit codes
+    // (the costs are fitted on 4-bit codes) only where the full-width tiles leave CUs idle
+    const bool half_ok = code_bits == 4 || (int64_t)((M + 127) / 128) * col_tiles(N, 2) < P;
     double best = 1e300;
     Plan plan{1, 1, {Launch{0, M, 64, 2}, Launch{0, 0, 0, 0}}};
     for (int b = 0; b < kNumTiles; ++b) {
-        if (costs[b].tn == 1 && !narrow) continue;
+        if (costs[b].tn == 1 && !half_ok) continue;
         const int tn = col_tiles(N, costs[b].tn);
         for (int sp = 1; sp <= kMaxSplits && sp <= nsteps; ++sp) {
             const int kchunk = (nsteps + sp - 1) / sp;
@@ -1044,7 +1048,7 @@ Plan plan_gemm(int M, int N, int K, int code_bits) {
     }
     // one tile shape for whole rounds of full tile rows, another for the rows left
     for (int b = 0; b < kNumTiles; ++b) {
-        if (costs[b].tn == 1 && !narrow) continue;
+        if (costs[b].tn == 1 && !half_ok) continue;
         const TileCost& c1 = costs[b];
         const int tn1 = col_tiles(N, c1.tn);
         const int rows_per_round = (c1.occ * P / tn1) * c1.bm;
@@ -1052,7 +1056,7 @@ Plan plan_gemm(int M, int N, int K, int code_bits) {
         const int r1 = (M / rows_per_round) * rows_per_round;
         if (r1 <= 0 || r1 >= M) continue;
         for (int b2 = 0; b2 < kNumTiles; ++b2) {
-            if (b2 == b || (costs[b2].tn == 1 && !narrow)) continue;
+            if (b2 == b || (costs[b2].tn == 1 && !half_ok)) continue;
             const TileCost& c2 = costs[b2];
             const double c = launch_cost((int64_t)(r1 / c1.bm) * tn1, nsteps, c1, P) +
                              launch_cost((int64_t)((M - r1 + c2.bm - 1) / c2.bm) * col_tiles(N, c2.tn), nsteps, c2, P);
