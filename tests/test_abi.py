@@ -168,7 +168,7 @@ def test_linear_plans_are_valid():
                         assert ls[0]["rows"][1] == ls[1]["rows"][0] and p["splits"] == 1, p
                     for l in ls:
                         assert l["rows"][0] < l["rows"][1], p
-                        assert l["tile"] in ((256, 256), (128, 256), (128, 128), (64, 256)), p
+                        assert l["tile"] in ((256, 256), (128, 256), (128, 128), (64, 256), (64, 128)), p
                     steps, sp = K // 64, p["splits"]
                     assert 1 <= sp <= 8, p
                     chunk = -(-steps // sp)

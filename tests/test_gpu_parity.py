@@ -635,7 +635,9 @@ def test_linear_full_size_sampled():
     (3000, 4000, 1280, oracle.MASK_W8, cham.A_MXFP8),      # 8-bit codes, 256-row tiles, MX activations
     (3000, 4000, 1280, oracle.MASK_W4, cham.A_MXINT8),     # 128-row tiles, MX activations
     (8192, 4608, 1152, oracle.MASK_W8, cham.A_FP8_E4M3),   # two launches: 256-row then 128-row tiles
-    (1000, 1000, 1280, oracle.MASK_W4, cham.A_FP8_E4M3),   # half-width tiles, 4 k-splits, ragged M and N
+    (1000, 1000, 1280, oracle.MASK_W4, cham.A_FP8_E4M3),   # 64 x 128 tiles, ragged M and N
+    (1024, 1280, 1280, oracle.MASK_W4, cham.A_FP8_E5M2),   # 64 x 128 tiles: the single-step out-projection
+    (1040, 1200, 1216, oracle.MASK_W4, cham.A_MXINT8),     # 64 x 128 tiles, MX activations, ragged M and N
     (700, 777, 1280, oracle.MASK_W8, cham.A_INT8_ASYM),    # half-width tiles, 8-bit codes, 5 k-splits
     (240, 1152, 4096, oracle.MASK_W4, cham.A_FP8_E4M3),    # PixArt-like cross-attn KV: 240 rows, 8 k-splits
     (4096, 5120, 640, oracle.MASK_W4, cham.A_INT8_ASYM),   # 640-wide GEGLU at 4096 tokens
